@@ -1,0 +1,188 @@
+"""Prefix-cache bookkeeping oracle (test infrastructure only).
+
+Follows the paper's description of the reuse plane: KV memory is managed in
+fixed-size blocks addressed through a per-request block table (Section 2,
+PagedAttention's virtual-memory-inspired KV layout), and Automatic Prefix
+Caching lets a request reuse the KV blocks of a matching prefix (Section 2;
+Section 3: shared policy prefixes should not be recomputed; Section 5.3: the
+system prompt, policy text and schema stay identical across many requests).
+The paper states no procedure, so the rules below are the readings recorded in
+the design notes:
+
+* a block is shareable only when it is full; its identity is the *whole* token
+  prefix up to and including it (a dict keyed by that tuple -- no hashing);
+* admission walks full blocks from the start and stops at the first prefix not
+  in the index; at most ``(L - 1) // bs`` blocks are taken from the cache so at
+  least one token is computed;
+* new blocks come from the front of a caller-ordered free list;
+* a prompt's full blocks are registered at admission, a sequence's other full
+  blocks when it is released, each only if the block before it is registered
+  and its prefix is not registered yet (the first registration wins; a
+  duplicate stays private);
+* released blocks that are registered stay cached with refcount 0 (no eviction);
+  unregistered ones return to the back of the free list;
+* truncation (rolling back draft or chunk tokens) may only drop unregistered
+  blocks; they return to the *front* of the free list, so ``extend`` followed
+  by ``truncate`` restores the pool exactly.
+"""
+from __future__ import annotations
+
+from collections import deque
+
+import numpy as np
+
+
+class OracleError(Exception):
+    code = "error"
+
+
+class ArgError(OracleError):
+    code = "arg"
+
+
+class NoBlocksError(OracleError):
+    code = "no_blocks"
+
+
+class UnknownSeqError(OracleError):
+    code = "unknown_seq"
+
+
+class PrefixCacheOracle:
+    def __init__(self, num_blocks: int, block_size: int, free_order):
+        free_order = [int(b) for b in free_order]
+        if num_blocks <= 0 or block_size <= 0:
+            raise ArgError("pool sizes must be positive")
+        if sorted(free_order) != list(range(num_blocks)):
+            raise ArgError("free_order must be a permutation of the block ids")
+        self.bs = block_size
+        self.num_blocks = num_blocks
+        self.free = deque(free_order)
+        self.index = {}          # tuple(whole token prefix) -> physical block
+        self.registered = set()  # physical blocks present in ``index``
+        self.ref = [0] * num_blocks
+        self.seqs = {}           # seq_id -> {"tokens": list, "blocks": list, "n_reg": int}
+
+    # -- helpers -----------------------------------------------------------
+    def _seq(self, seq_id):
+        if seq_id not in self.seqs:
+            raise UnknownSeqError(f"unknown sequence {seq_id}")
+        return self.seqs[seq_id]
+
+    def _register_run(self, st):
+        """Register full blocks after the sequence's registered leading run,
+        in logical order, while the chain is unbroken and the prefix is new."""
+        bs, toks, blocks = self.bs, st["tokens"], st["blocks"]
+        j = st["n_reg"]
+        while (j + 1) * bs <= len(toks):
+            key = tuple(toks[:(j + 1) * bs])
+            if key in self.index:
+                break
+            self.index[key] = blocks[j]
+            self.registered.add(blocks[j])
+            j += 1
+        st["n_reg"] = j
+
+    # -- operations ----------------------------------------------------------
+    def add(self, seq_id, tokens) -> int:
+        """Admit a sequence; return the number of tokens whose KV is reused."""
+        toks = [int(t) for t in tokens]
+        L, bs = len(toks), self.bs
+        if seq_id in self.seqs:
+            raise ArgError(f"sequence {seq_id} already exists")
+        if L < 1:
+            raise ArgError("a sequence needs at least one token")
+        hits = []
+        while (len(hits) + 1) * bs <= L - 1:
+            key = tuple(toks[:(len(hits) + 1) * bs])
+            if key not in self.index:
+                break
+            hits.append(self.index[key])
+        need = -(-L // bs) - len(hits)
+        if need > len(self.free):
+            raise NoBlocksError(f"need {need} blocks, {len(self.free)} free")
+        for b in hits:
+            self.ref[b] += 1
+        new = [self.free.popleft() for _ in range(need)]
+        for b in new:
+            self.ref[b] = 1
+        st = {"tokens": toks, "blocks": hits + new, "n_reg": len(hits)}
+        self.seqs[seq_id] = st
+        self._register_run(st)
+        return len(hits) * bs
+
+    def extend(self, seq_id, tokens):
+        st = self._seq(seq_id)
+        toks = [int(t) for t in tokens]
+        newL = len(st["tokens"]) + len(toks)
+        need = -(-newL // self.bs) - len(st["blocks"])
+        if need > len(self.free):
+            raise NoBlocksError(f"need {need} blocks, {len(self.free)} free")
+        for _ in range(need):
+            b = self.free.popleft()
+            self.ref[b] = 1
+            st["blocks"].append(b)
+        st["tokens"].extend(toks)
+
+    def truncate(self, seq_id, new_len: int):
+        st = self._seq(seq_id)
+        L = len(st["tokens"])
+        if new_len < 1 or new_len > L or new_len < st["n_reg"] * self.bs:
+            raise ArgError(f"cannot truncate to {new_len} (length {L}, "
+                           f"registered {st['n_reg'] * self.bs})")
+        keep = -(-new_len // self.bs)
+        dropped = st["blocks"][keep:]
+        for b in reversed(dropped):
+            self.ref[b] -= 1
+            assert self.ref[b] == 0 and b not in self.registered
+            self.free.appendleft(b)
+        del st["blocks"][keep:]
+        del st["tokens"][new_len:]
+
+    def free_seq(self, seq_id):
+        st = self._seq(seq_id)
+        self._register_run(st)
+        for b in st["blocks"]:
+            self.ref[b] -= 1
+            if self.ref[b] == 0 and b not in self.registered:
+                self.free.append(b)
+        del self.seqs[seq_id]
+
+    def seq_len(self, seq_id) -> int:
+        return len(self._seq(seq_id)["tokens"])
+
+    def metadata(self, seq_ids, q_lens, max_blocks_per_seq: int):
+        """Block table (padded with -1), lengths, query offsets and the slot of
+        every query token (the last ``q_lens[r]`` positions of sequence r)."""
+        seq_ids = list(seq_ids)
+        q_lens = [int(x) for x in q_lens]
+        if len(seq_ids) != len(q_lens):
+            raise ArgError("seq_ids and q_lens differ in length")
+        if len(set(seq_ids)) != len(seq_ids):
+            raise ArgError("a sequence appears twice in one batch")
+        n, bs = len(seq_ids), self.bs
+        bt = np.full((n, max_blocks_per_seq), -1, dtype=np.int32)
+        seq_lens = np.zeros(n, dtype=np.int32)
+        cu = np.zeros(n + 1, dtype=np.int32)
+        slots = []
+        for r, (sid, ql) in enumerate(zip(seq_ids, q_lens)):
+            st = self._seq(sid)
+            L = len(st["tokens"])
+            if ql < 0 or ql > L:
+                raise ArgError(f"q_len {ql} outside [0, {L}]")
+            if len(st["blocks"]) > max_blocks_per_seq:
+                raise ArgError("max_blocks_per_seq too small")
+            bt[r, :len(st["blocks"])] = st["blocks"]
+            seq_lens[r] = L
+            cu[r + 1] = cu[r] + ql
+            for t in range(L - ql, L):
+                slots.append(st["blocks"][t // bs] * bs + t % bs)
+        return {"block_table": bt, "seq_lens": seq_lens, "cu_seqlens_q": cu,
+                "slot_mapping": np.asarray(slots, dtype=np.int32)}
+
+    # -- introspection used by invariant tests --------------------------------
+    def free_list(self):
+        return list(self.free)
+
+    def blocks_of(self, seq_id):
+        return list(self._seq(seq_id)["blocks"])
