@@ -1,0 +1,213 @@
+"""Benchmark: prefix-cached paged attention on one MI355X.
+
+A step is one pass of the whole hot path over one batch of the workload:
+prefix-hit lookup and block allocation for the batch (host C++), metadata and
+launch plan (host C++), their asynchronous upload, the K/V append of the new
+tokens and the attention launch (HIP), then the batch's release/rollback.
+Default workload: suffix prefill of 64 requests against a cached 2048-token
+prefix at the Llama-3-8B attention shape (the TFLOP/s headline).  Other
+workloads: --workload decode|verify|mixed|tiny.
+
+Prints one JSON line.  ``value`` is the step throughput (prefill and mixed:
+attention TFLOP/s; decode and verify: algorithmic HBM GB/s of the step);
+``roofline`` is the attention launch alone, timed with HIP events on the
+stream it runs on; ``cpu_baseline`` is the float64 oracle on a bounded sample
+of the same launch, on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "prefix-cached paged attn: prefill TFLOP/s, decode HBM GB/s, % of peak"
+DESCRIPTIONS = {
+    "prefill": "suffix prefill: 64 requests sharing one cached 2048-token prefix, suffix "
+               "U[256,1024], causal within the suffix; 32 q / 8 kv heads, head_dim 128, "
+               "block 16, bf16 (Llama-3-8B attention shape)",
+    "decode": "decode: 256 sequences, context 2048 shared + U[256,1024] + U[1,128], 1 query "
+              "each; 32/8 heads, d128, bf16",
+    "mixed": "mixed launch: 512 requests over 4 cached prefixes 1k/2k/4k/8k (Zipf 1.1), "
+             "64 x 512-token prefill chunks + 448 decode tokens; 28/4 heads, d128, bf16",
+    "verify": "speculative verify: 32 requests, 16384 shared prefix + 4096 cached suffix, "
+              "5 causal query tokens; 64/8 heads, d128, bf16 (Llama-3-70B attention shape)",
+    "tiny": "tiny fp32: 4 requests, 128-token shared prefix, suffix U[32,64]; 8/2 heads, d64",
+}
+
+
+def cpu_baseline(wl, launch, budget_s: float = 12.0):
+    """Time the float64 oracle on the first requests of the launch until the
+    budget is spent; report its throughput in the metric's unit."""
+    from oracle.run import OracleReplay
+    from oracle.attention import gather_sequence, sequence_attention
+    from paper_2605_11232_amd import perf
+    orc = OracleReplay(wl).setup()
+    res = orc.launch(launch, attend=False)
+    md = res["meta"]
+    q = launch.q.get()
+    cu, L = md["cu_seqlens_q"], md["seq_lens"]
+    cfg = wl.cfg
+    scale = cfg.head_dim ** -0.5
+    t0 = time.perf_counter()
+    done = 0
+    flops = 0.0
+    for r in range(len(L)):
+        a, b = int(cu[r]), int(cu[r + 1])
+        if a == b:
+            continue
+        K, V = gather_sequence(orc.k_cache, orc.v_cache, md["block_table"][r], int(L[r]))
+        sequence_attention(q[a:b].astype(np.float64), K, V, scale)
+        flops += perf.attention_flops([L[r]], [0, b - a], cfg.num_q_heads, cfg.head_dim)
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    sub = {"block_table": md["block_table"][:done], "seq_lens": md["seq_lens"][:done],
+           "cu_seqlens_q": md["cu_seqlens_q"][:done + 1]}
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    return dt, done, flops, threads, sub
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="prefill", choices=list(DESCRIPTIONS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=0,
+                    help="run only this many steps without the CPU baseline (profiling)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the hot path here is a single-GPU kernel "
+              f"library; --gpus {args.gpus} is not supported (see DESIGN.md for how the "
+              f"path would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2605_11232_amd import perf, synth
+    from paper_2605_11232_amd.runtime import DeviceReplay, Staging
+
+    torch.cuda.set_device(0)
+    name = args.workload
+    W, K = args.warmup, args.steps
+    if args.profile_steps:
+        W, K = 1, args.profile_steps
+    wl = synth.workload(name, steps=W + K + 2)
+    cfg = wl.cfg
+    dev = DeviceReplay(wl).setup()
+    launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K)]
+    L0 = launches[0]
+    T = L0.total_q
+    tdt = dev.tdtype
+    q = torch.from_numpy(L0.q.get()).to("cuda", tdt)
+    k_new = torch.from_numpy(L0.k_new.get()).to("cuda", tdt)
+    v_new = torch.from_numpy(L0.v_new.get()).to("cuda", tdt)
+    out = torch.empty((T, cfg.num_q_heads, cfg.head_dim), dtype=tdt, device="cuda")
+    lse = torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device="cuda")
+    n = len(L0.seq_ids)
+    # plan size bound: tile items + single-wave items (key splits of >= 256) +
+    # split groups, plus per-XCD padding
+    max_keys = wl.max_blocks_per_seq * cfg.block_size
+    plan_words = 16 + 8 * (cfg.num_kv_heads * (T * cfg.group // 128 + n)
+                           + cfg.num_kv_heads * n * (max_keys // 256 + 2) + 64)
+    stagings = [Staging("cuda", n, wl.max_blocks_per_seq, T, plan_words) for _ in range(2)]
+    stream = torch.cuda.current_stream()
+
+    def step(s, record=None):
+        p = dev.prepare_staged(launches[s], stagings[s % 2], q, k_new, v_new, out, lse)
+        dev.append(p)
+        if record is not None:
+            record[0].record(stream)
+        dev.attend(p)
+        if record is not None:
+            record[1].record(stream)
+        dev.finish(launches[s])
+        return p
+
+    for s in range(W):
+        p = step(s)
+    torch.cuda.synchronize()
+    meta = p.meta if W else None
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        p = step(W + i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    meta = {k: np.array(v, copy=True) for k, v in p.meta.items()}
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
+
+    flops = perf.attention_flops(meta["seq_lens"], meta["cu_seqlens_q"], cfg.num_q_heads,
+                                 cfg.head_dim)
+    attn_bytes = perf.attention_bytes(meta, cfg, unique=True)
+    logical_bytes = perf.attention_bytes(meta, cfg, unique=False)
+    app_bytes = perf.append_bytes(T, cfg)
+    ms = wall / K * 1e3
+    compute_bound = name in ("prefill", "mixed")
+    if cfg.dtype == "f32":
+        peak, unit, bound = perf.MI355X_PEAKS["fp32_vector_tflops"], "TFLOP/s", "alu"
+        achieved = flops / (attn_ms * 1e-3) / 1e12
+        value, vunit = flops / (ms * 1e-3) / 1e12, "TFLOP/s"
+    elif compute_bound:
+        peak, unit, bound = perf.MI355X_PEAKS["bf16_tflops"], "TFLOP/s", "mfma"
+        achieved = flops / (attn_ms * 1e-3) / 1e12
+        value, vunit = flops / (ms * 1e-3) / 1e12, "TFLOP/s"
+    else:
+        peak, unit, bound = perf.MI355X_PEAKS["hbm_gbs"], "GB/s", "hbm"
+        achieved = attn_bytes / (attn_ms * 1e-3) / 1e9
+        value, vunit = (attn_bytes + app_bytes) / (ms * 1e-3) / 1e9, "GB/s"
+
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": vunit,
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": DESCRIPTIONS[name], "name": name,
+                   "requests": len(L0.seq_ids), "query_tokens": T,
+                   "attn_flops": flops, "attn_unique_bytes": attn_bytes,
+                   "attn_logical_bytes": logical_bytes, "append_bytes": app_bytes,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": "pa_attn_" + ("prefill" if name in ("prefill", "mixed", "tiny") else name),
+                     "avg_launch_ms": round(attn_ms, 4),
+                     "effective_logical_gbs": round(logical_bytes / (attn_ms * 1e-3) / 1e9, 1)},
+    }
+    if not args.no_cpu_baseline and not args.profile_steps:
+        dt, done, cflops, threads, sub = cpu_baseline(synth.workload(name, steps=2), L0)
+        if compute_bound or cfg.dtype == "f32":
+            cval, cunit = cflops / dt / 1e12, "TFLOP/s"
+        else:
+            cval = perf.attention_bytes(sub, cfg, unique=True) / dt / 1e9
+            cunit = "GB/s"
+        rec["cpu_baseline"] = {"value": cval, "unit": cunit, "cores": threads, "kind": "oracle",
+                               "sample": f"float64 oracle attention of the first {done} of "
+                                         f"{len(L0.seq_ids)} requests of the same launch "
+                                         f"(all heads), {dt:.1f} s"}
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

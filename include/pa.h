@@ -1,0 +1,239 @@
+/*
+ * pa.h -- C ABI of libpa: prefix-cached paged attention for AMD MI355X (gfx950).
+ *
+ * The library serves requests whose prompts share long, identical prefixes
+ * (policy text, taxonomies, output schemas) followed by short per-case
+ * evidence and a short structured output (paper: Introduction; Section 3,
+ * workload phenotypes).  KV memory is held in fixed-size blocks addressed
+ * through a per-request block table (Section 2, PagedAttention), and blocks
+ * holding a matching prefix are reused instead of recomputed (Section 2,
+ * Automatic Prefix Caching; Section 3: shared policy prefixes should not be
+ * recomputed; Section 5.3).  Attention runs for suffix prefill (per-case
+ * evidence against the cached prefix plus its own causal context), decode,
+ * and speculative verification of draft tokens (Section 2 and Section 5.2,
+ * EAGLE-style speculative decoding), including chunked-prefill chunks mixed
+ * with decode tokens in one launch (Section 5.2: split prefills under a
+ * batched-token budget; Section 6, Table "playbook": long prefills blocking
+ * short decodes).
+ *
+ * Conventions
+ *  - Every function returns a pa_status (0 on success, negative on error);
+ *    pa_last_error() returns a message for the calling thread's last error.
+ *  - Host functions take host pointers.  Device functions take device
+ *    pointers owned by the caller and enqueue work on the caller's
+ *    hipStream_t (passed as void*; NULL = the default stream) without
+ *    synchronising.  The library allocates no device memory.
+ *  - Arguments are checked on the host before anything is launched; a failed
+ *    check launches nothing.  Pool operations that fail leave the pool
+ *    unchanged.
+ *  - Cache layout (both tensors contiguous, element type = dtype):
+ *      k_cache[num_blocks][num_kv_heads][block_size][head_dim]
+ *      v_cache[num_blocks][num_kv_heads][head_dim][block_size]
+ *    A token's slot is block * block_size + offset.  Values are transposed
+ *    per block so that the PV product reads keys contiguously.
+ *  - Query/output layout: q[total_q][num_q_heads][head_dim] packed by
+ *    sequence (sequence r owns rows cu_seqlens_q[r] .. cu_seqlens_q[r+1]-1,
+ *    which are its LAST q_len positions); out has q's layout and dtype;
+ *    lse[total_q][num_q_heads] is float32 natural-log log-sum-exp of the
+ *    scaled scores, or NULL.
+ *  - Query head h reads kv-head h / (num_q_heads / num_kv_heads).
+ *  - A query at logical position a sees keys 0..a (causal, bottom-right).
+ *  - Supported: block_size 16, head_dim 64 or 128, num_q_heads a multiple of
+ *    num_kv_heads; dtype PA_BF16 (MFMA path, float32 accumulation) or PA_F32
+ *    (float32 VALU path).  Integers are int32; num_blocks * block_size must
+ *    be below 2^31.
+ *  - Not thread-safe per pool; device calls on one stream are ordered.
+ */
+#ifndef PA_H_
+#define PA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PA_OK = 0,
+  PA_ERR_ARG = -1,          /* invalid argument / inconsistent sizes            */
+  PA_ERR_UNSUPPORTED = -2,  /* valid but not implemented (head_dim, dtype, ...) */
+  PA_ERR_NO_BLOCKS = -3,    /* the free list cannot satisfy an allocation       */
+  PA_ERR_UNKNOWN_SEQ = -4,  /* no live sequence with that id                    */
+  PA_ERR_LAUNCH = -5        /* the HIP runtime rejected a launch                */
+} pa_status;
+
+typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
+
+/* Message describing the calling thread's most recent error ("" if none). */
+const char* pa_last_error(void);
+/* ABI version of this header (increments on incompatible changes). */
+int32_t pa_abi_version(void);
+
+/* ------------------------------------------------------------------------ *
+ * Host block manager: prefix-hit lookup, block allocation, block tables,    *
+ * slot mapping (paper: Section 2, PagedAttention block tables and APC).     *
+ * ------------------------------------------------------------------------ */
+
+typedef struct pa_pool pa_pool; /* opaque, host memory owned by the library */
+
+/* Create a pool of num_blocks blocks of block_size tokens.  free_order is a
+ * permutation of 0..num_blocks-1 giving the order in which blocks are handed
+ * out (copied; the caller keeps ownership).  *out receives the pool. */
+int pa_pool_create(int32_t num_blocks, int32_t block_size, const int32_t* free_order,
+                   pa_pool** out);
+void pa_pool_destroy(pa_pool* pool);
+
+/* Admit sequence seq_id with its n_tokens prompt tokens.  Full blocks are
+ * matched against cached blocks from the start: block j is reused when the
+ * whole token prefix up to and including it equals a cached one; the walk
+ * stops at the first miss and never covers the last token (at most
+ * (n_tokens-1)/block_size blocks are reused).  The remaining blocks are taken
+ * from the front of the free list; the prompt's full blocks are then cached
+ * (each only if the block before it is cached and its prefix is new).
+ * *n_cached_out (may be NULL) receives the number of reused tokens.
+ * Errors: PA_ERR_ARG (duplicate id, n_tokens < 1, NULL tokens),
+ * PA_ERR_NO_BLOCKS (pool unchanged). */
+int pa_seq_add(pa_pool* pool, int64_t seq_id, const int32_t* tokens, int32_t n_tokens,
+               int32_t* n_cached_out);
+
+/* Append n_tokens tokens (decode, draft or later prefill-chunk tokens).  New
+ * blocks come from the front of the free list; nothing is cached until the
+ * sequence is freed.  Errors: PA_ERR_UNKNOWN_SEQ, PA_ERR_ARG, PA_ERR_NO_BLOCKS. */
+int pa_seq_extend(pa_pool* pool, int64_t seq_id, const int32_t* tokens, int32_t n_tokens);
+
+/* Roll sequence seq_id back to new_len tokens (rejected drafts, a chunk to
+ * redo).  Blocks no longer needed return to the FRONT of the free list, so
+ * extend followed by truncate restores the pool exactly.  new_len must be at
+ * least the number of tokens in the sequence's leading cached blocks.
+ * Errors: PA_ERR_UNKNOWN_SEQ, PA_ERR_ARG. */
+int pa_seq_truncate(pa_pool* pool, int64_t seq_id, int32_t new_len);
+
+/* Release a finished sequence.  Its full blocks are cached first (same rule as
+ * at admission); cached blocks stay resident with no owner (no eviction);
+ * uncached blocks return to the back of the free list.
+ * Errors: PA_ERR_UNKNOWN_SEQ. */
+int pa_seq_free(pa_pool* pool, int64_t seq_id);
+
+/* Current length of a live sequence.  Errors: PA_ERR_UNKNOWN_SEQ. */
+int pa_seq_len(const pa_pool* pool, int64_t seq_id, int32_t* len_out);
+
+/* Copy the physical blocks of a live sequence (logical order) into out
+ * (capacity entries); *n_out receives the count.  Errors: PA_ERR_UNKNOWN_SEQ,
+ * PA_ERR_ARG (capacity too small). */
+int pa_seq_blocks(const pa_pool* pool, int64_t seq_id, int32_t* out, int32_t capacity,
+                  int32_t* n_out);
+
+/* Copy the free list (front first) into out; *n_out receives its length. */
+int pa_pool_free_list(const pa_pool* pool, int32_t* out, int32_t capacity, int32_t* n_out);
+
+/* Build the varlen metadata of one launch over n_seqs live sequences (batch
+ * order = seq_ids order; an id may appear once).  q_lens[r] in [0, len_r]
+ * query tokens are the sequence's last q_lens[r] positions.  Outputs (host,
+ * caller-owned):
+ *   block_table[n_seqs][max_blocks_per_seq]  physical block ids, padded -1
+ *   seq_lens[n_seqs]                         sequence lengths (keys visible)
+ *   cu_seqlens_q[n_seqs+1]                   exclusive prefix sum of q_lens
+ *   slot_mapping[sum q_lens]                 slot of every query token
+ * slot_capacity is the length of slot_mapping.  Errors: PA_ERR_ARG
+ * (q_len out of range, a sequence needing more than max_blocks_per_seq blocks,
+ * repeated id, capacity too small), PA_ERR_UNKNOWN_SEQ. */
+int pa_build_metadata(const pa_pool* pool, int32_t n_seqs, const int64_t* seq_ids,
+                      const int32_t* q_lens, int32_t max_blocks_per_seq, int32_t* block_table,
+                      int32_t* seq_lens, int32_t* cu_seqlens_q, int32_t* slot_mapping,
+                      int64_t slot_capacity);
+
+/* ------------------------------------------------------------------------ *
+ * Launch plan (host).                                                        *
+ * ------------------------------------------------------------------------ */
+
+typedef enum { PA_KIND_PREFILL = 0, PA_KIND_DECODE = 1, PA_KIND_VERIFY = 2 } pa_kind;
+
+typedef struct pa_plan_info {
+  int32_t kind;            /* pa_kind the plan was built for                      */
+  int32_t n_q;             /* query tokens per sequence (decode 1, verify n_q)    */
+  int32_t n_tile_items;    /* 128-row work items (one workgroup each)             */
+  int32_t n_row_items;     /* <=48-row work items (one wavefront each)            */
+  int32_t n_groups;        /* split groups the merge step combines                */
+  int32_t n_merge_rows;    /* (token, head) rows produced by the merge step       */
+  int32_t grid;            /* workgroups of the attention launch                  */
+  int32_t variant;         /* kernel instantiation (internal)                     */
+  int64_t plan_words;      /* int32 words of the plan array                       */
+  int64_t workspace_bytes; /* device scratch the attention call needs             */
+} pa_plan_info;
+
+/* Split one attention launch into work items from HOST copies of seq_lens and
+ * cu_seqlens_q (as produced by pa_build_metadata).  With plan == NULL only
+ * *info is filled (size query).  Otherwise the int32 plan (plan_capacity
+ * words, host memory) is written; the caller copies it to device memory and
+ * passes the device copy and *info to the attention call.
+ * kind PA_KIND_DECODE requires every q_len == 1, PA_KIND_VERIFY every q_len ==
+ * n_q (1..8); PA_KIND_PREFILL takes any q_len >= 0 (prefill chunks and decode
+ * tokens may be mixed).  num_cus = compute units to fill (0: 256).
+ * Errors: PA_ERR_ARG, PA_ERR_UNSUPPORTED. */
+int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int32_t* seq_lens,
+                 const int32_t* cu_seqlens_q, int32_t num_q_heads, int32_t num_kv_heads,
+                 int32_t head_dim, int32_t block_size, int32_t dtype, int32_t num_cus,
+                 int32_t* plan, int64_t plan_capacity, pa_plan_info* info);
+
+/* ------------------------------------------------------------------------ *
+ * Device operations.                                                         *
+ * ------------------------------------------------------------------------ */
+
+/* Store the keys/values of n_tokens new tokens into their cache slots:
+ * k_cache[s/bs][h][s%bs][:] = k_new[i][h][:] and
+ * v_cache[s/bs][h][:][s%bs] = v_new[i][h][:] for s = slot_mapping[i].
+ * k_new, v_new: [n_tokens][num_kv_heads][head_dim] (dtype).  A slot outside
+ * [0, num_blocks*block_size) skips its token (use -1 for padding).
+ * Bit-exact copy.  Errors: PA_ERR_ARG, PA_ERR_UNSUPPORTED, PA_ERR_LAUNCH. */
+int pa_kv_append(const void* k_new, const void* v_new, const int32_t* slot_mapping,
+                 int32_t n_tokens, void* k_cache, void* v_cache, int32_t num_blocks,
+                 int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t dtype,
+                 void* stream);
+
+/* Paged attention over a prefix-shared KV cache.  For sequence r, q-head h
+ * and its query i at logical position a = seq_lens[r] - q_len_r + i:
+ *   out = sum_{t<=a} softmax_t(scale * q . k_t) v_t,   k_t, v_t from kv-head
+ *   h / G of the block table row r,
+ *   lse = log sum_{t<=a} exp(scale * q . k_t).
+ * Device inputs: q, caches, block_table[n_seqs][max_blocks_per_seq],
+ * seq_lens[n_seqs], cu_seqlens_q[n_seqs+1] (the same values the plan was built
+ * from), plan (device copy of pa_attn_plan's output) with its *info,
+ * workspace of at least info->workspace_bytes bytes (any contents) or NULL if
+ * that is 0.  Block ids must lie in [0, num_blocks); out-of-range ids are
+ * clamped so no access leaves the cache (results are then undefined).
+ * The three entry points differ only in the plan kind they accept.
+ * Errors: PA_ERR_ARG, PA_ERR_UNSUPPORTED, PA_ERR_LAUNCH. */
+int pa_attn_prefill(const void* q, const void* k_cache, const void* v_cache, int32_t num_blocks,
+                    const int32_t* block_table, int32_t max_blocks_per_seq,
+                    const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,
+                    int32_t total_q, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                    int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                    const pa_plan_info* info, void* workspace, size_t workspace_bytes,
+                    void* out, float* lse, void* stream);
+
+/* Decode: one query token per sequence (plan kind PA_KIND_DECODE). */
+int pa_attn_decode(const void* q, const void* k_cache, const void* v_cache, int32_t num_blocks,
+                   const int32_t* block_table, int32_t max_blocks_per_seq,
+                   const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,
+                   int32_t total_q, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                   int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                   const pa_plan_info* info, void* workspace, size_t workspace_bytes,
+                   void* out, float* lse, void* stream);
+
+/* Speculative verification: n_q = info->n_q query tokens per sequence (the
+ * draft tokens and the bonus position), causal among themselves (plan kind
+ * PA_KIND_VERIFY). */
+int pa_attn_verify(const void* q, const void* k_cache, const void* v_cache, int32_t num_blocks,
+                   const int32_t* block_table, int32_t max_blocks_per_seq,
+                   const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,
+                   int32_t total_q, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                   int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                   const pa_plan_info* info, void* workspace, size_t workspace_bytes,
+                   void* out, float* lse, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PA_H_ */

@@ -7,8 +7,8 @@ product package: it depends on numpy alone.
 
 Contents
 --------
-``apc``        Prefix-cache bookkeeping written with Python dicts keyed by the
-               whole token prefix: prefix-hit lookup, block allocation from a
+``apc``        Prefix-cache bookkeeping written with a trie of Python dicts keyed by
+               block token tuples: prefix-hit lookup, block allocation from a
                caller-ordered free list, block tables, slot mapping and varlen
                metadata (paper: Section 2 on PagedAttention's block-granular,
                virtual-memory-like KV layout and on Automatic Prefix Caching

@@ -10,9 +10,12 @@ The paper states no procedure, so the rules below are the readings recorded in
 the design notes:
 
 * a block is shareable only when it is full; its identity is the *whole* token
-  prefix up to and including it (a dict keyed by that tuple -- no hashing);
+  prefix up to and including it.  Cached blocks live in a trie of nested
+  dicts, one level per block, keyed by that block's token tuple, so a path
+  from the root spells out the full prefix (no hashing of ids, no parent
+  pointers);
 * admission walks full blocks from the start and stops at the first prefix not
-  in the index; at most ``(L - 1) // bs`` blocks are taken from the cache so at
+  in the trie; at most ``(L - 1) // bs`` blocks are taken from the cache so at
   least one token is computed;
 * new blocks come from the front of a caller-ordered free list;
 * a prompt's full blocks are registered at admission, a sequence's other full
@@ -58,8 +61,8 @@ class PrefixCacheOracle:
         self.bs = block_size
         self.num_blocks = num_blocks
         self.free = deque(free_order)
-        self.index = {}          # tuple(whole token prefix) -> physical block
-        self.registered = set()  # physical blocks present in ``index``
+        self.root = {}           # tuple(block tokens) -> [physical block, children dict]
+        self.registered = set()  # physical blocks present in the trie
         self.ref = [0] * num_blocks
         self.seqs = {}           # seq_id -> {"tokens": list, "blocks": list, "n_reg": int}
 
@@ -69,17 +72,26 @@ class PrefixCacheOracle:
             raise UnknownSeqError(f"unknown sequence {seq_id}")
         return self.seqs[seq_id]
 
+    def _children(self, toks, depth):
+        """Trie level below the first ``depth`` blocks of ``toks``."""
+        level = self.root
+        for j in range(depth):
+            level = level[tuple(toks[j * self.bs:(j + 1) * self.bs])][1]
+        return level
+
     def _register_run(self, st):
         """Register full blocks after the sequence's registered leading run,
         in logical order, while the chain is unbroken and the prefix is new."""
         bs, toks, blocks = self.bs, st["tokens"], st["blocks"]
         j = st["n_reg"]
+        level = self._children(toks, j)
         while (j + 1) * bs <= len(toks):
-            key = tuple(toks[:(j + 1) * bs])
-            if key in self.index:
+            key = tuple(toks[j * bs:(j + 1) * bs])
+            if key in level:
                 break
-            self.index[key] = blocks[j]
+            level[key] = [blocks[j], {}]
             self.registered.add(blocks[j])
+            level = level[key][1]
             j += 1
         st["n_reg"] = j
 
@@ -93,11 +105,13 @@ class PrefixCacheOracle:
         if L < 1:
             raise ArgError("a sequence needs at least one token")
         hits = []
+        level = self.root
         while (len(hits) + 1) * bs <= L - 1:
-            key = tuple(toks[:(len(hits) + 1) * bs])
-            if key not in self.index:
+            key = tuple(toks[len(hits) * bs:(len(hits) + 1) * bs])
+            if key not in level:
                 break
-            hits.append(self.index[key])
+            hits.append(level[key][0])
+            level = level[key][1]
         need = -(-L // bs) - len(hits)
         if need > len(self.free):
             raise NoBlocksError(f"need {need} blocks, {len(self.free)} free")

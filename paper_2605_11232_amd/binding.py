@@ -1,0 +1,244 @@
+"""ctypes binding of libpa (include/pa.h): argument marshalling only.
+
+Every computation runs in the C++/HIP library; this module converts numpy
+arrays and torch tensors to pointers and return codes to exceptions.  If the
+library is missing it raises -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpa.so")
+
+PA_OK, PA_ERR_ARG, PA_ERR_UNSUPPORTED, PA_ERR_NO_BLOCKS, PA_ERR_UNKNOWN_SEQ, PA_ERR_LAUNCH = (
+    0, -1, -2, -3, -4, -5)
+PA_F32, PA_BF16 = 0, 1
+KIND_PREFILL, KIND_DECODE, KIND_VERIFY = 0, 1, 2
+_CODES = {PA_ERR_ARG: "arg", PA_ERR_UNSUPPORTED: "unsupported", PA_ERR_NO_BLOCKS: "no_blocks",
+          PA_ERR_UNKNOWN_SEQ: "unknown_seq", PA_ERR_LAUNCH: "launch"}
+
+# Every symbol include/pa.h declares.
+EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy", "pa_seq_add",
+           "pa_seq_extend", "pa_seq_truncate", "pa_seq_free", "pa_seq_len", "pa_seq_blocks",
+           "pa_pool_free_list", "pa_build_metadata", "pa_attn_plan", "pa_kv_append",
+           "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify"]
+
+
+class PaError(RuntimeError):
+    def __init__(self, rc: int, msg: str):
+        super().__init__(f"[{_CODES.get(rc, rc)}] {msg}")
+        self.rc = rc
+        self.code = _CODES.get(rc, str(rc))
+
+
+class PlanInfo(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("n_q", C.c_int32), ("n_tile_items", C.c_int32),
+                ("n_row_items", C.c_int32), ("n_groups", C.c_int32), ("n_merge_rows", C.c_int32),
+                ("grid", C.c_int32), ("variant", C.c_int32), ("plan_words", C.c_int64),
+                ("workspace_bytes", C.c_int64)]
+
+
+_lib = None
+_P = C.c_void_p
+_I32P = C.POINTER(C.c_int32)
+_I64P = C.POINTER(C.c_int64)
+
+
+def lib():
+    """Load libpa.so (built in-tree by ``paper_2605_11232_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2605_11232_amd.build` (no fallback exists)")
+    L = C.CDLL(LIB_PATH)
+    i32, i64, f32 = C.c_int32, C.c_int64, C.c_float
+    sig = {
+        "pa_last_error": (C.c_char_p, []),
+        "pa_abi_version": (i32, []),
+        "pa_pool_create": (C.c_int, [i32, i32, _I32P, C.POINTER(_P)]),
+        "pa_pool_destroy": (None, [_P]),
+        "pa_seq_add": (C.c_int, [_P, i64, _I32P, i32, _I32P]),
+        "pa_seq_extend": (C.c_int, [_P, i64, _I32P, i32]),
+        "pa_seq_truncate": (C.c_int, [_P, i64, i32]),
+        "pa_seq_free": (C.c_int, [_P, i64]),
+        "pa_seq_len": (C.c_int, [_P, i64, _I32P]),
+        "pa_seq_blocks": (C.c_int, [_P, i64, _I32P, i32, _I32P]),
+        "pa_pool_free_list": (C.c_int, [_P, _I32P, i32, _I32P]),
+        "pa_build_metadata": (C.c_int, [_P, i32, _I64P, _I32P, i32, _I32P, _I32P, _I32P, _I32P, i64]),
+        "pa_attn_plan": (C.c_int, [i32, i32, i32, _I32P, _I32P, i32, i32, i32, i32, i32, i32, _I32P,
+                                   i64, C.POINTER(PlanInfo)]),
+        "pa_kv_append": (C.c_int, [_P, _P, _P, i32, _P, _P, i32, i32, i32, i32, i32, _P]),
+    }
+    attn = (C.c_int, [_P, _P, _P, i32, _P, i32, _P, _P, i32, i32, i32, i32, i32, i32, f32, i32, _P,
+                      C.POINTER(PlanInfo), _P, C.c_size_t, _P, _P, _P])
+    for name in ("pa_attn_prefill", "pa_attn_decode", "pa_attn_verify"):
+        sig[name] = attn
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != PA_OK:
+        raise PaError(rc, lib().pa_last_error().decode())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _ptr(a: np.ndarray, ctype=C.c_int32):
+    return a.ctypes.data_as(C.POINTER(ctype))
+
+
+class Pool:
+    """Host block manager (prefix-hit lookup, allocation, tables, slots)."""
+
+    def __init__(self, num_blocks: int, block_size: int, free_order):
+        self._lib = lib()
+        fo = _i32(free_order)
+        h = _P()
+        _check(self._lib.pa_pool_create(int(num_blocks), int(block_size),
+                                        _ptr(fo) if fo.size else None, C.byref(h)))
+        self._h = h
+        self.num_blocks, self.block_size = int(num_blocks), int(block_size)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._lib.pa_pool_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def add(self, seq_id: int, tokens) -> int:
+        t = _i32(tokens)
+        n = C.c_int32(0)
+        _check(self._lib.pa_seq_add(self._h, int(seq_id), _ptr(t) if t.size else None, t.size,
+                                    C.byref(n)))
+        return n.value
+
+    def extend(self, seq_id: int, tokens):
+        t = _i32(tokens)
+        _check(self._lib.pa_seq_extend(self._h, int(seq_id), _ptr(t) if t.size else None, t.size))
+
+    def truncate(self, seq_id: int, new_len: int):
+        _check(self._lib.pa_seq_truncate(self._h, int(seq_id), int(new_len)))
+
+    def free(self, seq_id: int):
+        _check(self._lib.pa_seq_free(self._h, int(seq_id)))
+
+    def seq_len(self, seq_id: int) -> int:
+        n = C.c_int32(0)
+        _check(self._lib.pa_seq_len(self._h, int(seq_id), C.byref(n)))
+        return n.value
+
+    def blocks_of(self, seq_id: int):
+        n = C.c_int32(0)
+        rc = self._lib.pa_seq_blocks(self._h, int(seq_id), None, 0, C.byref(n))
+        if rc not in (PA_OK, PA_ERR_ARG):
+            _check(rc)
+        out = np.zeros(max(1, n.value), dtype=np.int32)
+        _check(self._lib.pa_seq_blocks(self._h, int(seq_id), _ptr(out), out.size, C.byref(n)))
+        return out[:n.value].tolist()
+
+    def free_list(self):
+        n = C.c_int32(0)
+        out = np.zeros(self.num_blocks, dtype=np.int32)
+        _check(self._lib.pa_pool_free_list(self._h, _ptr(out), out.size, C.byref(n)))
+        return out[:n.value].tolist()
+
+    def metadata(self, seq_ids, q_lens, max_blocks_per_seq: int, out=None):
+        """Block table, seq_lens, cu_seqlens_q and slot_mapping (numpy int32).
+        ``out`` may supply preallocated arrays (e.g. pinned) to fill."""
+        ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
+        ql = _i32(q_lens)
+        n = ids.size
+        total = int(ql.sum()) if n else 0
+        if out is None:
+            out = {"block_table": np.empty((n, max_blocks_per_seq), np.int32),
+                   "seq_lens": np.empty(n, np.int32), "cu_seqlens_q": np.empty(n + 1, np.int32),
+                   "slot_mapping": np.empty(total, np.int32)}
+        bt, sl, cu, sm = (out["block_table"], out["seq_lens"], out["cu_seqlens_q"],
+                          out["slot_mapping"])
+        _check(self._lib.pa_build_metadata(
+            self._h, n, ids.ctypes.data_as(_I64P) if n else None, _ptr(ql) if n else None,
+            int(max_blocks_per_seq), _ptr(bt) if n else None, _ptr(sl) if n else None, _ptr(cu),
+            _ptr(sm) if sm.size else None, sm.size))
+        return out
+
+
+def plan(kind: int, n_q: int, seq_lens, cu_seqlens_q, num_q_heads: int, num_kv_heads: int,
+         head_dim: int, block_size: int, dtype: int, num_cus: int = 0, out=None):
+    """Build the launch plan on the host; returns (int32 plan array, PlanInfo).
+    ``out`` (int32 array, e.g. a pinned staging view) is used when large enough."""
+    L = lib()
+    sl, cu = _i32(seq_lens), _i32(cu_seqlens_q)
+    n = sl.size
+    info = PlanInfo()
+    args = (int(kind), int(n_q), n, _ptr(sl) if n else None, _ptr(cu), int(num_q_heads),
+            int(num_kv_heads), int(head_dim), int(block_size), int(dtype), int(num_cus))
+    _check(L.pa_attn_plan(*args, None, 0, C.byref(info)))
+    if out is not None and out.size >= info.plan_words:
+        arr = out
+    else:
+        arr = np.zeros(max(1, info.plan_words), dtype=np.int32)
+    _check(L.pa_attn_plan(*args, _ptr(arr), arr.size, C.byref(info)))
+    return arr[:info.plan_words], info
+
+
+def _dptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return PA_BF16
+    if t.dtype == torch.float32:
+        return PA_F32
+    raise PaError(PA_ERR_UNSUPPORTED, f"dtype {t.dtype}")
+
+
+def kv_append(k_new, v_new, slot_mapping, k_cache, v_cache, stream=None):
+    """Scatter new K/V ([T, Hkv, D] device tensors) into the paged cache."""
+    nb, hkv, bs, d = k_cache.shape
+    _check(lib().pa_kv_append(_dptr(k_new), _dptr(v_new), _dptr(slot_mapping),
+                              int(slot_mapping.numel()), _dptr(k_cache), _dptr(v_cache), nb, hkv,
+                              d, bs, _dtype_code(k_cache), _stream(stream)))
+
+
+def attention(kind: int, q, k_cache, v_cache, block_table, seq_lens, cu_seqlens_q, plan_dev,
+              info: PlanInfo, workspace, out, lse=None, scale=None, stream=None):
+    """Paged attention (prefill / decode / verify by ``kind``) on device tensors."""
+    nb, hkv, bs, d = k_cache.shape
+    total_q, hq, _ = q.shape
+    n_seqs = int(seq_lens.numel())
+    if scale is None:
+        scale = d ** -0.5
+    fn = {KIND_PREFILL: lib().pa_attn_prefill, KIND_DECODE: lib().pa_attn_decode,
+          KIND_VERIFY: lib().pa_attn_verify}[kind]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(fn(_dptr(q), _dptr(k_cache), _dptr(v_cache), nb, _dptr(block_table),
+              int(block_table.shape[1]), _dptr(seq_lens), _dptr(cu_seqlens_q), n_seqs, total_q,
+              hq, hkv, d, bs, float(scale), _dtype_code(q), _dptr(plan_dev), C.byref(info),
+              _dptr(workspace), ws_bytes, _dptr(out), _dptr(lse), _stream(stream)))

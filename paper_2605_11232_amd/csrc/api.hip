@@ -1,0 +1,139 @@
+// C-ABI device entry points: argument validation on the host, then launches
+// on the caller's stream.  See include/pa.h for the contract of each call.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+#include "plan_format.h"
+
+namespace pa {
+namespace dev {
+int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_blocks,
+                     const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
+                     const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
+                     const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
+                     int32_t nt, int64_t partial_rows, void* ws, void* out, float* lse,
+                     hipStream_t stream);
+int launch_attn_f32(const void* q, const void* kc, const void* vc, int32_t num_blocks,
+                    const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
+                    const int32_t* cu_q, int32_t n_seqs, int32_t total_q, int32_t hq, int32_t hkv,
+                    int32_t d, float scale, void* out, float* lse, hipStream_t stream);
+int launch_kv_append(const void* kn, const void* vn, const int32_t* slots, int32_t n, void* kc,
+                     void* vc, int32_t nb, int32_t hkv, int32_t d, int32_t dtype,
+                     hipStream_t stream);
+}  // namespace dev
+
+namespace {
+
+int check_shape(const char* fn, int32_t num_blocks, int32_t num_kv_heads, int32_t head_dim,
+                int32_t block_size, int32_t dtype) {
+  if (num_blocks <= 0 || num_kv_heads <= 0)
+    return fail(PA_ERR_ARG, "%s: num_blocks %d and num_kv_heads %d must be positive", fn,
+                num_blocks, num_kv_heads);
+  if (int64_t(num_blocks) * block_size >= (int64_t{1} << 31))
+    return fail(PA_ERR_ARG, "%s: num_blocks * block_size must be < 2^31", fn);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(PA_ERR_UNSUPPORTED, "%s: head_dim %d (supported: 64, 128)", fn, head_dim);
+  if (block_size != 16)
+    return fail(PA_ERR_UNSUPPORTED, "%s: block_size %d (supported: 16)", fn, block_size);
+  if (dtype != PA_F32 && dtype != PA_BF16)
+    return fail(PA_ERR_UNSUPPORTED, "%s: dtype %d (supported: PA_F32, PA_BF16)", fn, dtype);
+  return PA_OK;
+}
+
+int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_cache,
+                const void* v_cache, int32_t num_blocks, const int32_t* block_table,
+                int32_t max_blocks_per_seq, const int32_t* seq_lens, const int32_t* cu_seqlens_q,
+                int32_t n_seqs, int32_t total_q, int32_t num_q_heads, int32_t num_kv_heads,
+                int32_t head_dim, int32_t block_size, float scale, int32_t dtype,
+                const int32_t* plan, const pa_plan_info* info, void* workspace,
+                size_t workspace_bytes, void* out, float* lse, void* stream) {
+  clear_error();
+  int rc = check_shape(fn, num_blocks, num_kv_heads, head_dim, block_size, dtype);
+  if (rc) return rc;
+  if (num_q_heads <= 0 || num_q_heads % num_kv_heads)
+    return fail(PA_ERR_ARG, "%s: num_q_heads %d must be a positive multiple of num_kv_heads %d",
+                fn, num_q_heads, num_kv_heads);
+  if (n_seqs < 0 || total_q < 0 || max_blocks_per_seq < 1)
+    return fail(PA_ERR_ARG, "%s: negative size or max_blocks_per_seq < 1", fn);
+  if (!(scale > 0.f) || scale == __builtin_huge_valf())
+    return fail(PA_ERR_ARG, "%s: scale must be positive and finite", fn);
+  if (!info) return fail(PA_ERR_ARG, "%s: NULL plan info", fn);
+  if (info->kind != want_kind)
+    return fail(PA_ERR_ARG, "%s: plan was built for kind %d, this call needs kind %d", fn,
+                info->kind, want_kind);
+  if (total_q == 0 || n_seqs == 0) return PA_OK;
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !cu_seqlens_q || !out)
+    return fail(PA_ERR_ARG, "%s: NULL device pointer", fn);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (dtype == PA_F32) {
+    rc = dev::launch_attn_f32(q, k_cache, v_cache, num_blocks, block_table, max_blocks_per_seq,
+                              seq_lens, cu_seqlens_q, n_seqs, total_q, num_q_heads, num_kv_heads,
+                              head_dim, scale, out, lse, st);
+  } else {
+    if (!plan) return fail(PA_ERR_ARG, "%s: NULL plan", fn);
+    if (info->variant < 0 || info->variant > 3 || info->grid < 0 || info->n_groups < 0 ||
+        info->n_tile_items < 0 || info->n_tile_items > info->grid)
+      return fail(PA_ERR_ARG, "%s: corrupt plan info", fn);
+    if (static_cast<int64_t>(workspace_bytes) < info->workspace_bytes ||
+        (info->workspace_bytes > 0 && !workspace))
+      return fail(PA_ERR_ARG, "%s: workspace of %zu bytes, plan needs %lld", fn, workspace_bytes,
+                  (long long)info->workspace_bytes);
+    const int64_t partial_rows = info->workspace_bytes / (int64_t(head_dim + 1) * 4);
+    rc = dev::launch_attn_bf16(q, k_cache, v_cache, num_blocks, block_table, max_blocks_per_seq,
+                               seq_lens, cu_seqlens_q, num_q_heads, num_kv_heads, head_dim, scale,
+                               plan, info->grid, info->n_tile_items, info->n_groups,
+                               info->variant, partial_rows,
+                               workspace, out, lse, st);
+  }
+  if (rc) return fail(PA_ERR_LAUNCH, "%s: %s", fn, hipGetErrorString(static_cast<hipError_t>(rc)));
+  return PA_OK;
+}
+
+}  // namespace
+}  // namespace pa
+
+extern "C" {
+
+int pa_kv_append(const void* k_new, const void* v_new, const int32_t* slot_mapping,
+                 int32_t n_tokens, void* k_cache, void* v_cache, int32_t num_blocks,
+                 int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t dtype,
+                 void* stream) {
+  pa::clear_error();
+  int rc = pa::check_shape("pa_kv_append", num_blocks, num_kv_heads, head_dim, block_size, dtype);
+  if (rc) return rc;
+  if (n_tokens < 0) return pa::fail(PA_ERR_ARG, "pa_kv_append: n_tokens %d < 0", n_tokens);
+  if (n_tokens == 0) return PA_OK;
+  if (!k_new || !v_new || !slot_mapping || !k_cache || !v_cache)
+    return pa::fail(PA_ERR_ARG, "pa_kv_append: NULL device pointer");
+  rc = pa::dev::launch_kv_append(k_new, v_new, slot_mapping, n_tokens, k_cache, v_cache,
+                                 num_blocks, num_kv_heads, head_dim, dtype,
+                                 static_cast<hipStream_t>(stream));
+  if (rc)
+    return pa::fail(PA_ERR_LAUNCH, "pa_kv_append: %s",
+                    hipGetErrorString(static_cast<hipError_t>(rc)));
+  return PA_OK;
+}
+
+#define PA_ATTN_ARGS                                                                            \
+  const void *q, const void *k_cache, const void *v_cache, int32_t num_blocks,                  \
+      const int32_t *block_table, int32_t max_blocks_per_seq, const int32_t *seq_lens,          \
+      const int32_t *cu_seqlens_q, int32_t n_seqs, int32_t total_q, int32_t num_q_heads,        \
+      int32_t num_kv_heads, int32_t head_dim, int32_t block_size, float scale, int32_t dtype,   \
+      const int32_t *plan, const pa_plan_info *info, void *workspace, size_t workspace_bytes,   \
+      void *out, float *lse, void *stream
+#define PA_ATTN_PASS                                                                            \
+  q, k_cache, v_cache, num_blocks, block_table, max_blocks_per_seq, seq_lens, cu_seqlens_q,     \
+      n_seqs, total_q, num_q_heads, num_kv_heads, head_dim, block_size, scale, dtype, plan,     \
+      info, workspace, workspace_bytes, out, lse, stream
+
+int pa_attn_prefill(PA_ATTN_ARGS) {
+  return pa::attn_common("pa_attn_prefill", PA_KIND_PREFILL, PA_ATTN_PASS);
+}
+int pa_attn_decode(PA_ATTN_ARGS) {
+  return pa::attn_common("pa_attn_decode", PA_KIND_DECODE, PA_ATTN_PASS);
+}
+int pa_attn_verify(PA_ATTN_ARGS) {
+  return pa::attn_common("pa_attn_verify", PA_KIND_VERIFY, PA_ATTN_PASS);
+}
+
+}  // extern "C"

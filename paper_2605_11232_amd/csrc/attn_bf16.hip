@@ -1,0 +1,521 @@
+// bf16 paged attention over a prefix-shared KV cache on CDNA4 MFMA.
+//
+// What is computed (paper: Section 2, PagedAttention's block table and
+// Automatic Prefix Caching; Section 3, cached shared prefixes give the result
+// of recomputing them): for each query row, softmax(scale * q K^T) V over the
+// keys 0..a of its sequence, where a is the query's logical position, keys
+// and values gathered block by block through the block table.
+//
+// Two item kinds run in one launch (see plan.cpp):
+//  * tile items, one workgroup of 4 wavefronts x 32 rows: a 32-key tile of K
+//    and V^T is gathered from the paged cache into LDS (double buffered) and
+//    shared by the four wavefronts; S^T = K Q^T and O^T += V^T P^T run on
+//    32x32x16 MFMA.  Computing the transposed score tile puts one query row
+//    in each lane, so the online-softmax row max / sum needs a single
+//    cross-lane exchange, and the probabilities are already laid out as the
+//    B operand of the PV product (no LDS round trip for P).
+//  * row items, one wavefront each: <= 48 rows (decode's G rows, verification's
+//    n_q * G rows) on 16x16x32 MFMA with K and V^T streamed straight from HBM
+//    into registers over a split of the key range.
+//
+// The key order inside a tile is permuted so that each lane's eight PV
+// k-elements are eight consecutive keys: then V^T operands are single 16-byte
+// reads of the cache's [head_dim][block] value layout.
+//
+// Scores are scaled by scale * log2(e) and exponentiated with exp2; the
+// natural-log LSE is recovered as ln2 * (m + log2 l).
+#include "device_common.h"
+#include "plan_format.h"
+
+namespace pa {
+namespace dev {
+namespace {
+
+struct AttnArgs {
+  const __bf16* q;
+  const __bf16* kc;
+  const __bf16* vc;
+  const int32_t* bt;
+  const int32_t* seq_lens;
+  const int32_t* cu_q;
+  const int32_t* plan;
+  __bf16* out;
+  float* lse;
+  float* ws_o;
+  float* ws_lse;
+  int32_t max_blocks;
+  int32_t num_blocks;
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;
+  float scale_log2;
+};
+
+// Row r of a tile's K buffer holds key perm32(r): bits 2 and 3 swapped.
+__device__ __forceinline__ int perm32(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+template <int D>
+struct TileSmem {
+  static constexpr int KS = D + 8;   // bf16 per K row   (row stride 16 B odd multiple)
+  static constexpr int VS = 32 + 8;  // bf16 per V^T row (80 B)
+  __bf16 k[2][32 * KS];
+  __bf16 v[2][D * VS];
+};
+
+template <int D>
+__device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm) {
+  constexpr int KCH = D / 64;  // 16-byte K chunks per thread per tile (32 keys x D)
+  constexpr int VCH = D / 64;  // 16-byte V chunks per thread per tile (D x 32 keys)
+  const int r = it[I_SEQ], g = it[I_KVH], row0 = it[I_ROW0], nrows = it[I_NROWS];
+  const int kv0 = it[I_KV0], part = it[I_PART];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, j = lane & 31, hh = lane >> 5;
+  const int L = a.seq_lens[r];
+  const int qs = a.cu_q[r], n = a.cu_q[r + 1] - qs;
+  const int kend = min(it[I_KV1], L);
+  const int G = a.group;
+
+  const int lr = w * 32 + j;
+  const bool valid = lr < nrows;
+  const int rho = row0 + lr;
+  const int qi = rho / G;
+  const int hq = g * G + (rho - qi * G);
+  const int apos = valid ? L - n + qi : -1;
+
+  bf16x8 qf[D / 16];
+  {
+    const __bf16* qp = a.q + ((int64_t)(qs + qi) * a.hq + hq) * D + 8 * hh;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = as_bf16x8(valid ? ld16(qp + 16 * ks) : zero16());
+  }
+  f32x16 acc[D / 32];
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[dt][e] = 0.f;
+  float m = kNegInf, l = 0.f;
+
+  const int32_t* bt = a.bt + (int64_t)r * a.max_blocks;
+  const int64_t head_k = (int64_t)g * kBlock * D;  // offset of head g inside a K block
+  const int64_t blk_k = (int64_t)a.hkv * kBlock * D;
+  const int64_t head_v = (int64_t)g * D * kBlock;
+  const int64_t blk_v = (int64_t)a.hkv * D * kBlock;
+
+  u32x4 kr[KCH], vr[VCH];
+  auto load_tile = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + 256 * i;
+      const int kk = c / (D / 8), part8 = c % (D / 8);
+      const int key = t0 + kk;
+      if (key < kend) {
+        const int jb = min(key / kBlock, a.max_blocks - 1);
+        const int blk = clamp_block(bt[jb], a.num_blocks);
+        kr[i] = ld16(a.kc + blk * blk_k + head_k + (key % kBlock) * D + part8 * 8);
+      } else {
+        kr[i] = zero16();
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int c = tid + 256 * i;
+      const int b = c / (2 * D), d = (c % (2 * D)) >> 1, half = c & 1;
+      const int key0 = t0 + 16 * b + 8 * half;
+      if (key0 < kend) {
+        const int jb = min(key0 / kBlock, a.max_blocks - 1);
+        const int blk = clamp_block(bt[jb], a.num_blocks);
+        u32x4 x = ld16(a.vc + blk * blk_v + head_v + d * kBlock + 8 * half);
+        vr[i] = (key0 + 8 > kend) ? keep_bf16(x, kend - key0) : x;
+      } else {
+        vr[i] = zero16();
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + 256 * i;
+      const int kk = c / (D / 8), part8 = c % (D / 8);
+      st16(&sm.k[buf][perm32(kk) * TileSmem<D>::KS + part8 * 8], kr[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int c = tid + 256 * i;
+      const int b = c / (2 * D), d = (c % (2 * D)) >> 1, half = c & 1;
+      st16(&sm.v[buf][d * TileSmem<D>::VS + 16 * b + 8 * half], vr[i]);
+    }
+  };
+
+  const int ntiles = kend > kv0 ? (kend - kv0 + 31) / 32 : 0;
+  if (ntiles > 0) {
+    load_tile(kv0);
+    store_tile(0);
+  }
+  __syncthreads();
+  for (int tI = 0; tI < ntiles; ++tI) {
+    const int buf = tI & 1;
+    const int t0 = kv0 + 32 * tI;
+    const bool more = tI + 1 < ntiles;
+    if (more) load_tile(t0 + 32);
+
+    // S^T[key][row] for the wave's 32 rows.
+    f32x16 s;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s[e] = 0.f;
+    const __bf16* kb = &sm.k[buf][j * TileSmem<D>::KS + 8 * hh];
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+      s = mfma32(as_bf16x8(ld16(kb + 16 * ks)), qf[ks], s);
+
+    float mx = kNegInf;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int key = t0 + perm32(8 * (e >> 2) + 4 * hh + (e & 3));
+      const float v = key <= apos ? s[e] * a.scale_log2 : kNegInf;
+      s[e] = v;
+      mx = fmaxf(mx, v);
+    }
+    mx = fmaxf(mx, wave_xor(mx, 32));
+    const float mnew = fmaxf(m, mx);
+    const float mb = mnew == kNegInf ? 0.f : mnew;
+    const float alpha = exp2f(m - mb);
+    float ps = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      s[e] = exp2f(s[e] - mb);
+      ps += s[e];
+    }
+    ps += wave_xor(ps, 32);
+    l = l * alpha + ps;
+    m = mnew;
+    bf16x8 pb0, pb1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      pb0[e] = (__bf16)s[e];
+      pb1[e] = (__bf16)s[8 + e];
+    }
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
+      const __bf16* vb = &sm.v[buf][(32 * dt + j) * TileSmem<D>::VS + 8 * hh];
+      acc[dt] = mfma32(as_bf16x8(ld16(vb)), pb0, acc[dt]);
+      acc[dt] = mfma32(as_bf16x8(ld16(vb + 16)), pb1, acc[dt]);
+    }
+    if (more) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  if (!valid) return;
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  const float lse_v = l > 0.f ? kLn2 * (m + __log2f(l)) : kNegInf;
+  if (part < 0) {
+    __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = 32 * dt + 8 * q4 + 4 * hh;
+        __bf16 o4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o4[e] = (__bf16)(acc[dt][4 * q4 + e] * inv);
+        *reinterpret_cast<u32x2*>(op + d) = __builtin_bit_cast(u32x2, o4);
+      }
+    if (a.lse && hh == 0) a.lse[(int64_t)(qs + qi) * a.hq + hq] = lse_v;
+  } else {
+    float* op = a.ws_o + (int64_t)(part + lr) * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = 32 * dt + 8 * q4 + 4 * hh;
+        f32x4 o4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o4[e] = acc[dt][4 * q4 + e] * inv;
+        *reinterpret_cast<f32x4*>(op + d) = o4;
+      }
+    if (hh == 0) a.ws_lse[part + lr] = lse_v;
+  }
+}
+
+// Row item: one wavefront, NT 16-column tiles of rows, keys [kv0, kv1).
+template <int D, int NT>
+__device__ void row_item(const int32_t* it, const AttnArgs& a) {
+  constexpr int KS = D / 32;  // k-steps of the QK product (32 dims each)
+  constexpr int DT = D / 16;  // 16-row tiles of O^T
+  const int r = it[I_SEQ];
+  if (r < 0) return;
+  const int g = it[I_KVH], row0 = it[I_ROW0], nrows = it[I_NROWS];
+  const int kv0 = it[I_KV0], part = it[I_PART];
+  const int lane = threadIdx.x & 63, j = lane & 15, g4 = lane >> 4;
+  const int L = a.seq_lens[r];
+  const int qs = a.cu_q[r], n = a.cu_q[r + 1] - qs;
+  const int kv1 = min(it[I_KV1], L);
+  const int G = a.group;
+
+  int apos[NT], qi[NT], hq[NT];
+  bf16x8 qf[NT][KS];
+  f32x4 acc[DT][NT];
+  float m[NT], l[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int lr = 16 * nt + j;
+    const bool valid = lr < nrows;
+    const int rho = row0 + lr;
+    qi[nt] = rho / G;
+    hq[nt] = g * G + (rho - qi[nt] * G);
+    apos[nt] = valid ? L - n + qi[nt] : -1;
+    const __bf16* qp = a.q + ((int64_t)(qs + qi[nt]) * a.hq + hq[nt]) * D + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[nt][ks] = as_bf16x8(valid ? ld16(qp + 32 * ks) : zero16());
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m[nt] = kNegInf;
+    l[nt] = 0.f;
+  }
+
+  const int32_t* bt = a.bt + (int64_t)r * a.max_blocks;
+  const int64_t blk_k = (int64_t)a.hkv * kBlock * D, head_k = (int64_t)g * kBlock * D;
+  const int64_t blk_v = (int64_t)a.hkv * D * kBlock, head_v = (int64_t)g * D * kBlock;
+  // K operand row j of score tile tt holds key 8 * (j / 4) + 4 * tt + j % 4.
+  const int kA0 = 8 * (j >> 2) + (j & 3);
+
+  // One register set for K and one for V^T: the next step's K loads are
+  // issued as soon as the score MFMAs have consumed K, and its V^T loads as
+  // soon as the PV MFMAs have consumed V^T, so HBM reads overlap the softmax
+  // and the MFMAs of the current step.
+  u32x4 kreg[2][KS], vreg[DT];
+  int b0 = 0, b1 = 0;
+  auto blocks_of = [&](int t0) {
+    const int jb = t0 / kBlock;
+    b0 = clamp_block(bt[min(jb, a.max_blocks - 1)], a.num_blocks);
+    b1 = t0 + 16 < kv1 ? clamp_block(bt[min(jb + 1, a.max_blocks - 1)], a.num_blocks) : b0;
+  };
+  auto load_k = [&]() {
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const int kk = kA0 + 4 * tt;
+      const int blk = kk < 16 ? b0 : b1;
+      const __bf16* p = a.kc + blk * blk_k + head_k + (kk & 15) * D + 8 * g4;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kreg[tt][ks] = ld16(p + 32 * ks);
+    }
+  };
+  auto load_v = [&](int t0) {
+    const int blk = g4 < 2 ? b0 : b1;
+    const int key0 = t0 + 8 * g4;
+    const __bf16* p = a.vc + blk * blk_v + head_v + j * kBlock + 8 * (g4 & 1);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      u32x4 x = ld16(p + 16 * kBlock * dt);
+      vreg[dt] = key0 >= kv1 ? zero16() : (key0 + 8 > kv1 ? keep_bf16(x, kv1 - key0) : x);
+    }
+  };
+
+  if (kv0 < kv1) {
+    blocks_of(kv0);
+    load_k();
+    load_v(kv0);
+  }
+  for (int t0 = kv0; t0 < kv1; t0 += 32) {
+    const bool more = t0 + 32 < kv1;
+    f32x4 s[2][NT];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) c = mfma16(as_bf16x8(kreg[tt][ks]), qf[nt][ks], c);
+        s[tt][nt] = c;
+      }
+    if (more) {
+      blocks_of(t0 + 32);
+      load_k();
+    }
+    bf16x8 pb[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      float mx = kNegInf;
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = t0 + 8 * g4 + 4 * tt + e;
+          const float v = (key <= apos[nt] && key < kv1) ? s[tt][nt][e] * a.scale_log2 : kNegInf;
+          s[tt][nt][e] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, wave_xor(mx, 16));
+      mx = fmaxf(mx, wave_xor(mx, 32));
+      const float mnew = fmaxf(m[nt], mx);
+      const float mb = mnew == kNegInf ? 0.f : mnew;
+      const float alpha = exp2f(m[nt] - mb);
+      float ps = 0.f;
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float p = exp2f(s[tt][nt][e] - mb);
+          ps += p;
+          pb[nt][4 * tt + e] = (__bf16)p;
+        }
+      ps += wave_xor(ps, 16);
+      ps += wave_xor(ps, 32);
+      l[nt] = l[nt] * alpha + ps;
+      m[nt] = mnew;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) acc[dt][nt] *= alpha;
+    }
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16x8 vf = as_bf16x8(vreg[dt]);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[dt][nt] = mfma16(vf, pb[nt], acc[dt][nt]);
+    }
+    if (more) load_v(t0 + 32);
+  }
+
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int lr = 16 * nt + j;
+    if (lr >= nrows) continue;
+    const float inv = l[nt] > 0.f ? 1.f / l[nt] : 0.f;
+    const float lse_v = l[nt] > 0.f ? kLn2 * (m[nt] + __log2f(l[nt])) : kNegInf;
+    if (part < 0) {
+      __bf16* op = a.out + ((int64_t)(qs + qi[nt]) * a.hq + hq[nt]) * D + 4 * g4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        __bf16 o4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o4[e] = (__bf16)(acc[dt][nt][e] * inv);
+        *reinterpret_cast<u32x2*>(op + 16 * dt) = __builtin_bit_cast(u32x2, o4);
+      }
+      if (a.lse && g4 == 0) a.lse[(int64_t)(qs + qi[nt]) * a.hq + hq[nt]] = lse_v;
+    } else {
+      float* op = a.ws_o + (int64_t)(part + lr) * D + 4 * g4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4*>(op + 16 * dt) = acc[dt][nt] * inv;
+      if (g4 == 0) a.ws_lse[part + lr] = lse_v;
+    }
+  }
+}
+
+// MIX: 1 = tile items only, 2 = row items only, 3 = both (a mixed launch).
+// Separate instantiations keep a pure prefill or pure decode launch from
+// paying the other path's registers and LDS.
+template <int D, int NT, int MIX>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
+  const int32_t* plan = a.plan;
+  const int n_tile = plan[H_N_TILE];
+  const int b = blockIdx.x;
+  if constexpr (MIX & 1) {
+    __shared__ TileSmem<D> sm;
+    if (b < n_tile) {
+      tile_item<D>(plan + plan[H_TILE_OFF] + b * kItemWords, a, sm);
+      return;
+    }
+  }
+  if constexpr (MIX & 2) {
+    const int idx = 4 * (b - n_tile) + (threadIdx.x >> 6);
+    if (b >= n_tile && idx < plan[H_N_ROW])
+      row_item<D, NT>(plan + plan[H_ROW_OFF] + idx * kItemWords, a);
+  }
+}
+
+// Combine split partial results by log-sum-exp: one workgroup per group, one
+// wavefront per row, each lane D/64 dims.
+template <int D>
+__global__ __launch_bounds__(256) void merge_kernel(AttnArgs a) {
+  const int32_t* plan = a.plan;
+  const int32_t* gr = plan + plan[H_GROUP_OFF] + blockIdx.x * kGroupWords;
+  const int r = gr[G_SEQ], g = gr[G_KVH], row0 = gr[G_ROW0], nrows = gr[G_NROWS];
+  const int nsplit = gr[G_NSPLIT], part = gr[G_PART];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int qs = a.cu_q[r];
+  for (int lr = w; lr < nrows; lr += 4) {
+    float mx = kNegInf;
+    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, a.ws_lse[part + s * nrows + lr]);
+    float o[D / 64];
+#pragma unroll
+    for (int k = 0; k < D / 64; ++k) o[k] = 0.f;
+    float lse_v = kNegInf;
+    if (mx != kNegInf) {
+      float sum = 0.f;
+      for (int s = 0; s < nsplit; ++s) sum += exp2f((a.ws_lse[part + s * nrows + lr] - mx) * kLog2e);
+      lse_v = mx + kLn2 * __log2f(sum);
+      for (int s = 0; s < nsplit; ++s) {
+        const int pr = part + s * nrows + lr;
+        const float wgt = exp2f((a.ws_lse[pr] - lse_v) * kLog2e);
+#pragma unroll
+        for (int k = 0; k < D / 64; ++k) o[k] += wgt * a.ws_o[(int64_t)pr * D + lane + 64 * k];
+      }
+    }
+    const int rho = row0 + lr;
+    const int qi = rho / a.group;
+    const int hq = g * a.group + (rho - qi * a.group);
+    __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D;
+#pragma unroll
+    for (int k = 0; k < D / 64; ++k) op[lane + 64 * k] = (__bf16)o[k];
+    if (a.lse && lane == 0) a.lse[(int64_t)(qs + qi) * a.hq + hq] = lse_v;
+  }
+}
+
+}  // namespace
+
+int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_blocks,
+                     const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
+                     const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
+                     const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
+                     int32_t nt, int64_t partial_rows, void* ws, void* out, float* lse,
+                     hipStream_t stream) {
+  AttnArgs a;
+  a.q = static_cast<const __bf16*>(q);
+  a.kc = static_cast<const __bf16*>(kc);
+  a.vc = static_cast<const __bf16*>(vc);
+  a.bt = bt;
+  a.seq_lens = seq_lens;
+  a.cu_q = cu_q;
+  a.plan = plan;
+  a.out = static_cast<__bf16*>(out);
+  a.lse = lse;
+  a.ws_o = static_cast<float*>(ws);
+  a.ws_lse = a.ws_o ? a.ws_o + partial_rows * d : nullptr;
+  a.max_blocks = max_blocks;
+  a.num_blocks = num_blocks;
+  a.hq = hq;
+  a.hkv = hkv;
+  a.group = hq / hkv;
+  a.scale_log2 = scale * kLog2e;
+  if (grid > 0) {
+    const int mix = (n_tile > 0 ? 1 : 0) | (grid > n_tile ? 2 : 0);
+#define PA_LAUNCH(DD, NN, MM) \
+  hipLaunchKernelGGL((attn_bf16_kernel<DD, NN, MM>), dim3(grid), dim3(256), 0, stream, a)
+#define PA_LAUNCH_D(DD)                                          \
+  do {                                                           \
+    if (mix == 1) PA_LAUNCH(DD, 1, 1);                           \
+    else if (nt <= 1) { if (mix == 2) PA_LAUNCH(DD, 1, 2); else PA_LAUNCH(DD, 1, 3); } \
+    else if (nt == 2) { if (mix == 2) PA_LAUNCH(DD, 2, 2); else PA_LAUNCH(DD, 2, 3); } \
+    else { if (mix == 2) PA_LAUNCH(DD, 3, 2); else PA_LAUNCH(DD, 3, 3); } \
+  } while (0)
+    if (d == 128) PA_LAUNCH_D(128);
+    else PA_LAUNCH_D(64);
+#undef PA_LAUNCH_D
+#undef PA_LAUNCH
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return static_cast<int>(e);
+  }
+  if (n_groups > 0) {
+    if (d == 128)
+      hipLaunchKernelGGL(merge_kernel<128>, dim3(n_groups), dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL(merge_kernel<64>, dim3(n_groups), dim3(256), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return static_cast<int>(e);
+  }
+  return 0;
+}
+
+}  // namespace dev
+}  // namespace pa

@@ -1,0 +1,57 @@
+// Device-side helpers shared by the HIP kernels of libpa (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pa {
+namespace dev {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kBlock = 16;                     // tokens per KV block
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ u32x4 zero16() { return u32x4{0u, 0u, 0u, 0u}; }
+
+// Keep only the first `keep` (0..8) bf16 lanes of a 16-byte vector.
+__device__ __forceinline__ u32x4 keep_bf16(u32x4 v, int keep) {
+  u32x4 r;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int e0 = 2 * k;
+    uint32_t m = (e0 < keep ? 0x0000FFFFu : 0u) | (e0 + 1 < keep ? 0xFFFF0000u : 0u);
+    r[k] = v[k] & m;
+  }
+  return r;
+}
+
+// 32x32x16 bf16 MFMA: C[32x32] += A[32x16] * B[16x32].  Lane l holds A row
+// l % 32 and B column l % 32, k elements 8 * (l / 32) .. + 7; C column l % 32,
+// rows 8 * (e / 4) + 4 * (l / 32) + e % 4 for element e.
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+// 16x16x32 bf16 MFMA: lane l holds A row l % 16 and B column l % 16, k elements
+// 8 * (l / 16) .. + 7; C column l % 16, rows 4 * (l / 16) + e.
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float wave_xor(float v, int mask) { return __shfl_xor(v, mask, 64); }
+
+__device__ __forceinline__ int clamp_block(int b, int num_blocks) {
+  return b < 0 ? 0 : (b >= num_blocks ? num_blocks - 1 : b);
+}
+
+}  // namespace dev
+}  // namespace pa

@@ -1,0 +1,53 @@
+// Layout of the int32 launch plan shared by the host planner and the device
+// kernels.  A plan is a header followed by fixed-size records.
+#pragma once
+
+#include <cstdint>
+
+namespace pa {
+
+constexpr int32_t kPlanMagic = 0x31304150;  // "PA01"
+
+// Header words.
+enum : int32_t {
+  H_MAGIC = 0,
+  H_KIND,
+  H_N_TILE,        // 128-row items, one workgroup each
+  H_N_ROW,         // <= kRowItemMaxRows-row items, one wavefront each (multiple of 4, padded)
+  H_N_GROUPS,      // split groups combined by the merge kernel
+  H_GRID,          // workgroups of the attention launch = N_TILE + N_ROW / 4
+  H_HQ,
+  H_HKV,
+  H_D,
+  H_N_SEQS,
+  H_TOTAL_Q,
+  H_NT,            // 16-column MFMA tiles a row item needs (1..3; 0 if none)
+  H_TILE_OFF,      // word offset of the tile items
+  H_ROW_OFF,       // word offset of the row items
+  H_GROUP_OFF,     // word offset of the split groups
+  H_PARTIAL_ROWS,  // rows of partial results in the workspace
+  kHeaderWords = 16
+};
+
+// Work item (tile or row item): rows [row0, row0 + nrows) of sequence seq's
+// packed (query, head-in-group) rows for kv-head kvh, keys [kv0, kv1).
+// Row rho is query rho / G, q-head kvh * G + rho % G.  part = -1: write the
+// final output; otherwise the item writes normalised partial outputs and
+// log-sum-exps at workspace rows part + (rho - row0).  seq = -1: empty slot.
+enum : int32_t {
+  I_SEQ = 0, I_KVH, I_ROW0, I_NROWS, I_KV0, I_KV1, I_PART, I_PAD,
+  kItemWords = 8
+};
+
+// Split group: rows [row0, row0 + nrows) of (seq, kvh) were computed by
+// nsplit items whose partial rows start at part + s * nrows.
+enum : int32_t {
+  G_SEQ = 0, G_KVH, G_ROW0, G_NROWS, G_NSPLIT, G_PART, G_PAD0, G_PAD1,
+  kGroupWords = 8
+};
+
+constexpr int32_t kTileRows = 128;       // rows per tile item (4 waves x 32)
+constexpr int32_t kRowItemMaxRows = 48;  // rows a single-wave item can hold (3 x 16)
+constexpr int32_t kKeyStep = 32;         // keys per inner iteration
+
+}  // namespace pa

@@ -1,0 +1,310 @@
+// Host block manager: prefix-hit lookup, block allocation, block tables and
+// slot mapping for a paged KV cache whose leading blocks are shared prefixes.
+//
+// Paper: Section 2 (PagedAttention's block-granular KV layout addressed through
+// a per-request block table; Automatic Prefix Caching reuses the KV blocks of
+// matching prefixes), Section 3 (shared policy prefixes are not recomputed),
+// Section 5.3 (prefixes identical across thousands of requests).
+//
+// A cached block is identified by (predecessor block, its block_size tokens).
+// Because a block is cached only when its predecessor is cached, that pair
+// stands for the whole token prefix up to the block, so a match on it is a
+// match on the full prefix.  The hash only narrows candidates: every hit is
+// confirmed by comparing the predecessor id and the stored tokens, so hash
+// collisions cannot produce a false hit.
+#include <algorithm>
+#include <cstring>
+#include <deque>
+#include <new>
+#include <unordered_map>
+#include <vector>
+
+#include "internal.h"
+
+struct pa_pool {
+  int32_t num_blocks = 0;
+  int32_t bs = 0;
+  std::deque<int32_t> free_list;
+  std::vector<int32_t> ref;          // live sequences holding each block
+  std::vector<uint8_t> cached;       // block is in the prefix index
+  std::vector<int32_t> pred;         // cached block's predecessor (-1: first block)
+  std::vector<int32_t> content;      // cached block's tokens, [num_blocks][bs]
+  std::unordered_multimap<uint64_t, int32_t> index;
+
+  struct Seq {
+    std::vector<int32_t> tokens;
+    std::vector<int32_t> blocks;
+    int32_t n_cached_run = 0;  // leading blocks of this sequence that are in the index
+  };
+  std::unordered_map<int64_t, Seq> seqs;
+
+  static int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+  uint64_t key_hash(int32_t p, const int32_t* t) const {
+    uint64_t h = 0x9E3779B97F4A7C15ull ^ static_cast<uint32_t>(p);
+    for (int32_t i = 0; i < bs; ++i) {
+      h ^= static_cast<uint32_t>(t[i]);
+      h *= 0x100000001B3ull;
+      h ^= h >> 29;
+    }
+    return h;
+  }
+
+  // Cached block whose predecessor is p and whose tokens are t[0..bs), or -1.
+  int32_t find(int32_t p, const int32_t* t) const {
+    auto range = index.equal_range(key_hash(p, t));
+    for (auto it = range.first; it != range.second; ++it) {
+      const int32_t b = it->second;
+      if (pred[b] == p &&
+          std::memcmp(&content[static_cast<size_t>(b) * bs], t, sizeof(int32_t) * bs) == 0)
+        return b;
+    }
+    return -1;
+  }
+
+  // Cache the sequence's full blocks after its cached run, in logical order,
+  // while the chain is unbroken and each prefix is new.
+  void cache_run(Seq& s) {
+    int32_t j = s.n_cached_run;
+    const int64_t L = static_cast<int64_t>(s.tokens.size());
+    while (static_cast<int64_t>(j + 1) * bs <= L) {
+      const int32_t p = j ? s.blocks[j - 1] : -1;
+      const int32_t* t = &s.tokens[static_cast<size_t>(j) * bs];
+      if (find(p, t) >= 0) break;
+      const int32_t b = s.blocks[j];
+      cached[b] = 1;
+      pred[b] = p;
+      std::memcpy(&content[static_cast<size_t>(b) * bs], t, sizeof(int32_t) * bs);
+      index.emplace(key_hash(p, t), b);
+      ++j;
+    }
+    s.n_cached_run = j;
+  }
+};
+
+extern "C" {
+
+int pa_pool_create(int32_t num_blocks, int32_t block_size, const int32_t* free_order,
+                   pa_pool** out) {
+  pa::clear_error();
+  if (!out || !free_order) return pa::fail(PA_ERR_ARG, "pa_pool_create: NULL argument");
+  *out = nullptr;
+  if (num_blocks <= 0 || block_size <= 0)
+    return pa::fail(PA_ERR_ARG, "pa_pool_create: num_blocks %d and block_size %d must be positive",
+                    num_blocks, block_size);
+  if (static_cast<int64_t>(num_blocks) * block_size >= (int64_t{1} << 31))
+    return pa::fail(PA_ERR_ARG, "pa_pool_create: num_blocks * block_size must be < 2^31");
+  std::vector<uint8_t> seen(num_blocks, 0);
+  for (int32_t i = 0; i < num_blocks; ++i) {
+    const int32_t b = free_order[i];
+    if (b < 0 || b >= num_blocks || seen[b])
+      return pa::fail(PA_ERR_ARG, "pa_pool_create: free_order is not a permutation (entry %d = %d)",
+                      i, b);
+    seen[b] = 1;
+  }
+  pa_pool* p = new (std::nothrow) pa_pool();
+  if (!p) return pa::fail(PA_ERR_ARG, "pa_pool_create: out of host memory");
+  p->num_blocks = num_blocks;
+  p->bs = block_size;
+  p->free_list.assign(free_order, free_order + num_blocks);
+  p->ref.assign(num_blocks, 0);
+  p->cached.assign(num_blocks, 0);
+  p->pred.assign(num_blocks, -1);
+  p->content.assign(static_cast<size_t>(num_blocks) * block_size, 0);
+  *out = p;
+  return PA_OK;
+}
+
+void pa_pool_destroy(pa_pool* pool) { delete pool; }
+
+int pa_seq_add(pa_pool* pool, int64_t seq_id, const int32_t* tokens, int32_t n_tokens,
+               int32_t* n_cached_out) {
+  pa::clear_error();
+  if (!pool || !tokens) return pa::fail(PA_ERR_ARG, "pa_seq_add: NULL argument");
+  if (n_tokens < 1) return pa::fail(PA_ERR_ARG, "pa_seq_add: n_tokens %d < 1", n_tokens);
+  if (pool->seqs.count(seq_id))
+    return pa::fail(PA_ERR_ARG, "pa_seq_add: sequence %lld already exists", (long long)seq_id);
+  const int32_t bs = pool->bs;
+  std::vector<int32_t> hits;
+  int32_t prev = -1;
+  while (static_cast<int64_t>(hits.size() + 1) * bs <= n_tokens - 1) {
+    const int32_t b = pool->find(prev, tokens + hits.size() * bs);
+    if (b < 0) break;
+    hits.push_back(b);
+    prev = b;
+  }
+  const int64_t need = pa_pool::cdiv(n_tokens, bs) - static_cast<int64_t>(hits.size());
+  if (need > static_cast<int64_t>(pool->free_list.size()))
+    return pa::fail(PA_ERR_NO_BLOCKS, "pa_seq_add: need %lld blocks, %zu free", (long long)need,
+                    pool->free_list.size());
+  pa_pool::Seq s;
+  s.tokens.assign(tokens, tokens + n_tokens);
+  s.blocks = hits;
+  s.n_cached_run = static_cast<int32_t>(hits.size());
+  for (int32_t b : hits) ++pool->ref[b];
+  for (int64_t i = 0; i < need; ++i) {
+    const int32_t b = pool->free_list.front();
+    pool->free_list.pop_front();
+    pool->ref[b] = 1;
+    s.blocks.push_back(b);
+  }
+  pool->cache_run(s);
+  pool->seqs.emplace(seq_id, std::move(s));
+  if (n_cached_out) *n_cached_out = static_cast<int32_t>(hits.size()) * bs;
+  return PA_OK;
+}
+
+int pa_seq_extend(pa_pool* pool, int64_t seq_id, const int32_t* tokens, int32_t n_tokens) {
+  pa::clear_error();
+  if (!pool || (n_tokens > 0 && !tokens)) return pa::fail(PA_ERR_ARG, "pa_seq_extend: NULL argument");
+  if (n_tokens < 0) return pa::fail(PA_ERR_ARG, "pa_seq_extend: n_tokens %d < 0", n_tokens);
+  auto it = pool->seqs.find(seq_id);
+  if (it == pool->seqs.end())
+    return pa::fail(PA_ERR_UNKNOWN_SEQ, "pa_seq_extend: unknown sequence %lld", (long long)seq_id);
+  pa_pool::Seq& s = it->second;
+  const int64_t new_len = static_cast<int64_t>(s.tokens.size()) + n_tokens;
+  if (new_len >= (int64_t{1} << 31))
+    return pa::fail(PA_ERR_ARG, "pa_seq_extend: sequence length overflows int32");
+  const int64_t need = pa_pool::cdiv(new_len, pool->bs) - static_cast<int64_t>(s.blocks.size());
+  if (need > static_cast<int64_t>(pool->free_list.size()))
+    return pa::fail(PA_ERR_NO_BLOCKS, "pa_seq_extend: need %lld blocks, %zu free", (long long)need,
+                    pool->free_list.size());
+  for (int64_t i = 0; i < need; ++i) {
+    const int32_t b = pool->free_list.front();
+    pool->free_list.pop_front();
+    pool->ref[b] = 1;
+    s.blocks.push_back(b);
+  }
+  s.tokens.insert(s.tokens.end(), tokens, tokens + n_tokens);
+  return PA_OK;
+}
+
+int pa_seq_truncate(pa_pool* pool, int64_t seq_id, int32_t new_len) {
+  pa::clear_error();
+  if (!pool) return pa::fail(PA_ERR_ARG, "pa_seq_truncate: NULL pool");
+  auto it = pool->seqs.find(seq_id);
+  if (it == pool->seqs.end())
+    return pa::fail(PA_ERR_UNKNOWN_SEQ, "pa_seq_truncate: unknown sequence %lld", (long long)seq_id);
+  pa_pool::Seq& s = it->second;
+  const int64_t L = static_cast<int64_t>(s.tokens.size());
+  const int64_t floor_len = static_cast<int64_t>(s.n_cached_run) * pool->bs;
+  if (new_len < 1 || new_len > L || new_len < floor_len)
+    return pa::fail(PA_ERR_ARG, "pa_seq_truncate: new_len %d outside [%lld, %lld]", new_len,
+                    (long long)std::max<int64_t>(1, floor_len), (long long)L);
+  const size_t keep = static_cast<size_t>(pa_pool::cdiv(new_len, pool->bs));
+  for (size_t j = s.blocks.size(); j-- > keep;) {
+    const int32_t b = s.blocks[j];
+    --pool->ref[b];
+    pool->free_list.push_front(b);
+  }
+  s.blocks.resize(keep);
+  s.tokens.resize(static_cast<size_t>(new_len));
+  return PA_OK;
+}
+
+int pa_seq_free(pa_pool* pool, int64_t seq_id) {
+  pa::clear_error();
+  if (!pool) return pa::fail(PA_ERR_ARG, "pa_seq_free: NULL pool");
+  auto it = pool->seqs.find(seq_id);
+  if (it == pool->seqs.end())
+    return pa::fail(PA_ERR_UNKNOWN_SEQ, "pa_seq_free: unknown sequence %lld", (long long)seq_id);
+  pa_pool::Seq& s = it->second;
+  pool->cache_run(s);
+  for (int32_t b : s.blocks) {
+    if (--pool->ref[b] == 0 && !pool->cached[b]) pool->free_list.push_back(b);
+  }
+  pool->seqs.erase(it);
+  return PA_OK;
+}
+
+int pa_seq_len(const pa_pool* pool, int64_t seq_id, int32_t* len_out) {
+  pa::clear_error();
+  if (!pool || !len_out) return pa::fail(PA_ERR_ARG, "pa_seq_len: NULL argument");
+  auto it = pool->seqs.find(seq_id);
+  if (it == pool->seqs.end())
+    return pa::fail(PA_ERR_UNKNOWN_SEQ, "pa_seq_len: unknown sequence %lld", (long long)seq_id);
+  *len_out = static_cast<int32_t>(it->second.tokens.size());
+  return PA_OK;
+}
+
+int pa_seq_blocks(const pa_pool* pool, int64_t seq_id, int32_t* out, int32_t capacity,
+                  int32_t* n_out) {
+  pa::clear_error();
+  if (!pool || !n_out || (capacity > 0 && !out))
+    return pa::fail(PA_ERR_ARG, "pa_seq_blocks: NULL argument");
+  auto it = pool->seqs.find(seq_id);
+  if (it == pool->seqs.end())
+    return pa::fail(PA_ERR_UNKNOWN_SEQ, "pa_seq_blocks: unknown sequence %lld", (long long)seq_id);
+  const auto& b = it->second.blocks;
+  *n_out = static_cast<int32_t>(b.size());
+  if (static_cast<int64_t>(b.size()) > capacity)
+    return pa::fail(PA_ERR_ARG, "pa_seq_blocks: capacity %d < %zu", capacity, b.size());
+  std::copy(b.begin(), b.end(), out);
+  return PA_OK;
+}
+
+int pa_pool_free_list(const pa_pool* pool, int32_t* out, int32_t capacity, int32_t* n_out) {
+  pa::clear_error();
+  if (!pool || !n_out || (capacity > 0 && !out))
+    return pa::fail(PA_ERR_ARG, "pa_pool_free_list: NULL argument");
+  *n_out = static_cast<int32_t>(pool->free_list.size());
+  if (static_cast<int64_t>(pool->free_list.size()) > capacity)
+    return pa::fail(PA_ERR_ARG, "pa_pool_free_list: capacity %d < %zu", capacity,
+                    pool->free_list.size());
+  std::copy(pool->free_list.begin(), pool->free_list.end(), out);
+  return PA_OK;
+}
+
+int pa_build_metadata(const pa_pool* pool, int32_t n_seqs, const int64_t* seq_ids,
+                      const int32_t* q_lens, int32_t max_blocks_per_seq, int32_t* block_table,
+                      int32_t* seq_lens, int32_t* cu_seqlens_q, int32_t* slot_mapping,
+                      int64_t slot_capacity) {
+  pa::clear_error();
+  if (!pool || n_seqs < 0 || max_blocks_per_seq < 1 || !cu_seqlens_q ||
+      (n_seqs > 0 && (!seq_ids || !q_lens || !block_table || !seq_lens)))
+    return pa::fail(PA_ERR_ARG, "pa_build_metadata: NULL or invalid argument");
+  const int32_t bs = pool->bs;
+  // validate everything before writing anything
+  std::vector<const pa_pool::Seq*> seqs(n_seqs);
+  std::unordered_map<int64_t, int32_t> seen;
+  int64_t total = 0;
+  for (int32_t r = 0; r < n_seqs; ++r) {
+    auto it = pool->seqs.find(seq_ids[r]);
+    if (it == pool->seqs.end())
+      return pa::fail(PA_ERR_UNKNOWN_SEQ, "pa_build_metadata: unknown sequence %lld",
+                      (long long)seq_ids[r]);
+    if (!seen.emplace(seq_ids[r], r).second)
+      return pa::fail(PA_ERR_ARG, "pa_build_metadata: sequence %lld appears twice",
+                      (long long)seq_ids[r]);
+    const pa_pool::Seq& s = it->second;
+    const int64_t L = static_cast<int64_t>(s.tokens.size());
+    if (q_lens[r] < 0 || q_lens[r] > L)
+      return pa::fail(PA_ERR_ARG, "pa_build_metadata: q_len %d outside [0, %lld] for row %d",
+                      q_lens[r], (long long)L, r);
+    if (static_cast<int64_t>(s.blocks.size()) > max_blocks_per_seq)
+      return pa::fail(PA_ERR_ARG, "pa_build_metadata: sequence needs %zu blocks > max %d",
+                      s.blocks.size(), max_blocks_per_seq);
+    total += q_lens[r];
+    seqs[r] = &s;
+  }
+  if (total >= (int64_t{1} << 31))
+    return pa::fail(PA_ERR_ARG, "pa_build_metadata: total query tokens overflow int32");
+  if (total > slot_capacity || (total > 0 && !slot_mapping))
+    return pa::fail(PA_ERR_ARG, "pa_build_metadata: slot_capacity %lld < %lld",
+                    (long long)slot_capacity, (long long)total);
+  int64_t k = 0;
+  cu_seqlens_q[0] = 0;
+  for (int32_t r = 0; r < n_seqs; ++r) {
+    const pa_pool::Seq& s = *seqs[r];
+    const int32_t L = static_cast<int32_t>(s.tokens.size());
+    int32_t* row = block_table + static_cast<int64_t>(r) * max_blocks_per_seq;
+    std::fill(row, row + max_blocks_per_seq, -1);
+    std::copy(s.blocks.begin(), s.blocks.end(), row);
+    seq_lens[r] = L;
+    cu_seqlens_q[r + 1] = cu_seqlens_q[r] + q_lens[r];
+    for (int32_t t = L - q_lens[r]; t < L; ++t) slot_mapping[k++] = s.blocks[t / bs] * bs + t % bs;
+  }
+  return PA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,192 @@
+"""Drive a synthetic workload through libpa on the GPU.
+
+Host bookkeeping (prefix-hit lookup, allocation, metadata, launch plan) runs in
+the library's C++ block manager and planner; K/V appends and attention run in
+its HIP kernels.  torch provides device memory, pinned staging buffers and the
+stream -- nothing else.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+KIND = {"prefill": B.KIND_PREFILL, "decode": B.KIND_DECODE, "verify": B.KIND_VERIFY}
+
+
+def torch_dtype(name: str):
+    return {"bf16": torch.bfloat16, "f32": torch.float32}[name]
+
+
+class Prepared:
+    """Device-resident inputs of one launch (metadata, plan, q, new K/V)."""
+
+    def __init__(self, **kw):
+        self.__dict__.update(kw)
+
+
+class Staging:
+    """Pinned host buffers and device buffers for one launch's metadata and
+    plan.  The host fills the pinned buffers while the GPU still works on an
+    earlier launch; ``ready`` (recorded after the copies) guards reuse."""
+
+    def __init__(self, device, n_seqs, max_blocks, max_tokens, plan_words):
+        def pair(n):
+            h = torch.empty(max(1, n), dtype=torch.int32, pin_memory=True)
+            return h, torch.empty(max(1, n), dtype=torch.int32, device=device)
+        self.n_seqs, self.max_blocks = n_seqs, max_blocks
+        self.bt = pair(n_seqs * max_blocks)
+        self.sl = pair(n_seqs)
+        self.cu = pair(n_seqs + 1)
+        self.slots = pair(max_tokens)
+        self.plan = pair(plan_words)
+        self.ready = None
+
+    def wait(self):
+        if self.ready is not None:
+            self.ready.synchronize()
+
+
+class DeviceReplay:
+    def __init__(self, wl, device: str = "cuda", kind: str | None = None, num_cus: int = 0):
+        cfg = wl.cfg
+        self.wl, self.cfg, self.device = wl, cfg, torch.device(device)
+        self.tdtype = torch_dtype(cfg.dtype)
+        self.dcode = B.PA_BF16 if cfg.dtype == "bf16" else B.PA_F32
+        self.pool = B.Pool(wl.num_blocks, cfg.block_size, wl.free_order)
+        shape_k = (wl.num_blocks, cfg.num_kv_heads, cfg.block_size, cfg.head_dim)
+        shape_v = (wl.num_blocks, cfg.num_kv_heads, cfg.head_dim, cfg.block_size)
+        # Uninitialised on purpose: the kernels must never read unwritten slots.
+        self.k_cache = torch.empty(shape_k, dtype=self.tdtype, device=self.device)
+        self.v_cache = torch.empty(shape_v, dtype=self.tdtype, device=self.device)
+        self.kind = kind
+        self.num_cus = num_cus
+        self.n_cached = {}
+
+    # -- host ops ------------------------------------------------------------
+    def _write_kv(self, seq_id, k: np.ndarray, v: np.ndarray):
+        md = self.pool.metadata([seq_id], [len(k)], self.wl.max_blocks_per_seq)
+        dev = self.device
+        slots = torch.from_numpy(md["slot_mapping"]).to(dev)
+        kt = torch.from_numpy(k).to(dev, self.tdtype)
+        vt = torch.from_numpy(v).to(dev, self.tdtype)
+        B.kv_append(kt, vt, slots, self.k_cache, self.v_cache)
+
+    def apply(self, op):
+        p = self.pool
+        if op.kind == "add":
+            self.n_cached[op.seq_id] = p.add(op.seq_id, op.tokens)
+        elif op.kind == "extend":
+            p.extend(op.seq_id, op.tokens)
+        elif op.kind == "free":
+            p.free(op.seq_id)
+        elif op.kind == "truncate":
+            p.truncate(op.seq_id, op.n)
+        elif op.kind == "write_kv":
+            self._write_kv(op.seq_id, op.k.get(), op.v.get())
+        else:
+            raise ValueError(op.kind)
+
+    def setup(self):
+        for op in self.wl.setup:
+            self.apply(op)
+        torch.cuda.synchronize()
+        return self
+
+    def launch_kind(self, launch) -> str:
+        if self.kind:
+            return self.kind
+        ql = set(launch.q_lens)
+        if ql == {1}:
+            return "decode"
+        if len(ql) == 1 and 1 < next(iter(ql)) <= 8:
+            return "verify"
+        return "prefill"
+
+    # -- one launch ------------------------------------------------------------
+    def prepare(self, launch, q=None, k_new=None, v_new=None) -> Prepared:
+        """Run the launch's host ops, build metadata and plan, stage to device."""
+        self.n_cached = {}
+        for op in launch.pre:
+            self.apply(op)
+        cfg, dev = self.cfg, self.device
+        md = self.pool.metadata(launch.seq_ids, launch.q_lens, self.wl.max_blocks_per_seq)
+        kind = self.launch_kind(launch)
+        n_q = launch.q_lens[0] if kind == "verify" else 1
+        plan, info = B.plan(KIND[kind], n_q, md["seq_lens"], md["cu_seqlens_q"], cfg.num_q_heads,
+                            cfg.num_kv_heads, cfg.head_dim, cfg.block_size, self.dcode, self.num_cus)
+        if q is None:
+            q = torch.from_numpy(launch.q.get()).to(dev, self.tdtype)
+        if k_new is None:
+            k_new = torch.from_numpy(launch.k_new.get()).to(dev, self.tdtype)
+        if v_new is None:
+            v_new = torch.from_numpy(launch.v_new.get()).to(dev, self.tdtype)
+        ws = None
+        if info.workspace_bytes:
+            ws = torch.empty(int(info.workspace_bytes), dtype=torch.uint8, device=dev)
+        T = launch.total_q
+        return Prepared(
+            kind=kind, meta=md, info=info, plan_host=plan,
+            block_table=torch.from_numpy(md["block_table"]).to(dev),
+            seq_lens=torch.from_numpy(md["seq_lens"]).to(dev),
+            cu=torch.from_numpy(md["cu_seqlens_q"]).to(dev),
+            slots=torch.from_numpy(md["slot_mapping"]).to(dev),
+            plan=torch.from_numpy(plan).to(dev), q=q, k_new=k_new, v_new=v_new, ws=ws,
+            out=torch.empty((T, cfg.num_q_heads, cfg.head_dim), dtype=self.tdtype, device=dev),
+            lse=torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device=dev),
+            n_cached=dict(self.n_cached))
+
+    def prepare_staged(self, launch, st: Staging, q, k_new, v_new, out, lse) -> Prepared:
+        """Like ``prepare`` but through preallocated pinned/device buffers with
+        asynchronous copies, so host bookkeeping overlaps earlier GPU work."""
+        self.n_cached = {}
+        for op in launch.pre:
+            self.apply(op)
+        cfg = self.cfg
+        n = len(launch.seq_ids)
+        T = launch.total_q
+        st.wait()
+        hv = {"block_table": st.bt[0][:n * st.max_blocks].numpy().reshape(n, st.max_blocks),
+              "seq_lens": st.sl[0][:n].numpy(), "cu_seqlens_q": st.cu[0][:n + 1].numpy(),
+              "slot_mapping": st.slots[0][:T].numpy()}
+        md = self.pool.metadata(launch.seq_ids, launch.q_lens, st.max_blocks, out=hv)
+        kind = self.launch_kind(launch)
+        n_q = launch.q_lens[0] if kind == "verify" else 1
+        plan, info = B.plan(KIND[kind], n_q, md["seq_lens"], md["cu_seqlens_q"], cfg.num_q_heads,
+                            cfg.num_kv_heads, cfg.head_dim, cfg.block_size, self.dcode,
+                            self.num_cus, out=st.plan[0].numpy())
+        if info.plan_words > st.plan[0].numel():
+            raise RuntimeError("staging plan buffer too small")
+        for (h, d), cnt in ((st.bt, n * st.max_blocks), (st.sl, n), (st.cu, n + 1),
+                            (st.slots, T), (st.plan, int(info.plan_words))):
+            if cnt:
+                d[:cnt].copy_(h[:cnt], non_blocking=True)
+        st.ready = torch.cuda.Event()
+        st.ready.record()
+        ws = None
+        if info.workspace_bytes:
+            ws = torch.empty(int(info.workspace_bytes), dtype=torch.uint8, device=self.device)
+        return Prepared(
+            kind=kind, meta=md, info=info, plan_host=plan,
+            block_table=st.bt[1][:n * st.max_blocks].view(n, st.max_blocks),
+            seq_lens=st.sl[1][:n], cu=st.cu[1][:n + 1], slots=st.slots[1][:T],
+            plan=st.plan[1][:int(info.plan_words)], q=q, k_new=k_new, v_new=v_new, ws=ws,
+            out=out, lse=lse, n_cached=dict(self.n_cached))
+
+    def append(self, p: Prepared, stream=None):
+        B.kv_append(p.k_new, p.v_new, p.slots, self.k_cache, self.v_cache, stream)
+
+    def attend(self, p: Prepared, stream=None):
+        B.attention(KIND[p.kind], p.q, self.k_cache, self.v_cache, p.block_table, p.seq_lens, p.cu,
+                    p.plan, p.info, p.ws, p.out, p.lse, stream=stream)
+
+    def run(self, launch) -> Prepared:
+        p = self.prepare(launch)
+        self.append(p)
+        self.attend(p)
+        return p
+
+    def finish(self, launch):
+        for op in launch.post:
+            self.apply(op)

@@ -208,8 +208,21 @@ def _tiny(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
     needed = P // bs + sum(_cdiv(P + int(S[r]) + n_dec, bs) - P // bs for r in range(R))
     nb = 64
     assert needed <= nb
+
+    def step(st: int) -> Launch:
+        # repeated prefill launches (benchmarking): fresh suffix token ids per
+        # step, requests released afterwards
+        first = launches[0]
+        pre = [Op("add", r, _concat(prefix, tokens(s, TAG_SUFFIX_TOK, (r, st + 1), int(S[r]))))
+               for r in range(R)]
+        return Launch(pre, first.seq_ids, first.q_lens, first.q, first.k_new, first.v_new,
+                      [Op("free", r) for r in range(R)])
+
+    if steps > 1:
+        nb = max(nb, P // bs + steps * sum(_cdiv(P + int(S[r]), bs) - P // bs for r in range(R))
+                 + 64)
     free_order = rng(s, TAG_FREE).permutation(nb).astype(np.int32)
-    return Workload(cfg, nb, free_order, setup, launches, None, _cdiv(max_len, bs),
+    return Workload(cfg, nb, free_order, setup, launches, step, _cdiv(max_len, bs),
                     {"prefix": P, "suffix": S.tolist(), "decode_steps": n_dec})
 
 

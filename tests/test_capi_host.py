@@ -1,0 +1,244 @@
+"""CPU tests of the C-ABI boundary (no GPU): the library loads, exports every
+symbol include/pa.h declares, and its host block manager produces the same
+block tables, slot mappings and prefix-hit counts as the oracle, bit for bit;
+error paths leave the pool unchanged.  Device entry points are only called
+with arguments that fail host validation (nothing is launched)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2605_11232_amd import binding as B
+from paper_2605_11232_amd import synth
+from oracle.apc import OracleError, PrefixCacheOracle
+from tests.test_oracle_apc import _random_batch, run_golden
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_symbols():
+    txt = open(os.path.join(ROOT, "include", "pa.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)  # drop comments
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(pa_[a-z0-9_]+)\s*\(",
+                                 txt, flags=re.M)))
+
+
+def test_exports_every_declared_symbol():
+    lib = B.lib()
+    declared = _header_symbols()
+    assert set(declared) == set(B.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.pa_abi_version() == 1
+
+
+def _lib_apply(pool, st, toks):
+    try:
+        if st["op"] == "add":
+            return pool.add(st["seq"], toks)
+        if st["op"] == "extend":
+            return pool.extend(st["seq"], toks)
+        if st["op"] == "free":
+            return pool.free(st["seq"])
+        if st["op"] == "truncate":
+            return pool.truncate(st["seq"], st["n"])
+        if st["op"] == "metadata":
+            return pool.metadata(st["seqs"], st["q_lens"], st["max_blocks"])
+    except B.PaError as e:
+        return ("error", e.code)
+    raise ValueError(st["op"])
+
+
+def test_worked_example_library():
+    run_golden(B.Pool, _lib_apply)
+
+
+class _Both:
+    """Apply every operation to the oracle and the library and compare."""
+
+    def __init__(self, nb, bs, order):
+        self.o = PrefixCacheOracle(nb, bs, order)
+        self.l = B.Pool(nb, bs, order)
+
+    def do(self, name, *args):
+        res = []
+        for impl, fn in ((self.o, {"free": "free_seq"}.get(name, name)), (self.l, name)):
+            try:
+                res.append(("ok", getattr(impl, fn)(*args)))
+            except OracleError as e:
+                res.append(("error", e.code))
+            except B.PaError as e:
+                res.append(("error", e.code))
+        assert res[0] == res[1], (name, args, res)
+        assert self.o.free_list() == self.l.free_list()
+        return res[0]
+
+    def meta(self, ids, q_lens, mb):
+        a = self.o.metadata(ids, q_lens, mb)
+        b = self.l.metadata(ids, q_lens, mb)
+        for k in a:
+            np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+        return a
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_random_operation_sequences_bit_exact(seed):
+    r = np.random.default_rng(1000 + seed)
+    bs = int(r.choice([2, 4, 16]))
+    nb = int(r.integers(8, 120))
+    both = _Both(nb, bs, r.permutation(nb).tolist())
+    prefixes, reqs = _random_batch(seed, bs=bs, vocab=int(r.choice([2, 3, 50])))
+    live = {}
+    next_id = 0
+    for step in range(120):
+        op = r.integers(0, 6)
+        if op <= 1 or not live:
+            p, toks = reqs[int(r.integers(0, len(reqs)))]
+            if r.random() < 0.3:
+                toks = toks[:int(r.integers(1, len(toks) + 1))]
+            res = both.do("add", next_id, toks)
+            if res[0] == "ok":
+                live[next_id] = len(toks)
+            next_id += 1
+        elif op == 2:
+            sid = int(r.choice(list(live)))
+            n = int(r.integers(0, 2 * bs + 2))
+            res = both.do("extend", sid, r.integers(0, 4, size=n).tolist())
+        elif op == 3:
+            sid = int(r.choice(list(live)))
+            L = both.o.seq_len(sid)
+            both.do("truncate", sid, int(r.integers(0, L + 2)))
+        elif op == 4:
+            sid = int(r.choice(list(live)))
+            both.do("free", sid)
+            del live[sid]
+        else:
+            ids = list(live)
+            r.shuffle(ids)
+            ids = ids[:int(r.integers(1, len(ids) + 1))]
+            q = [int(r.integers(0, both.o.seq_len(i) + 1)) for i in ids]
+            both.meta(ids, q, 64 if bs >= 4 else 200)
+        # unknown sequences and duplicate ids behave alike
+        if step % 17 == 0:
+            both.do("free", 10 ** 9)
+            if live:
+                sid = next(iter(live))
+                both.do("add", sid, [1, 2, 3])
+
+
+@pytest.mark.parametrize("name", ["tiny", "prefill", "decode", "mixed", "verify"])
+def test_workload_tables_bit_exact(name):
+    """Setup + first launch of every workload at full size: tables, slots and
+    prefix hits agree exactly (values are not drawn; tables only)."""
+    wl = synth.workload(name, steps=2)
+    o = PrefixCacheOracle(wl.num_blocks, wl.cfg.block_size, wl.free_order)
+    l = B.Pool(wl.num_blocks, wl.cfg.block_size, wl.free_order)
+
+    def apply(op):
+        if op.kind == "write_kv":
+            return None
+        fn = {"add": ("add", "add"), "extend": ("extend", "extend"), "free": ("free_seq", "free"),
+              "truncate": ("truncate", "truncate")}[op.kind]
+        args = (op.seq_id, op.tokens) if op.tokens is not None else (op.seq_id, op.n)
+        if op.kind == "free":
+            args = (op.seq_id,)
+        a = getattr(o, fn[0])(*args)
+        b = getattr(l, fn[1])(*args)
+        assert a == b, op.kind
+        return a
+
+    for op in wl.setup:
+        apply(op)
+    extra = [wl.step(1)] if wl.step and name != "tiny" else []
+    for launch in wl.launches[:2] + extra:
+        hits = [apply(op) for op in launch.pre]
+        mo = o.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
+        ml = l.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
+        for k in mo:
+            np.testing.assert_array_equal(mo[k], ml[k], err_msg=k)
+        # the configured prefix is reused in full by every admitted request
+        if name in ("prefill", "tiny") and launch.pre[0].kind == "add":
+            assert set(hits) == {wl.notes["prefix"]}
+        for op in launch.post:
+            apply(op)
+        assert o.free_list() == l.free_list()
+
+
+def test_plan_covers_every_row_once():
+    """Each (token, head) row is produced exactly once: by one unsplit item or
+    by one split group whose items cover [0, seq_len) without overlap."""
+    r = np.random.default_rng(5)
+    for trial in range(30):
+        n = int(r.integers(1, 40))
+        hkv = int(r.choice([1, 2, 4, 8]))
+        G = int(r.choice([1, 4, 7, 8]))
+        L = r.integers(1, 5000, size=n)
+        q = np.minimum(L, r.choice([1, 2, 5, 8, 33, 300, 1000], size=n))
+        if trial % 3 == 0:
+            q[:] = 1
+        cu = np.concatenate([[0], np.cumsum(q)])
+        kind = B.KIND_DECODE if trial % 3 == 0 else B.KIND_PREFILL
+        plan, info = B.plan(kind, 1, L, cu, hkv * G, hkv, 128, 16, B.PA_BF16, 256)
+        h = plan[:16]
+        assert h[0] == 0x31304150 and h[5] == info.grid == h[2] + h[3] // 4
+        items = plan[h[12]:h[12] + 8 * h[2]].reshape(-1, 8).tolist()
+        items += plan[h[13]:h[13] + 8 * h[3]].reshape(-1, 8).tolist()
+        groups = plan[h[14]:h[14] + 8 * h[4]].reshape(-1, 8)
+        cover = {}
+        for seq, kvh, row0, nrows, kv0, kv1, part, _ in items:
+            if seq < 0:
+                continue
+            assert kv0 % 32 == 0 and 0 <= kv0 < kv1 <= L[seq]
+            for rho in range(row0, row0 + nrows):
+                cover.setdefault((seq, kvh, rho), []).append((kv0, kv1, part))
+        assert len(cover) == sum(int(q[s]) * G * hkv for s in range(n))
+        for (seq, kvh, rho), ranges in cover.items():
+            ranges.sort()
+            last_q = rho // G
+            need = int(L[seq] - q[seq] + last_q + 1)
+            if len(ranges) == 1:
+                assert ranges[0][2] == -1 and ranges[0][0] == 0 and ranges[0][1] >= need
+            else:
+                assert all(p >= 0 for _, _, p in ranges)
+                assert ranges[0][0] == 0 and ranges[-1][1] == L[seq]
+                assert all(ranges[i][1] == ranges[i + 1][0] for i in range(len(ranges) - 1))
+        assert int(info.workspace_bytes) == int(h[15]) * (128 + 1) * 4
+        assert sum(int(g[3]) * int(g[4]) for g in groups) == h[15]
+
+
+def test_device_calls_reject_bad_arguments_without_launching():
+    lib = B.lib()
+    info = B.PlanInfo()
+    info.kind = B.KIND_DECODE
+    args = [None, None, None, 16, None, 4, None, None, 1, 1, 8, 2, 128, 16, 0.1, B.PA_BF16, None,
+            ctypes.byref(info), None, 0, None, None, None]
+    # plan kind mismatch
+    assert lib.pa_attn_prefill(*args) == B.PA_ERR_ARG
+    assert b"kind" in lib.pa_last_error()
+    # unsupported head_dim / block_size / dtype
+    for idx, val, code in ((12, 96, B.PA_ERR_UNSUPPORTED), (13, 32, B.PA_ERR_UNSUPPORTED),
+                           (15, 7, B.PA_ERR_UNSUPPORTED), (10, 7, B.PA_ERR_ARG),
+                           (14, 0.0, B.PA_ERR_ARG)):
+        a = list(args)
+        a[idx] = val
+        assert lib.pa_attn_decode(*a) == code, idx
+    # NULL device pointers with work to do
+    assert lib.pa_attn_decode(*args) == B.PA_ERR_ARG
+    assert lib.pa_kv_append(None, None, None, 3, None, None, 16, 2, 128, 16, B.PA_BF16, None) == B.PA_ERR_ARG
+    assert lib.pa_kv_append(None, None, None, 0, None, None, 16, 2, 100, 16, B.PA_BF16, None) == B.PA_ERR_UNSUPPORTED
+
+
+def test_plan_rejects_inconsistent_lengths():
+    with pytest.raises(B.PaError) as e:
+        B.plan(B.KIND_DECODE, 1, [10, 10], [0, 1, 3], 8, 2, 128, 16, B.PA_BF16)
+    assert e.value.code == "arg"
+    with pytest.raises(B.PaError):
+        B.plan(B.KIND_VERIFY, 5, [10], [0, 4], 8, 2, 128, 16, B.PA_BF16)
+    with pytest.raises(B.PaError):
+        B.plan(B.KIND_PREFILL, 0, [3], [0, 4], 8, 2, 128, 16, B.PA_BF16)
+    with pytest.raises(B.PaError) as e:
+        B.plan(B.KIND_PREFILL, 0, [3], [0, 2], 8, 3, 128, 16, B.PA_BF16)
+    _, info = B.plan(B.KIND_PREFILL, 0, [], [0], 8, 2, 128, 16, B.PA_BF16)
+    assert info.grid == 0 and info.workspace_bytes == 0

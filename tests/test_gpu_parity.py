@@ -1,0 +1,233 @@
+"""GPU parity: libpa (HIP, through the C ABI) against the float64 oracle.
+
+Reduced sizes run the whole launch element by element (several 128-row tiles,
+split key ranges, ragged tails); full sizes run the exact launch the benchmark
+times and compare sampled rows.  Tables, slot mappings and prefix hits are
+compared bit for bit, the appended cache bit for bit, outputs within
+|o - r| <= atol + rtol |r| (bf16 1e-2 / 2e-2, float32 1e-5 / 1e-5).
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2605_11232_amd import synth
+from tests.parity import run_parity, sample_rows, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def test_tiny_f32_prefill_and_decode_steps():
+    _gpu()
+    errs, _, _ = run_parity(synth.workload("tiny"))
+    say("tiny normalized errors", errs)
+    assert len(errs) == 9
+
+
+def test_tiny_in_bf16():
+    _gpu()
+    run_parity(synth.workload("tiny", dtype="bf16"), label="tiny-bf16")
+
+
+@pytest.mark.parametrize("name,scale", [("prefill", 0.125), ("decode", 0.0625),
+                                        ("mixed", 0.0625), ("verify", 0.125)])
+def test_reduced(name, scale):
+    _gpu()
+    errs, _, _ = run_parity(synth.workload(name, scale=scale, steps=3), steps=[1],
+                            label=f"{name}@{scale}")
+    say(name, "normalized errors", errs)
+
+
+@pytest.mark.parametrize("name", ["prefill", "decode", "mixed", "verify"])
+def test_full_size_sampled(name):
+    """The benchmark's exact launch (full size) on sampled rows."""
+    _gpu()
+    wl = synth.workload(name, steps=2)
+    rows = sample_rows(wl.launches[0], 48, wl.cfg.num_q_heads, seed=7)
+    errs, _, _ = run_parity(wl, n_launches=1, rows=rows, label=f"{name}-full")
+    say(name, "full-size normalized error", errs)
+
+
+def test_bitwise_invariants():
+    """Outputs are identical bit for bit when physical placement changes and
+    when the shared prefix is duplicated instead of shared, and from run to run
+    (reduction order follows logical key order only)."""
+    _gpu()
+    base = synth.workload("prefill", scale=0.125)
+    wl_b = synth.workload("prefill", scale=0.125)
+    wl_b.free_order = np.random.default_rng(3).permutation(wl_b.num_blocks).astype(np.int32)
+    from paper_2605_11232_amd.runtime import DeviceReplay
+
+    def outputs(wl):
+        d = DeviceReplay(wl).setup()
+        p = d.run(wl.launches[0])
+        torch.cuda.synchronize()
+        return p.out.view(torch.int16).cpu().numpy(), p.lse.cpu().numpy(), p.meta["block_table"]
+
+    oa, la, bta = outputs(base)
+    oa2, la2, _ = outputs(base)
+    ob, lb, btb = outputs(wl_b)
+    assert not np.array_equal(bta, btb)
+    np.testing.assert_array_equal(oa, oa2)
+    np.testing.assert_array_equal(oa, ob)
+    np.testing.assert_array_equal(la, lb)
+    # duplicated prefix: no pre-population, each request carries its own copy
+    wl_c = synth.workload("prefill", scale=0.125)
+    pref_ops = [op for op in wl_c.setup]
+    add_op = pref_ops[0]
+    k, v = pref_ops[1].k.get(), pref_ops[1].v.get()
+    wl_c.setup = []
+    launch = wl_c.launches[0]
+    # every request now stores its own copy of the prefix
+    wl_c.num_blocks = base.num_blocks + len(launch.q_lens) * (len(add_op.tokens) // 16 + 1)
+    wl_c.free_order = np.arange(wl_c.num_blocks, dtype=np.int32)
+    P = len(add_op.tokens)
+    new_pre = []
+    for i, op in enumerate(launch.pre):
+        toks = op.tokens.copy()
+        toks[:P] += 1 + i  # distinct token ids -> no sharing
+        new_pre.append(synth.Op("add", op.seq_id, toks))
+    qv = launch.q.get()
+    kn, vn = launch.k_new.get(), launch.v_new.get()
+    # each request now computes its prefix too: prepend prefix K/V, and
+    # queries for the prefix positions (discarded), to every request
+    R = len(launch.q_lens)
+    cu = np.concatenate([[0], np.cumsum(launch.q_lens)])
+    Hq, D = qv.shape[1], qv.shape[2]
+    qs, ks, vs, ql = [], [], [], []
+    for r in range(R):
+        qs += [np.zeros((P, Hq, D), np.float32), qv[cu[r]:cu[r + 1]]]
+        ks += [k, kn[cu[r]:cu[r + 1]]]
+        vs += [v, vn[cu[r]:cu[r + 1]]]
+        ql.append(P + launch.q_lens[r])
+
+    class Fixed:
+        def __init__(self, a):
+            self.a = a
+
+        def get(self):
+            return self.a
+
+    wl_c.launches = [synth.Launch(new_pre, launch.seq_ids, ql, Fixed(np.concatenate(qs)),
+                                  Fixed(np.concatenate(ks)), Fixed(np.concatenate(vs)))]
+    oc, lc, _ = outputs(wl_c)
+    keep = np.concatenate([np.arange(cu[r] + (r + 1) * P, cu[r + 1] + (r + 1) * P) for r in range(R)])
+    np.testing.assert_array_equal(oa, oc[keep])
+    np.testing.assert_array_equal(la, lc[keep])
+
+
+def test_needle_through_block_table():
+    """Q = alpha e1, one key per kv-head = beta e1 at a chosen logical position,
+    all other keys 0: o = (e^s v* + sum of the other visible v) / (e^s + a).
+    A mis-mapped block moves the result by O(1)."""
+    _gpu()
+    from paper_2605_11232_amd import binding as B
+    from paper_2605_11232_amd.runtime import DeviceReplay
+    import math
+    wl = synth.workload("verify", scale=0.125)
+    cfg = wl.cfg
+    d = DeviceReplay(wl).setup()
+    launch = wl.step(0)
+    p = d.prepare(launch)
+    Hq, Hkv, D = cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    G = Hq // Hkv
+    alpha, beta = 4.0, 8.0
+    sigma = alpha * beta / math.sqrt(D)
+    # zero every key of the launch's sequences, keep values
+    bt = p.meta["block_table"]
+    L = p.meta["seq_lens"]
+    r = np.random.default_rng(0)
+    needles = {}
+    P = wl.notes["prefix"]
+    for i in range(len(L)):
+        blocks = torch.from_numpy(bt[i][:(L[i] + 15) // 16].astype(np.int64)).to(d.device)
+        d.k_cache[blocks] = 0
+    for i in range(len(L)):
+        for g in range(Hkv):
+            # private positions only: prefix blocks are shared by every request
+            t = int(r.integers(P, L[i] - 5))
+            needles[(i, g)] = t
+            d.k_cache[int(bt[i][t // 16]), g, t % 16, 0] = beta
+    p.k_new.zero_()
+    q = torch.zeros_like(p.q)
+    q[:, :, 0] = alpha
+    p.q = q
+    d.append(p)
+    d.attend(p)
+    torch.cuda.synchronize()
+    out = p.out.float().cpu().numpy()
+    # values: gather logical V on the host from the device cache
+    vc = d.v_cache.float().cpu().numpy()
+    cu = p.meta["cu_seqlens_q"]
+    for i in range(len(L)):
+        for j in range(cu[i + 1] - cu[i]):
+            a = L[i] - (cu[i + 1] - cu[i]) + j
+            tpos = np.arange(a + 1)
+            V = vc[bt[i][tpos // 16], :, :, tpos % 16]  # [a+1, Hkv, D]
+            for h in range(Hq):
+                g = h // G
+                ts = needles[(i, g)]
+                want = (math.exp(sigma) * V[ts, g] + V[:, g].sum(0) - V[ts, g]) / (math.exp(sigma) + a)
+                got = out[cu[i] + j, h]
+                assert np.all(np.abs(got - want) <= 1e-2 + 2e-2 * np.abs(want)), (i, j, h)
+
+
+def test_edge_cases():
+    """Empty launch, zero-query sequences mixed in, a one-token sequence,
+    head_dim 64 in bf16, G = 1, verify with 64 rows (tile path)."""
+    _gpu()
+    from oracle.run import OracleReplay
+    from paper_2605_11232_amd.runtime import DeviceReplay
+    from tests.parity import TOL, close
+    cfg = synth.AttnConfig("edge", "bf16", 4, 4, 64, 16, 77)
+    Val = synth.Values
+    r = np.random.default_rng(1)
+
+    def mk(q_lens, lens, seed, cfg=cfg):
+        """Sequences of length lens[i] whose last q_lens[i] tokens are queried;
+        the earlier positions get their K/V written in setup."""
+        setup, pre = [], []
+        for i, (q, L) in enumerate(zip(q_lens, lens)):
+            toks = r.integers(0, 50, size=L).astype(np.int32)
+            if L - q >= 1:
+                setup.append(synth.Op("add", i, toks[:L - q]))
+                setup.append(synth.Op("write_kv", i,
+                                      k=Val((seed, 15, i), (L - q, cfg.num_kv_heads, cfg.head_dim), "bf16"),
+                                      v=Val((seed, 16, i), (L - q, cfg.num_kv_heads, cfg.head_dim), "bf16")))
+                pre.append(synth.Op("extend", i, toks[L - q:]))
+            else:
+                pre.append(synth.Op("add", i, toks))
+        T = sum(q_lens)
+        return setup, synth.Launch(pre, list(range(len(lens))), q_lens,
+                                   Val((seed, 4), (T, cfg.num_q_heads, cfg.head_dim), "bf16"),
+                                   Val((seed, 5), (T, cfg.num_kv_heads, cfg.head_dim), "bf16"),
+                                   Val((seed, 6), (T, cfg.num_kv_heads, cfg.head_dim), "bf16"))
+
+    cases = [([0, 0], [5, 9]), ([1], [1]), ([0, 7, 0, 300, 1], [4, 7, 33, 300, 1000])]
+    for ci, (ql, lens) in enumerate(cases):
+        say("[edge] case", ci, ql, lens)
+        setup, launch = mk(ql, lens, 50 + ci)
+        wl = synth.Workload(cfg, 256, np.random.default_rng(ci).permutation(256).astype(np.int32),
+                            setup, [launch], None, 80)
+        o = OracleReplay(wl).setup()
+        dv = DeviceReplay(wl, kind="prefill").setup()
+        ro = o.launch(wl.launches[0])
+        p = dv.run(wl.launches[0])
+        torch.cuda.synchronize()
+        if sum(ql):
+            close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"edge{ci}")
+    # verify with n_q = 8 and G = 8: 64 rows per sequence -> tile items
+    cfg8 = synth.AttnConfig("edge8", "bf16", 16, 2, 128, 16, 78)
+    setup, launch = mk([8, 8], [40, 517], 9, cfg=cfg8)
+    wl = synth.Workload(cfg8, 128, np.arange(128, dtype=np.int32), setup, [launch], None, 40)
+    o = OracleReplay(wl).setup()
+    dv = DeviceReplay(wl, kind="verify").setup()
+    ro = o.launch(wl.launches[0])
+    p = dv.run(wl.launches[0])
+    torch.cuda.synchronize()
+    assert p.info.n_tile_items > 0
+    close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], "verify-64-rows")

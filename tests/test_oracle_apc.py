@@ -187,9 +187,9 @@ def test_extend_truncate_restores_pool():
 def test_no_blocks_leaves_pool_unchanged():
     pool = PrefixCacheOracle(4, 4, [0, 1, 2, 3])
     pool.add(0, list(range(12)))
-    snap = (pool.free_list(), dict(pool.index), list(pool.ref))
+    snap = (pool.free_list(), repr(pool.root), list(pool.ref))
     with pytest.raises(NoBlocksError):
         pool.add(1, list(range(100, 108)))
     with pytest.raises(NoBlocksError):
         pool.extend(0, list(range(8)))
-    assert (pool.free_list(), dict(pool.index), list(pool.ref)) == snap
+    assert (pool.free_list(), repr(pool.root), list(pool.ref)) == snap
