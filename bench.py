@@ -133,7 +133,7 @@ def main():
         dev.attend(p)
         if record is not None:
             record[1].record(stream)
-        dev.finish(launches[s])
+        dev.finish(launches[s], batched=True)
         return p
 
     for s in range(W):

@@ -115,6 +115,20 @@ int pa_seq_truncate(pa_pool* pool, int64_t seq_id, int32_t new_len);
  * Errors: PA_ERR_UNKNOWN_SEQ. */
 int pa_seq_free(pa_pool* pool, int64_t seq_id);
 
+/* Batched forms for a serving step: n operations applied in order, exactly as
+ * n calls of the single-sequence function would (sequence i owns tokens
+ * token_offsets[i] .. token_offsets[i+1]-1 of the concatenated `tokens`).
+ * They stop at the first failing operation, which leaves the pool as it was
+ * before that operation; *n_done (may be NULL) receives the number of
+ * operations applied.  n_cached_out (may be NULL) receives n entries. */
+int pa_seqs_add(pa_pool* pool, int32_t n, const int64_t* seq_ids, const int32_t* token_offsets,
+                const int32_t* tokens, int32_t* n_cached_out, int32_t* n_done);
+int pa_seqs_extend(pa_pool* pool, int32_t n, const int64_t* seq_ids,
+                   const int32_t* token_offsets, const int32_t* tokens, int32_t* n_done);
+int pa_seqs_truncate(pa_pool* pool, int32_t n, const int64_t* seq_ids, const int32_t* new_lens,
+                     int32_t* n_done);
+int pa_seqs_free(pa_pool* pool, int32_t n, const int64_t* seq_ids, int32_t* n_done);
+
 /* Current length of a live sequence.  Errors: PA_ERR_UNKNOWN_SEQ. */
 int pa_seq_len(const pa_pool* pool, int64_t seq_id, int32_t* len_out);
 

@@ -23,7 +23,8 @@ _CODES = {PA_ERR_ARG: "arg", PA_ERR_UNSUPPORTED: "unsupported", PA_ERR_NO_BLOCKS
 
 # Every symbol include/pa.h declares.
 EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy", "pa_seq_add",
-           "pa_seq_extend", "pa_seq_truncate", "pa_seq_free", "pa_seq_len", "pa_seq_blocks",
+           "pa_seq_extend", "pa_seq_truncate", "pa_seq_free", "pa_seqs_add", "pa_seqs_extend",
+           "pa_seqs_truncate", "pa_seqs_free", "pa_seq_len", "pa_seq_blocks",
            "pa_pool_free_list", "pa_build_metadata", "pa_attn_plan", "pa_kv_append",
            "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify"]
 
@@ -67,6 +68,10 @@ def lib():
         "pa_seq_extend": (C.c_int, [_P, i64, _I32P, i32]),
         "pa_seq_truncate": (C.c_int, [_P, i64, i32]),
         "pa_seq_free": (C.c_int, [_P, i64]),
+        "pa_seqs_add": (C.c_int, [_P, i32, _I64P, _I32P, _I32P, _I32P, _I32P]),
+        "pa_seqs_extend": (C.c_int, [_P, i32, _I64P, _I32P, _I32P, _I32P]),
+        "pa_seqs_truncate": (C.c_int, [_P, i32, _I64P, _I32P, _I32P]),
+        "pa_seqs_free": (C.c_int, [_P, i32, _I64P, _I32P]),
         "pa_seq_len": (C.c_int, [_P, i64, _I32P]),
         "pa_seq_blocks": (C.c_int, [_P, i64, _I32P, i32, _I32P]),
         "pa_pool_free_list": (C.c_int, [_P, _I32P, i32, _I32P]),
@@ -139,6 +144,32 @@ class Pool:
 
     def free(self, seq_id: int):
         _check(self._lib.pa_seq_free(self._h, int(seq_id)))
+
+    # -- batched forms (one library call per serving step) --------------------
+    def add_many(self, seq_ids, offsets, tokens):
+        """Admit len(seq_ids) sequences; returns reused-token counts (int32)."""
+        ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
+        off, tok = _i32(offsets), _i32(tokens)
+        out = np.zeros(ids.size, np.int32)
+        _check(self._lib.pa_seqs_add(self._h, ids.size, ids.ctypes.data_as(_I64P), _ptr(off),
+                                     _ptr(tok) if tok.size else None, _ptr(out), None))
+        return out
+
+    def extend_many(self, seq_ids, offsets, tokens):
+        ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
+        off, tok = _i32(offsets), _i32(tokens)
+        _check(self._lib.pa_seqs_extend(self._h, ids.size, ids.ctypes.data_as(_I64P), _ptr(off),
+                                        _ptr(tok) if tok.size else None, None))
+
+    def truncate_many(self, seq_ids, new_lens):
+        ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
+        nl = _i32(new_lens)
+        _check(self._lib.pa_seqs_truncate(self._h, ids.size, ids.ctypes.data_as(_I64P), _ptr(nl),
+                                          None))
+
+    def free_many(self, seq_ids):
+        ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
+        _check(self._lib.pa_seqs_free(self._h, ids.size, ids.ctypes.data_as(_I64P), None))
 
     def seq_len(self, seq_id: int) -> int:
         n = C.c_int32(0)

@@ -23,6 +23,7 @@ HOST_SOURCES = ["pool.cpp", "plan.cpp", "errors.cpp"]
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+CXX = os.environ.get("CXX", "g++")  # host-only sources (no device code)
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall"]
 # Packed-fp32 VALU forms are kept out of the generated code.
 HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
@@ -49,7 +50,7 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
             objs.append(o)
         for s in HOST_SOURCES:
             o = os.path.join(tmp, s + ".o")
-            cmds.append([HIPCC, *COMMON, "-c", os.path.join(CSRC, s), "-o", o])
+            cmds.append([CXX, *COMMON, "-c", os.path.join(CSRC, s), "-o", o])
             objs.append(o)
         with ThreadPoolExecutor(max_workers=jobs) as ex:
             outs = list(ex.map(_run, cmds))

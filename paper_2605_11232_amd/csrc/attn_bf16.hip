@@ -14,9 +14,10 @@
 //    in each lane, so the online-softmax row max / sum needs a single
 //    cross-lane exchange, and the probabilities are already laid out as the
 //    B operand of the PV product (no LDS round trip for P).
-//  * row items, one wavefront each: <= 48 rows (decode's G rows, verification's
-//    n_q * G rows) on 16x16x32 MFMA with K and V^T streamed straight from HBM
-//    into registers over a split of the key range.
+//  * row items, one wavefront each: <= 16 rows (decode's G rows; verification's
+//    n_q * G rows as several items over the same keys) on 16x16x32 MFMA with K
+//    and V^T streamed straight from HBM into registers over a split of the key
+//    range.
 //
 // The key order inside a tile is permuted so that each lane's eight PV
 // k-elements are eight consecutive keys: then V^T operands are single 16-byte
@@ -82,6 +83,9 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   const int qi = rho / G;
   const int hq = g * G + (rho - qi * G);
   const int apos = valid ? L - n + qi : -1;
+  // Rows are ordered by query, so the wave's first row has its smallest
+  // position: key tiles entirely at or below it need no causal mask.
+  const int wave_amin = L - n + (row0 + w * 32) / G;
 
   bf16x8 qf[D / 16];
   {
@@ -94,7 +98,11 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[dt][e] = 0.f;
-  float m = kNegInf, l = 0.f;
+  // Running reference max m (raw scores) and this lane's partial row sum l
+  // (the two lane halves hold disjoint keys of the same row; they are added
+  // at the end).  p = exp2(c * (s - m)) with c = scale * log2(e).
+  const float c = a.scale_log2;
+  float m = kNegInf, mc = 0.f, l = 0.f;
 
   const int32_t* bt = a.bt + (int64_t)r * a.max_blocks;
   const int64_t head_k = (int64_t)g * kBlock * D;  // offset of head g inside a K block
@@ -103,46 +111,42 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   const int64_t blk_v = (int64_t)a.hkv * D * kBlock;
 
   u32x4 kr[KCH], vr[VCH];
+  // Gather one 32-key tile (two blocks, ids read once per tile) into
+  // registers.  Every load is in bounds: a missing second block aliases the
+  // first; values of keys at or past kend are zeroed (never-written slots may
+  // hold anything), keys there are masked in the scores.
   auto load_tile = [&](int t0) {
+    const int jb = t0 / kBlock;
+    const int b0 = clamp_block(bt[min(jb, a.max_blocks - 1)], a.num_blocks);
+    const int b1 = t0 + 16 < kend ? clamp_block(bt[min(jb + 1, a.max_blocks - 1)], a.num_blocks) : b0;
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
-      const int c = tid + 256 * i;
-      const int kk = c / (D / 8), part8 = c % (D / 8);
-      const int key = t0 + kk;
-      if (key < kend) {
-        const int jb = min(key / kBlock, a.max_blocks - 1);
-        const int blk = clamp_block(bt[jb], a.num_blocks);
-        kr[i] = ld16(a.kc + blk * blk_k + head_k + (key % kBlock) * D + part8 * 8);
-      } else {
-        kr[i] = zero16();
-      }
+      const int c8 = tid + 256 * i;
+      const int kk = c8 / (D / 8), part8 = c8 % (D / 8);
+      const int blk = kk < 16 ? b0 : b1;
+      kr[i] = ld16(a.kc + blk * blk_k + head_k + (kk & 15) * D + part8 * 8);
     }
+    const bool tail = t0 + 32 > kend;
 #pragma unroll
     for (int i = 0; i < VCH; ++i) {
-      const int c = tid + 256 * i;
-      const int b = c / (2 * D), d = (c % (2 * D)) >> 1, half = c & 1;
-      const int key0 = t0 + 16 * b + 8 * half;
-      if (key0 < kend) {
-        const int jb = min(key0 / kBlock, a.max_blocks - 1);
-        const int blk = clamp_block(bt[jb], a.num_blocks);
-        u32x4 x = ld16(a.vc + blk * blk_v + head_v + d * kBlock + 8 * half);
-        vr[i] = (key0 + 8 > kend) ? keep_bf16(x, kend - key0) : x;
-      } else {
-        vr[i] = zero16();
-      }
+      const int c8 = tid + 256 * i;
+      const int b = c8 / (2 * D), d = (c8 % (2 * D)) >> 1, half = c8 & 1;
+      u32x4 x = ld16(a.vc + (b ? b1 : b0) * blk_v + head_v + d * kBlock + 8 * half);
+      if (tail) x = keep_bf16(x, min(max(kend - (t0 + 16 * b + 8 * half), 0), 8));
+      vr[i] = x;
     }
   };
   auto store_tile = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
-      const int c = tid + 256 * i;
-      const int kk = c / (D / 8), part8 = c % (D / 8);
+      const int c8 = tid + 256 * i;
+      const int kk = c8 / (D / 8), part8 = c8 % (D / 8);
       st16(&sm.k[buf][perm32(kk) * TileSmem<D>::KS + part8 * 8], kr[i]);
     }
 #pragma unroll
     for (int i = 0; i < VCH; ++i) {
-      const int c = tid + 256 * i;
-      const int b = c / (2 * D), d = (c % (2 * D)) >> 1, half = c & 1;
+      const int c8 = tid + 256 * i;
+      const int b = c8 / (2 * D), d = (c8 % (2 * D)) >> 1, half = c8 & 1;
       st16(&sm.v[buf][d * TileSmem<D>::VS + 16 * b + 8 * half], vr[i]);
     }
   };
@@ -168,27 +172,39 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
     for (int ks = 0; ks < D / 16; ++ks)
       s = mfma32(as_bf16x8(ld16(kb + 16 * ks)), qf[ks], s);
 
-    float mx = kNegInf;
+    if (t0 + 31 > wave_amin) {  // wave-uniform: only diagonal / tail tiles
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = t0 + perm32(8 * (e >> 2) + 4 * hh + (e & 3));
-      const float v = key <= apos ? s[e] * a.scale_log2 : kNegInf;
-      s[e] = v;
-      mx = fmaxf(mx, v);
+      for (int e = 0; e < 16; ++e) {
+        const int key = t0 + perm32(8 * (e >> 2) + 4 * hh + (e & 3));
+        s[e] = key <= apos ? s[e] : kNegInf;
+      }
     }
+    float mx = fmaxf(fmaxf(s[0], s[1]), s[2]);
+#pragma unroll
+    for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[e]), s[e + 1]);
+    mx = fmaxf(mx, s[15]);
     mx = fmaxf(mx, wave_xor(mx, 32));
-    const float mnew = fmaxf(m, mx);
-    const float mb = mnew == kNegInf ? 0.f : mnew;
-    const float alpha = exp2f(m - mb);
-    float ps = 0.f;
+    // Move the reference max only when a score exceeds it by more than 2^8
+    // (probabilities stay <= 256, exact for float32 sums and bf16 operands);
+    // the decision is taken for the whole wavefront so the rescale is skipped
+    // by every lane together.
+    if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
+      const float mnew = fmaxf(m, mx);
+      const float mcn = mnew == kNegInf ? 0.f : mnew * c;
+      const float alpha = m == kNegInf ? 0.f : exp2f(mc - mcn);
+      l *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
+      m = mnew;
+      mc = mcn;
+    }
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      s[e] = exp2f(s[e] - mb);
-      ps += s[e];
+      s[e] = exp2f(fmaf(s[e], c, -mc));
+      l += s[e];
     }
-    ps += wave_xor(ps, 32);
-    l = l * alpha + ps;
-    m = mnew;
     bf16x8 pb0, pb1;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -197,8 +213,6 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
     }
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
       const __bf16* vb = &sm.v[buf][(32 * dt + j) * TileSmem<D>::VS + 8 * hh];
       acc[dt] = mfma32(as_bf16x8(ld16(vb)), pb0, acc[dt]);
       acc[dt] = mfma32(as_bf16x8(ld16(vb + 16)), pb1, acc[dt]);
@@ -207,9 +221,10 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
     __syncthreads();
   }
 
+  l += wave_xor(l, 32);
   if (!valid) return;
   const float inv = l > 0.f ? 1.f / l : 0.f;
-  const float lse_v = l > 0.f ? kLn2 * (m + __log2f(l)) : kNegInf;
+  const float lse_v = l > 0.f ? kLn2 * (mc + __log2f(l)) : kNegInf;
   if (part < 0) {
     __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D;
 #pragma unroll
@@ -239,8 +254,10 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   }
 }
 
-// Row item: one wavefront, NT 16-column tiles of rows, keys [kv0, kv1).
-template <int D, int NT>
+// Row item: one wavefront, up to 16 rows (one 16-column MFMA tile), keys
+// [kv0, kv1).  Rows beyond 16 (verification: n_q * G) are separate items over
+// the same keys, placed next to each other so their loads meet in cache.
+template <int D>
 __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   constexpr int KS = D / 32;  // k-steps of the QK product (32 dims each)
   constexpr int DT = D / 16;  // 16-row tiles of O^T
@@ -254,26 +271,24 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   const int kv1 = min(it[I_KV1], L);
   const int G = a.group;
 
-  int apos[NT], qi[NT], hq[NT];
-  bf16x8 qf[NT][KS];
-  f32x4 acc[DT][NT];
-  float m[NT], l[NT];
+  const bool valid = j < nrows;
+  const int rho = row0 + j;
+  const int qi = rho / G;
+  const int hq = g * G + (rho - qi * G);
+  const int apos = valid ? L - n + qi : -1;
+  const int amin = L - n + row0 / G;  // smallest position among the item's rows
+
+  bf16x8 qf[KS];
+  {
+    const __bf16* qp = a.q + ((int64_t)(qs + qi) * a.hq + hq) * D + 8 * g4;
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int lr = 16 * nt + j;
-    const bool valid = lr < nrows;
-    const int rho = row0 + lr;
-    qi[nt] = rho / G;
-    hq[nt] = g * G + (rho - qi[nt] * G);
-    apos[nt] = valid ? L - n + qi[nt] : -1;
-    const __bf16* qp = a.q + ((int64_t)(qs + qi[nt]) * a.hq + hq[nt]) * D + 8 * g4;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[nt][ks] = as_bf16x8(valid ? ld16(qp + 32 * ks) : zero16());
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) acc[dt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m[nt] = kNegInf;
-    l[nt] = 0.f;
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = as_bf16x8(valid ? ld16(qp + 32 * ks) : zero16());
   }
+  f32x4 acc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const float c = a.scale_log2;
+  float m = kNegInf, mc = 0.f, l = 0.f;
 
   const int32_t* bt = a.bt + (int64_t)r * a.max_blocks;
   const int64_t blk_k = (int64_t)a.hkv * kBlock * D, head_k = (int64_t)g * kBlock * D;
@@ -284,7 +299,8 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   // One register set for K and one for V^T: the next step's K loads are
   // issued as soon as the score MFMAs have consumed K, and its V^T loads as
   // soon as the PV MFMAs have consumed V^T, so HBM reads overlap the softmax
-  // and the MFMAs of the current step.
+  // and the MFMAs of the current step.  All loads are in bounds (a missing
+  // second block aliases the first).
   u32x4 kreg[2][KS], vreg[DT];
   int b0 = 0, b1 = 0;
   auto blocks_of = [&](int t0) {
@@ -302,110 +318,101 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
       for (int ks = 0; ks < KS; ++ks) kreg[tt][ks] = ld16(p + 32 * ks);
     }
   };
-  auto load_v = [&](int t0) {
-    const int blk = g4 < 2 ? b0 : b1;
-    const int key0 = t0 + 8 * g4;
-    const __bf16* p = a.vc + blk * blk_v + head_v + j * kBlock + 8 * (g4 & 1);
+  auto load_v = [&]() {
+    const __bf16* p = a.vc + (g4 < 2 ? b0 : b1) * blk_v + head_v + j * kBlock + 8 * (g4 & 1);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      u32x4 x = ld16(p + 16 * kBlock * dt);
-      vreg[dt] = key0 >= kv1 ? zero16() : (key0 + 8 > kv1 ? keep_bf16(x, kv1 - key0) : x);
-    }
+    for (int dt = 0; dt < DT; ++dt) vreg[dt] = ld16(p + 16 * kBlock * dt);
   };
 
   if (kv0 < kv1) {
     blocks_of(kv0);
     load_k();
-    load_v(kv0);
+    load_v();
   }
   for (int t0 = kv0; t0 < kv1; t0 += 32) {
     const bool more = t0 + 32 < kv1;
-    f32x4 s[2][NT];
+    f32x4 s[2];
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
+    for (int tt = 0; tt < 2; ++tt) {
+      f32x4 acc_s = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) c = mfma16(as_bf16x8(kreg[tt][ks]), qf[nt][ks], c);
-        s[tt][nt] = c;
-      }
+      for (int ks = 0; ks < KS; ++ks) acc_s = mfma16(as_bf16x8(kreg[tt][ks]), qf[ks], acc_s);
+      s[tt] = acc_s;
+    }
     if (more) {
       blocks_of(t0 + 32);
       load_k();
     }
-    bf16x8 pb[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      float mx = kNegInf;
+    // Lane (j, g4), element e of score tile tt holds key t0 + 8 g4 + 4 tt + e.
+    const bool masked = t0 + 31 > amin || !more;  // wave-uniform
+    if (masked) {
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int key = t0 + 8 * g4 + 4 * tt + e;
-          const float v = (key <= apos[nt] && key < kv1) ? s[tt][nt][e] * a.scale_log2 : kNegInf;
-          s[tt][nt][e] = v;
-          mx = fmaxf(mx, v);
+          s[tt][e] = (key <= apos && key < kv1) ? s[tt][e] : kNegInf;
         }
-      mx = fmaxf(mx, wave_xor(mx, 16));
-      mx = fmaxf(mx, wave_xor(mx, 32));
-      const float mnew = fmaxf(m[nt], mx);
-      const float mb = mnew == kNegInf ? 0.f : mnew;
-      const float alpha = exp2f(m[nt] - mb);
-      float ps = 0.f;
+      // zero values of keys at or past kv1 (slots that may never have been written)
+      const int keep = min(max(kv1 - (t0 + 8 * g4), 0), 8);
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float p = exp2f(s[tt][nt][e] - mb);
-          ps += p;
-          pb[nt][4 * tt + e] = (__bf16)p;
-        }
-      ps += wave_xor(ps, 16);
-      ps += wave_xor(ps, 32);
-      l[nt] = l[nt] * alpha + ps;
-      m[nt] = mnew;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) acc[dt][nt] *= alpha;
+      for (int dt = 0; dt < DT; ++dt) vreg[dt] = keep_bf16(vreg[dt], keep);
     }
+    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3]));
+    mx = fmaxf(mx, fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+    mx = fmaxf(mx, wave_xor(mx, 16));
+    mx = fmaxf(mx, wave_xor(mx, 32));
+    if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
+      const float mnew = fmaxf(m, mx);
+      const float mcn = mnew == kNegInf ? 0.f : mnew * c;
+      const float alpha = m == kNegInf ? 0.f : exp2f(mc - mcn);
+      l *= alpha;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const bf16x8 vf = as_bf16x8(vreg[dt]);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[dt][nt] = mfma16(vf, pb[nt], acc[dt][nt]);
+      for (int dt = 0; dt < DT; ++dt) acc[dt] *= alpha;
+      m = mnew;
+      mc = mcn;
     }
-    if (more) load_v(t0 + 32);
+    bf16x8 pb;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p = exp2f(fmaf(s[tt][e], c, -mc));
+        l += p;
+        pb[4 * tt + e] = (__bf16)p;
+      }
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt] = mfma16(as_bf16x8(vreg[dt]), pb, acc[dt]);
+    if (more) load_v();
   }
 
+  l += wave_xor(l, 16);
+  l += wave_xor(l, 32);
+  if (!valid) return;
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  const float lse_v = l > 0.f ? kLn2 * (mc + __log2f(l)) : kNegInf;
+  if (part < 0) {
+    __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D + 4 * g4;
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int lr = 16 * nt + j;
-    if (lr >= nrows) continue;
-    const float inv = l[nt] > 0.f ? 1.f / l[nt] : 0.f;
-    const float lse_v = l[nt] > 0.f ? kLn2 * (m[nt] + __log2f(l[nt])) : kNegInf;
-    if (part < 0) {
-      __bf16* op = a.out + ((int64_t)(qs + qi[nt]) * a.hq + hq[nt]) * D + 4 * g4;
+    for (int dt = 0; dt < DT; ++dt) {
+      __bf16 o4[4];
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        __bf16 o4[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o4[e] = (__bf16)(acc[dt][nt][e] * inv);
-        *reinterpret_cast<u32x2*>(op + 16 * dt) = __builtin_bit_cast(u32x2, o4);
-      }
-      if (a.lse && g4 == 0) a.lse[(int64_t)(qs + qi[nt]) * a.hq + hq[nt]] = lse_v;
-    } else {
-      float* op = a.ws_o + (int64_t)(part + lr) * D + 4 * g4;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4*>(op + 16 * dt) = acc[dt][nt] * inv;
-      if (g4 == 0) a.ws_lse[part + lr] = lse_v;
+      for (int e = 0; e < 4; ++e) o4[e] = (__bf16)(acc[dt][e] * inv);
+      *reinterpret_cast<u32x2*>(op + 16 * dt) = __builtin_bit_cast(u32x2, o4);
     }
+    if (a.lse && g4 == 0) a.lse[(int64_t)(qs + qi) * a.hq + hq] = lse_v;
+  } else {
+    float* op = a.ws_o + (int64_t)(part + j) * D + 4 * g4;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4*>(op + 16 * dt) = acc[dt] * inv;
+    if (g4 == 0) a.ws_lse[part + j] = lse_v;
   }
 }
 
 // MIX: 1 = tile items only, 2 = row items only, 3 = both (a mixed launch).
 // Separate instantiations keep a pure prefill or pure decode launch from
 // paying the other path's registers and LDS.
-template <int D, int NT, int MIX>
+template <int D, int MIX>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const int32_t* plan = a.plan;
   const int n_tile = plan[H_N_TILE];
@@ -420,7 +427,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   if constexpr (MIX & 2) {
     const int idx = 4 * (b - n_tile) + (threadIdx.x >> 6);
     if (b >= n_tile && idx < plan[H_N_ROW])
-      row_item<D, NT>(plan + plan[H_ROW_OFF] + idx * kItemWords, a);
+      row_item<D>(plan + plan[H_ROW_OFF] + idx * kItemWords, a);
   }
 }
 
@@ -468,7 +475,7 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
                      const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
                      const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
                      const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
-                     int32_t nt, int64_t partial_rows, void* ws, void* out, float* lse,
+                     int64_t partial_rows, void* ws, void* out, float* lse,
                      hipStream_t stream) {
   AttnArgs a;
   a.q = static_cast<const __bf16*>(q);
@@ -490,18 +497,13 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
   a.scale_log2 = scale * kLog2e;
   if (grid > 0) {
     const int mix = (n_tile > 0 ? 1 : 0) | (grid > n_tile ? 2 : 0);
-#define PA_LAUNCH(DD, NN, MM) \
-  hipLaunchKernelGGL((attn_bf16_kernel<DD, NN, MM>), dim3(grid), dim3(256), 0, stream, a)
-#define PA_LAUNCH_D(DD)                                          \
-  do {                                                           \
-    if (mix == 1) PA_LAUNCH(DD, 1, 1);                           \
-    else if (nt <= 1) { if (mix == 2) PA_LAUNCH(DD, 1, 2); else PA_LAUNCH(DD, 1, 3); } \
-    else if (nt == 2) { if (mix == 2) PA_LAUNCH(DD, 2, 2); else PA_LAUNCH(DD, 2, 3); } \
-    else { if (mix == 2) PA_LAUNCH(DD, 3, 2); else PA_LAUNCH(DD, 3, 3); } \
-  } while (0)
-    if (d == 128) PA_LAUNCH_D(128);
-    else PA_LAUNCH_D(64);
-#undef PA_LAUNCH_D
+#define PA_LAUNCH(DD, MM) \
+  hipLaunchKernelGGL((attn_bf16_kernel<DD, MM>), dim3(grid), dim3(256), 0, stream, a)
+    if (d == 128) {
+      if (mix == 1) PA_LAUNCH(128, 1); else if (mix == 2) PA_LAUNCH(128, 2); else PA_LAUNCH(128, 3);
+    } else {
+      if (mix == 1) PA_LAUNCH(64, 1); else if (mix == 2) PA_LAUNCH(64, 2); else PA_LAUNCH(64, 3);
+    }
 #undef PA_LAUNCH
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return static_cast<int>(e);

@@ -4,11 +4,12 @@
 // every row of an item reads the same keys and values (grouped-query
 // attention).  Sequences with many rows (suffix prefill, prefill chunks) are
 // cut into 128-row tile items, each a workgroup of four wavefronts sharing
-// key/value tiles through LDS.  Sequences with at most 48 rows (decode: G rows;
-// verification: n_q * G rows) become single-wavefront row items whose key range
-// is split so the launch has enough wavefronts in flight to stream the cache at
-// HBM bandwidth; their partial results are combined by log-sum-exp in a merge
-// pass.  Paper: Section 5.2 (split prefills under a batched-token budget, mixed
+// key/value tiles through LDS.  Sequences with at most 64 rows (decode: G rows;
+// verification: n_q * G rows) become single-wavefront row items of up to 16
+// rows whose key range is split so the launch has enough wavefronts in flight
+// to stream the cache at HBM bandwidth; the row groups of one key range sit
+// next to each other so their loads meet in cache, and split partial results
+// are combined by log-sum-exp in a merge pass.  Paper: Section 5.2 (split prefills under a batched-token budget, mixed
 // prefill and decode), Section 6, Table "playbook" (long prefills blocking
 // short decodes).
 //
@@ -114,7 +115,6 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   std::vector<std::vector<Item>> tile_q(kXcds), row_q(kXcds);
   std::vector<std::array<int32_t, pa::kGroupWords>> groups;
   int64_t partial_rows = 0;
-  int32_t nt_max = 0;
   int64_t n_tile = 0, n_row_real = 0;
 
   if (dtype == PA_BF16) {
@@ -123,7 +123,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     int64_t row_keys = 0;
     for (int32_t r = 0; r < n_seqs; ++r) {
       const int32_t n = cu_seqlens_q[r + 1] - cu_seqlens_q[r];
-      if (n > 0 && n * G <= pa::kRowItemMaxRows) row_keys += int64_t(seq_lens[r]) * num_kv_heads;
+      if (n > 0 && n * G <= pa::kRowSeqRows)
+        row_keys += int64_t(seq_lens[r]) * num_kv_heads * cdiv(n * G, pa::kRowItemRows);
     }
     const int64_t target_waves = int64_t(num_cus) * 16;
     int64_t chunk = std::max<int64_t>(256, cdiv(row_keys, std::max<int64_t>(1, target_waves)));
@@ -136,29 +137,37 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       const int32_t L = seq_lens[r];
       if (n == 0) continue;
       const int32_t rows = n * G;
-      if (rows <= pa::kRowItemMaxRows) {
-        nt_max = std::max<int32_t>(nt_max, static_cast<int32_t>(cdiv(rows, 16)));
+      if (rows <= pa::kRowSeqRows) {
         const int32_t nsplit = static_cast<int32_t>(std::max<int64_t>(1, cdiv(L, chunk)));
         // equal key ranges, multiples of the key step, covering [0, L)
         const int64_t per = cdiv(cdiv(L, nsplit), pa::kKeyStep) * pa::kKeyStep;
+        int32_t used = 0;
+        while (used < nsplit && int64_t(used) * per < L) ++used;
         for (int32_t g = 0; g < num_kv_heads; ++g) {
+          // per split, the row groups back to back
           std::vector<Item> its;
-          int32_t used = 0;
-          for (int32_t s = 0; s < nsplit; ++s) {
+          std::vector<int32_t> base;
+          for (int32_t row0 = 0; row0 < rows; row0 += pa::kRowItemRows) {
+            const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
+            base.push_back(used > 1 ? int32_t(partial_rows) : -1);
+            if (used > 1) {
+              groups.push_back({r, g, row0, nr, used, int32_t(partial_rows), 0, 0});
+              partial_rows += int64_t(used) * nr;
+            }
+          }
+          for (int32_t s = 0; s < used; ++s) {
             const int64_t k0 = s * per, k1 = std::min<int64_t>(L, (s + 1) * per);
-            if (k0 >= k1) break;
-            Item it{};
-            it.w = {r, g, 0, rows, int32_t(k0), int32_t(k1), -1, 0};
-            it.cost = k1 - k0;
-            its.push_back(it);
-            ++used;
+            int32_t gi = 0;
+            for (int32_t row0 = 0; row0 < rows; row0 += pa::kRowItemRows, ++gi) {
+              const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
+              Item it{};
+              it.w = {r, g, row0, nr, int32_t(k0), int32_t(k1),
+                      base[gi] < 0 ? -1 : int32_t(base[gi] + int64_t(s) * nr), 0};
+              it.cost = k1 - k0;
+              its.push_back(it);
+              ++n_row_real;
+            }
           }
-          if (used > 1) {
-            for (int32_t s = 0; s < used; ++s) its[s].w[pa::I_PART] = int32_t(partial_rows + int64_t(s) * rows);
-            groups.push_back({r, g, 0, rows, used, int32_t(partial_rows), 0, 0});
-            partial_rows += int64_t(used) * rows;
-          }
-          n_row_real += used;
           head_rows[g].push_back(std::move(its));
         }
       } else {
@@ -241,7 +250,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   info->n_merge_rows = 0;
   for (auto& g : groups) info->n_merge_rows += g[pa::G_NROWS];
   info->grid = int32_t(grid);
-  info->variant = dtype == PA_F32 ? 0 : nt_max;
+  info->variant = dtype == PA_F32 ? 0 : 1;
   info->plan_words = words;
   info->workspace_bytes = partial_rows * int64_t(head_dim + 1) * int64_t(sizeof(float));
   if (!plan) return PA_OK;
@@ -261,7 +270,6 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   h[pa::H_D] = head_dim;
   h[pa::H_N_SEQS] = n_seqs;
   h[pa::H_TOTAL_Q] = total_q;
-  h[pa::H_NT] = nt_max;
   h[pa::H_TILE_OFF] = int32_t(tile_off);
   h[pa::H_ROW_OFF] = int32_t(row_off);
   h[pa::H_GROUP_OFF] = int32_t(group_off);

@@ -13,7 +13,7 @@ enum : int32_t {
   H_MAGIC = 0,
   H_KIND,
   H_N_TILE,        // 128-row items, one workgroup each
-  H_N_ROW,         // <= kRowItemMaxRows-row items, one wavefront each (multiple of 4, padded)
+  H_N_ROW,         // <= kRowItemRows-row items, one wavefront each (multiple of 4, padded)
   H_N_GROUPS,      // split groups combined by the merge kernel
   H_GRID,          // workgroups of the attention launch = N_TILE + N_ROW / 4
   H_HQ,
@@ -21,7 +21,7 @@ enum : int32_t {
   H_D,
   H_N_SEQS,
   H_TOTAL_Q,
-  H_NT,            // 16-column MFMA tiles a row item needs (1..3; 0 if none)
+  H_RESERVED,
   H_TILE_OFF,      // word offset of the tile items
   H_ROW_OFF,       // word offset of the row items
   H_GROUP_OFF,     // word offset of the split groups
@@ -46,8 +46,9 @@ enum : int32_t {
   kGroupWords = 8
 };
 
-constexpr int32_t kTileRows = 128;       // rows per tile item (4 waves x 32)
-constexpr int32_t kRowItemMaxRows = 48;  // rows a single-wave item can hold (3 x 16)
+constexpr int32_t kTileRows = 128;    // rows per tile item (4 waves x 32)
+constexpr int32_t kRowItemRows = 16;  // rows per single-wave item (one 16-column MFMA tile)
+constexpr int32_t kRowSeqRows = 64;   // sequences with at most this many rows use row items
 constexpr int32_t kKeyStep = 32;         // keys per inner iteration
 
 }  // namespace pa

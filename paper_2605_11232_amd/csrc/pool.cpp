@@ -217,6 +217,65 @@ int pa_seq_free(pa_pool* pool, int64_t seq_id) {
   return PA_OK;
 }
 
+}  // extern "C"
+
+namespace {
+template <class F>
+int batch(const char* fn, int32_t n, const int64_t* seq_ids, int32_t* n_done, F&& op) {
+  if (n_done) *n_done = 0;
+  if (n < 0 || (n > 0 && !seq_ids)) return pa::fail(PA_ERR_ARG, "%s: invalid batch", fn);
+  for (int32_t i = 0; i < n; ++i) {
+    const int rc = op(i);
+    if (rc != PA_OK) return rc;
+    if (n_done) *n_done = i + 1;
+  }
+  return PA_OK;
+}
+
+bool offsets_ok(int32_t n, const int32_t* off, const int32_t* tokens) {
+  if (n == 0) return true;
+  if (!off || off[0] != 0) return false;
+  for (int32_t i = 0; i < n; ++i)
+    if (off[i + 1] < off[i]) return false;
+  return off[n] == 0 || tokens != nullptr;
+}
+}  // namespace
+
+extern "C" {
+
+int pa_seqs_add(pa_pool* pool, int32_t n, const int64_t* seq_ids, const int32_t* token_offsets,
+                const int32_t* tokens, int32_t* n_cached_out, int32_t* n_done) {
+  if (!offsets_ok(n, token_offsets, tokens))
+    return pa::fail(PA_ERR_ARG, "pa_seqs_add: invalid token offsets");
+  return batch("pa_seqs_add", n, seq_ids, n_done, [&](int32_t i) {
+    return pa_seq_add(pool, seq_ids[i], tokens + token_offsets[i],
+                      token_offsets[i + 1] - token_offsets[i],
+                      n_cached_out ? n_cached_out + i : nullptr);
+  });
+}
+
+int pa_seqs_extend(pa_pool* pool, int32_t n, const int64_t* seq_ids,
+                   const int32_t* token_offsets, const int32_t* tokens, int32_t* n_done) {
+  if (!offsets_ok(n, token_offsets, tokens))
+    return pa::fail(PA_ERR_ARG, "pa_seqs_extend: invalid token offsets");
+  return batch("pa_seqs_extend", n, seq_ids, n_done, [&](int32_t i) {
+    return pa_seq_extend(pool, seq_ids[i], tokens + token_offsets[i],
+                         token_offsets[i + 1] - token_offsets[i]);
+  });
+}
+
+int pa_seqs_truncate(pa_pool* pool, int32_t n, const int64_t* seq_ids, const int32_t* new_lens,
+                     int32_t* n_done) {
+  if (n > 0 && !new_lens) return pa::fail(PA_ERR_ARG, "pa_seqs_truncate: NULL new_lens");
+  return batch("pa_seqs_truncate", n, seq_ids, n_done,
+               [&](int32_t i) { return pa_seq_truncate(pool, seq_ids[i], new_lens[i]); });
+}
+
+int pa_seqs_free(pa_pool* pool, int32_t n, const int64_t* seq_ids, int32_t* n_done) {
+  return batch("pa_seqs_free", n, seq_ids, n_done,
+               [&](int32_t i) { return pa_seq_free(pool, seq_ids[i]); });
+}
+
 int pa_seq_len(const pa_pool* pool, int64_t seq_id, int32_t* len_out) {
   pa::clear_error();
   if (!pool || !len_out) return pa::fail(PA_ERR_ARG, "pa_seq_len: NULL argument");

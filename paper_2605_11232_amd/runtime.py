@@ -26,6 +26,33 @@ class Prepared:
         self.__dict__.update(kw)
 
 
+def batch_ops(ops):
+    """Group consecutive add/extend/free/truncate ops into batched calls
+    (computed once per launch and cached on it)."""
+    groups = []
+    for op in ops:
+        if op.kind == "write_kv" or not groups or groups[-1][0] != op.kind:
+            groups.append((op.kind, [op]))
+        else:
+            groups[-1][1].append(op)
+    packed = []
+    for kind, g in groups:
+        if kind == "write_kv":
+            packed.append((kind, g[0]))
+            continue
+        ids = np.array([op.seq_id for op in g], dtype=np.int64)
+        if kind in ("add", "extend"):
+            lens = np.array([len(op.tokens) for op in g], dtype=np.int32)
+            off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+            toks = np.concatenate([op.tokens for op in g]).astype(np.int32)
+            packed.append((kind, (ids, off, toks)))
+        elif kind == "truncate":
+            packed.append((kind, (ids, np.array([op.n for op in g], dtype=np.int32))))
+        else:
+            packed.append((kind, (ids,)))
+    return packed
+
+
 class Staging:
     """Pinned host buffers and device buffers for one launch's metadata and
     plan.  The host fills the pinned buffers while the GPU still works on an
@@ -88,6 +115,24 @@ class DeviceReplay:
         else:
             raise ValueError(op.kind)
 
+    def apply_batched(self, launch, which: str):
+        cache = launch.__dict__.setdefault("_batched", {})
+        if which not in cache:
+            cache[which] = batch_ops(getattr(launch, which))
+        p = self.pool
+        for kind, args in cache[which]:
+            if kind == "add":
+                hits = p.add_many(*args)
+                self.n_cached.update(zip(args[0].tolist(), hits.tolist()))
+            elif kind == "extend":
+                p.extend_many(*args)
+            elif kind == "truncate":
+                p.truncate_many(*args)
+            elif kind == "free":
+                p.free_many(*args)
+            else:
+                self.apply(args)
+
     def setup(self):
         for op in self.wl.setup:
             self.apply(op)
@@ -139,10 +184,10 @@ class DeviceReplay:
 
     def prepare_staged(self, launch, st: Staging, q, k_new, v_new, out, lse) -> Prepared:
         """Like ``prepare`` but through preallocated pinned/device buffers with
-        asynchronous copies, so host bookkeeping overlaps earlier GPU work."""
+        asynchronous copies and batched pool calls, so host bookkeeping
+        overlaps earlier GPU work."""
         self.n_cached = {}
-        for op in launch.pre:
-            self.apply(op)
+        self.apply_batched(launch, "pre")
         cfg = self.cfg
         n = len(launch.seq_ids)
         T = launch.total_q
@@ -187,6 +232,9 @@ class DeviceReplay:
         self.attend(p)
         return p
 
-    def finish(self, launch):
+    def finish(self, launch, batched: bool = False):
+        if batched:
+            self.apply_batched(launch, "post")
+            return
         for op in launch.post:
             self.apply(op)

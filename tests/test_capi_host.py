@@ -242,3 +242,43 @@ def test_plan_rejects_inconsistent_lengths():
         B.plan(B.KIND_PREFILL, 0, [3], [0, 2], 8, 3, 128, 16, B.PA_BF16)
     _, info = B.plan(B.KIND_PREFILL, 0, [], [0], 8, 2, 128, 16, B.PA_BF16)
     assert info.grid == 0 and info.workspace_bytes == 0
+
+
+def test_batched_pool_calls_match_single_calls():
+    """pa_seqs_* apply the single-sequence operations in order; a failing
+    operation stops the batch and leaves the pool as before that operation."""
+    r = np.random.default_rng(9)
+    bs, nb = 4, 60
+    order = r.permutation(nb).tolist()
+    o = PrefixCacheOracle(nb, bs, order)
+    lib_pool = B.Pool(nb, bs, order)
+    prefix = list(range(100, 112))
+    reqs = [prefix + r.integers(0, 9, size=int(r.integers(1, 9))).tolist() for _ in range(6)]
+    hits_o = [o.add(i, t) for i, t in enumerate(reqs)]
+    off = np.concatenate([[0], np.cumsum([len(t) for t in reqs])])
+    hits_l = lib_pool.add_many(list(range(6)), off, np.concatenate(reqs))
+    assert hits_o == hits_l.tolist()
+    ext = [r.integers(0, 9, size=int(r.integers(0, 6))).tolist() for _ in range(6)]
+    for i, t in enumerate(ext):
+        o.extend(i, t)
+    off = np.concatenate([[0], np.cumsum([len(t) for t in ext])])
+    lib_pool.extend_many(list(range(6)), off, np.concatenate(ext) if sum(map(len, ext)) else [])
+    new_lens = [len(reqs[i]) for i in range(6)]
+    for i in range(6):
+        o.truncate(i, new_lens[i])
+    lib_pool.truncate_many(list(range(6)), new_lens)
+    assert o.free_list() == lib_pool.free_list()
+    md_o = o.metadata(list(range(6)), [1] * 6, 16)
+    md_l = lib_pool.metadata(list(range(6)), [1] * 6, 16)
+    for k in md_o:
+        np.testing.assert_array_equal(md_o[k], md_l[k])
+    # a batch whose third operation fails: two applied, pool otherwise intact
+    n_done = ctypes.c_int32(-1)
+    ids = np.array([0, 1, 999, 2], dtype=np.int64)
+    rc = B.lib().pa_seqs_free(lib_pool._h, 4, ids.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                              ctypes.byref(n_done))
+    assert rc == B.PA_ERR_UNKNOWN_SEQ and n_done.value == 2
+    o.free_seq(0)
+    o.free_seq(1)
+    assert o.free_list() == lib_pool.free_list()
+    assert lib_pool.seq_len(2) == o.seq_len(2)

@@ -220,14 +220,16 @@ def test_edge_cases():
         torch.cuda.synchronize()
         if sum(ql):
             close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"edge{ci}")
-    # verify with n_q = 8 and G = 8: 64 rows per sequence -> tile items
-    cfg8 = synth.AttnConfig("edge8", "bf16", 16, 2, 128, 16, 78)
-    setup, launch = mk([8, 8], [40, 517], 9, cfg=cfg8)
-    wl = synth.Workload(cfg8, 128, np.arange(128, dtype=np.int32), setup, [launch], None, 40)
-    o = OracleReplay(wl).setup()
-    dv = DeviceReplay(wl, kind="verify").setup()
-    ro = o.launch(wl.launches[0])
-    p = dv.run(wl.launches[0])
-    torch.cuda.synchronize()
-    assert p.info.n_tile_items > 0
-    close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], "verify-64-rows")
+    # verify with n_q = 8: G = 8 gives 64 rows per sequence (four 16-row
+    # items over the same keys); G = 16 gives 128 rows (one tile item)
+    for G, want_tiles in ((8, False), (16, True)):
+        cfg8 = synth.AttnConfig(f"edge-g{G}", "bf16", 2 * G, 2, 128, 16, 78)
+        setup, launch = mk([8, 8], [40, 517], 9, cfg=cfg8)
+        wl = synth.Workload(cfg8, 128, np.arange(128, dtype=np.int32), setup, [launch], None, 40)
+        o = OracleReplay(wl).setup()
+        dv = DeviceReplay(wl, kind="verify").setup()
+        ro = o.launch(wl.launches[0])
+        p = dv.run(wl.launches[0])
+        torch.cuda.synchronize()
+        assert (p.info.n_tile_items > 0) == want_tiles
+        close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"verify-G{G}")
