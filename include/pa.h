@@ -129,6 +129,20 @@ int pa_seqs_truncate(pa_pool* pool, int32_t n, const int64_t* seq_ids, const int
                      int32_t* n_done);
 int pa_seqs_free(pa_pool* pool, int32_t n, const int64_t* seq_ids, int32_t* n_done);
 
+/* A serving step's pool operations of mixed kinds in one call: operation i
+ * applies ops[i] to seq_ids[i] exactly as the single-sequence function would;
+ * PA_OP_ADD / PA_OP_EXTEND take tokens token_offsets[i] .. token_offsets[i+1]-1
+ * (token_offsets has n+1 entries; other kinds own an empty range),
+ * PA_OP_TRUNCATE takes new_lens[i] (new_lens may be NULL if there is none),
+ * PA_OP_FREE takes nothing.  n_cached_out[i] (may be NULL) receives the
+ * reused-token count of an admission, 0 otherwise.  Stops at the first
+ * failing operation (pool as before that operation); *n_done (may be NULL)
+ * receives the number applied. */
+typedef enum { PA_OP_ADD = 0, PA_OP_EXTEND = 1, PA_OP_TRUNCATE = 2, PA_OP_FREE = 3 } pa_op;
+int pa_pool_apply(pa_pool* pool, int32_t n, const int32_t* ops, const int64_t* seq_ids,
+                  const int32_t* token_offsets, const int32_t* tokens, const int32_t* new_lens,
+                  int32_t* n_cached_out, int32_t* n_done);
+
 /* Current length of a live sequence.  Errors: PA_ERR_UNKNOWN_SEQ. */
 int pa_seq_len(const pa_pool* pool, int64_t seq_id, int32_t* len_out);
 

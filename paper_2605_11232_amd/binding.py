@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libpa.so")
 PA_OK, PA_ERR_ARG, PA_ERR_UNSUPPORTED, PA_ERR_NO_BLOCKS, PA_ERR_UNKNOWN_SEQ, PA_ERR_LAUNCH = (
     0, -1, -2, -3, -4, -5)
 PA_F32, PA_BF16 = 0, 1
+OP_ADD, OP_EXTEND, OP_TRUNCATE, OP_FREE = 0, 1, 2, 3
 KIND_PREFILL, KIND_DECODE, KIND_VERIFY = 0, 1, 2
 _CODES = {PA_ERR_ARG: "arg", PA_ERR_UNSUPPORTED: "unsupported", PA_ERR_NO_BLOCKS: "no_blocks",
           PA_ERR_UNKNOWN_SEQ: "unknown_seq", PA_ERR_LAUNCH: "launch"}
@@ -24,7 +25,7 @@ _CODES = {PA_ERR_ARG: "arg", PA_ERR_UNSUPPORTED: "unsupported", PA_ERR_NO_BLOCKS
 # Every symbol include/pa.h declares.
 EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy", "pa_seq_add",
            "pa_seq_extend", "pa_seq_truncate", "pa_seq_free", "pa_seqs_add", "pa_seqs_extend",
-           "pa_seqs_truncate", "pa_seqs_free", "pa_seq_len", "pa_seq_blocks",
+           "pa_seqs_truncate", "pa_seqs_free", "pa_pool_apply", "pa_seq_len", "pa_seq_blocks",
            "pa_pool_free_list", "pa_build_metadata", "pa_attn_plan", "pa_kv_append",
            "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify"]
 
@@ -72,6 +73,7 @@ def lib():
         "pa_seqs_extend": (C.c_int, [_P, i32, _I64P, _I32P, _I32P, _I32P]),
         "pa_seqs_truncate": (C.c_int, [_P, i32, _I64P, _I32P, _I32P]),
         "pa_seqs_free": (C.c_int, [_P, i32, _I64P, _I32P]),
+        "pa_pool_apply": (C.c_int, [_P, i32, _I32P, _I64P, _I32P, _I32P, _I32P, _I32P, _I32P]),
         "pa_seq_len": (C.c_int, [_P, i64, _I32P]),
         "pa_seq_blocks": (C.c_int, [_P, i64, _I32P, i32, _I32P]),
         "pa_pool_free_list": (C.c_int, [_P, _I32P, i32, _I32P]),
@@ -171,6 +173,15 @@ class Pool:
         ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
         _check(self._lib.pa_seqs_free(self._h, ids.size, ids.ctypes.data_as(_I64P), None))
 
+    def apply(self, ops, seq_ids, offsets, tokens, new_lens):
+        """Mixed pool operations in one call (arrays as pa_pool_apply takes
+        them); returns reused-token counts (int32, 0 for non-admissions)."""
+        out = np.zeros(len(ops), np.int32)
+        _check(self._lib.pa_pool_apply(self._h, len(ops), _ptr(ops), seq_ids.ctypes.data_as(_I64P),
+                                       _ptr(offsets), _ptr(tokens) if tokens.size else None,
+                                       _ptr(new_lens), _ptr(out), None))
+        return out
+
     def seq_len(self, seq_id: int) -> int:
         n = C.c_int32(0)
         _check(self._lib.pa_seq_len(self._h, int(seq_id), C.byref(n)))
@@ -221,11 +232,15 @@ def plan(kind: int, n_q: int, seq_lens, cu_seqlens_q, num_q_heads: int, num_kv_h
     info = PlanInfo()
     args = (int(kind), int(n_q), n, _ptr(sl) if n else None, _ptr(cu), int(num_q_heads),
             int(num_kv_heads), int(head_dim), int(block_size), int(dtype), int(num_cus))
-    _check(L.pa_attn_plan(*args, None, 0, C.byref(info)))
-    if out is not None and out.size >= info.plan_words:
-        arr = out
+    if out is not None:
+        rc = L.pa_attn_plan(*args, _ptr(out), out.size, C.byref(info))
+        if rc == PA_OK:
+            return out[:info.plan_words], info
+        if not (rc == PA_ERR_ARG and info.plan_words > out.size):
+            _check(rc)
     else:
-        arr = np.zeros(max(1, info.plan_words), dtype=np.int32)
+        _check(L.pa_attn_plan(*args, None, 0, C.byref(info)))
+    arr = np.zeros(max(1, info.plan_words), dtype=np.int32)
     _check(L.pa_attn_plan(*args, _ptr(arr), arr.size, C.byref(info)))
     return arr[:info.plan_words], info
 

@@ -25,9 +25,12 @@ ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CXX = os.environ.get("CXX", "g++")  # host-only sources (no device code)
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall"]
-# Packed-fp32 VALU forms are kept out of the generated code.
+# Packed-fp32 VALU forms are kept out of the generated code.  MFMA results stay
+# in ordinary VGPRs: with accumulation registers the compiler copied every
+# output accumulator between register files on each iteration of the softmax
+# loops.
 HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
-             "-packed-fp32-ops", "-munsafe-fp-atomics"]
+             "-packed-fp32-ops", "-munsafe-fp-atomics", "-mllvm", "--amdgpu-mfma-vgpr-form"]
 
 
 def _run(cmd):

@@ -191,7 +191,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
     if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
       const float mnew = fmaxf(m, mx);
       const float mcn = mnew == kNegInf ? 0.f : mnew * c;
-      const float alpha = m == kNegInf ? 0.f : exp2f(mc - mcn);
+      const float alpha = m == kNegInf ? 0.f : fast_exp2(mc - mcn);
       l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt)
@@ -202,7 +202,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
     }
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      s[e] = exp2f(fmaf(s[e], c, -mc));
+      s[e] = fast_exp2(fmaf(s[e], c, -mc));
       l += s[e];
     }
     bf16x8 pb0, pb1;
@@ -365,7 +365,7 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
     if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
       const float mnew = fmaxf(m, mx);
       const float mcn = mnew == kNegInf ? 0.f : mnew * c;
-      const float alpha = m == kNegInf ? 0.f : exp2f(mc - mcn);
+      const float alpha = m == kNegInf ? 0.f : fast_exp2(mc - mcn);
       l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) acc[dt] *= alpha;
@@ -377,7 +377,7 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p = exp2f(fmaf(s[tt][e], c, -mc));
+        const float p = fast_exp2(fmaf(s[tt][e], c, -mc));
         l += p;
         pb[4 * tt + e] = (__bf16)p;
       }

@@ -47,6 +47,11 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// 2^x on the hardware transcendental unit (v_exp_f32) without the library's
+// denormal-range fix-up: results below 2^-126 flush to zero, which only
+// drops probabilities that are negligible against the row maximum (>= 1).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ float wave_xor(float v, int mask) { return __shfl_xor(v, mask, 64); }
 
 __device__ __forceinline__ int clamp_block(int b, int num_blocks) {

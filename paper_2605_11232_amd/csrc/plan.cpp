@@ -9,15 +9,15 @@
 // rows whose key range is split so the launch has enough wavefronts in flight
 // to stream the cache at HBM bandwidth; the row groups of one key range sit
 // next to each other so their loads meet in cache, and split partial results
-// are combined by log-sum-exp in a merge pass.  Paper: Section 5.2 (split prefills under a batched-token budget, mixed
-// prefill and decode), Section 6, Table "playbook" (long prefills blocking
-// short decodes).
+// are combined by log-sum-exp in a merge pass.  Paper: Section 5.2 (split
+// prefills under a batched-token budget, mixed prefill and decode), Section 6,
+// Table "playbook" (long prefills blocking short decodes).
 //
 // Dispatch order: workgroup ids are handed to the eight XCDs round robin, and
 // each XCD has its own L2.  Items are queued per XCD by kv-head so that all
 // work of one kv-head -- and so the shared prefix blocks of that head, which
 // every sequence reads -- stays in one XCD's L2.  Within a queue, items are
-// ordered longest first to shorten the tail.
+// ordered longest first (coarse counting sort) to shorten the tail.
 #include <algorithm>
 #include <array>
 #include <vector>
@@ -29,10 +29,7 @@ namespace {
 
 constexpr int kXcds = 8;
 
-struct Item {
-  std::array<int32_t, pa::kItemWords> w;
-  int64_t cost;
-};
+using Rec = std::array<int32_t, pa::kItemWords>;
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -50,14 +47,35 @@ std::vector<int> xcds_of_head(int g, int hkv) {
   return x;
 }
 
+// Indices of `cost` ordered longest first by a stable counting sort on 256
+// coarse buckets (relative to the largest cost): O(n), and equal-cost items
+// keep their generation order (row groups of one key range stay adjacent).
+std::vector<int32_t> order_longest_first(const std::vector<int64_t>& cost) {
+  const size_t n = cost.size();
+  std::vector<int32_t> out(n);
+  if (n == 0) return out;
+  int64_t mx = 1;
+  for (int64_t c : cost) mx = std::max(mx, c);
+  std::vector<int32_t> key(n);
+  std::array<int32_t, 257> cnt{};
+  for (size_t i = 0; i < n; ++i) {
+    key[i] = 255 - static_cast<int32_t>((cost[i] * 255) / mx);  // 0 = longest
+    ++cnt[key[i] + 1];
+  }
+  for (int b = 0; b < 256; ++b) cnt[b + 1] += cnt[b];
+  for (size_t i = 0; i < n; ++i) out[cnt[key[i]]++] = static_cast<int32_t>(i);
+  return out;
+}
+
 // Interleave per-XCD queues of units into dispatch order: unit slot b goes to
 // queue b % kXcds while it has units, else to the longest remaining queue.
 template <class U>
-std::vector<U> interleave(std::vector<std::vector<U>>& queues) {
+std::vector<U> interleave(const std::vector<std::vector<U>>& queues) {
   std::vector<U> out;
   std::vector<size_t> pos(queues.size(), 0);
   size_t total = 0;
   for (auto& q : queues) total += q.size();
+  out.reserve(total);
   for (size_t b = 0; b < total; ++b) {
     size_t q = b % queues.size();
     if (pos[q] >= queues[q].size()) {
@@ -112,10 +130,10 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   }
   const int32_t total_q = n_seqs > 0 ? cu_seqlens_q[n_seqs] : 0;
 
-  std::vector<std::vector<Item>> tile_q(kXcds), row_q(kXcds);
   std::vector<std::array<int32_t, pa::kGroupWords>> groups;
   int64_t partial_rows = 0;
-  int64_t n_tile = 0, n_row_real = 0;
+  std::vector<Rec> tiles;
+  std::vector<std::array<Rec, 4>> quads;
 
   if (dtype == PA_BF16) {
     // Key-range split of row items: aim for enough single-wave items to keep
@@ -130,8 +148,26 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     int64_t chunk = std::max<int64_t>(256, cdiv(row_keys, std::max<int64_t>(1, target_waves)));
     chunk = cdiv(chunk, pa::kKeyStep) * pa::kKeyStep;
 
-    std::vector<std::vector<std::vector<Item>>> head_rows(num_kv_heads);
-    std::vector<std::vector<Item>> head_tiles(num_kv_heads);
+    std::vector<std::vector<Rec>> head_tiles(num_kv_heads), head_rows(num_kv_heads);
+    std::vector<std::vector<int64_t>> tile_cost(num_kv_heads), row_cost(num_kv_heads);
+    {
+      // exact per-head item counts, so the lists are allocated once
+      int64_t nt = 0, nr = 0;
+      for (int32_t r = 0; r < n_seqs; ++r) {
+        const int32_t n = cu_seqlens_q[r + 1] - cu_seqlens_q[r];
+        if (n == 0) continue;
+        if (n * G <= pa::kRowSeqRows)
+          nr += cdiv(n * G, pa::kRowItemRows) * std::max<int64_t>(1, cdiv(seq_lens[r], chunk));
+        else
+          nt += cdiv(int64_t(n) * G, pa::kTileRows);
+      }
+      for (int32_t g = 0; g < num_kv_heads; ++g) {
+        head_tiles[g].reserve(nt);
+        tile_cost[g].reserve(nt);
+        head_rows[g].reserve(nr);
+        row_cost[g].reserve(nr);
+      }
+    }
     for (int32_t r = 0; r < n_seqs; ++r) {
       const int32_t n = cu_seqlens_q[r + 1] - cu_seqlens_q[r];
       const int32_t L = seq_lens[r];
@@ -143,32 +179,29 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         const int64_t per = cdiv(cdiv(L, nsplit), pa::kKeyStep) * pa::kKeyStep;
         int32_t used = 0;
         while (used < nsplit && int64_t(used) * per < L) ++used;
+        const int32_t ngroups = static_cast<int32_t>(cdiv(rows, pa::kRowItemRows));
         for (int32_t g = 0; g < num_kv_heads; ++g) {
-          // per split, the row groups back to back
-          std::vector<Item> its;
-          std::vector<int32_t> base;
-          for (int32_t row0 = 0; row0 < rows; row0 += pa::kRowItemRows) {
+          int64_t base[pa::kRowSeqRows / pa::kRowItemRows];
+          for (int32_t gi = 0; gi < ngroups; ++gi) {
+            const int32_t row0 = gi * pa::kRowItemRows;
             const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
-            base.push_back(used > 1 ? int32_t(partial_rows) : -1);
+            base[gi] = used > 1 ? partial_rows : -1;
             if (used > 1) {
               groups.push_back({r, g, row0, nr, used, int32_t(partial_rows), 0, 0});
               partial_rows += int64_t(used) * nr;
             }
           }
-          for (int32_t s = 0; s < used; ++s) {
-            const int64_t k0 = s * per, k1 = std::min<int64_t>(L, (s + 1) * per);
-            int32_t gi = 0;
-            for (int32_t row0 = 0; row0 < rows; row0 += pa::kRowItemRows, ++gi) {
+          // per split, the row groups back to back
+          for (int32_t sp = 0; sp < used; ++sp) {
+            const int64_t k0 = sp * per, k1 = std::min<int64_t>(L, (sp + 1) * per);
+            for (int32_t gi = 0; gi < ngroups; ++gi) {
+              const int32_t row0 = gi * pa::kRowItemRows;
               const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
-              Item it{};
-              it.w = {r, g, row0, nr, int32_t(k0), int32_t(k1),
-                      base[gi] < 0 ? -1 : int32_t(base[gi] + int64_t(s) * nr), 0};
-              it.cost = k1 - k0;
-              its.push_back(it);
-              ++n_row_real;
+              head_rows[g].push_back({r, g, row0, nr, int32_t(k0), int32_t(k1),
+                                      base[gi] < 0 ? -1 : int32_t(base[gi] + int64_t(sp) * nr), 0});
+              row_cost[g].push_back(k1 - k0);
             }
           }
-          head_rows[g].push_back(std::move(its));
         }
       } else {
         const int32_t ntiles = static_cast<int32_t>(cdiv(rows, pa::kTileRows));
@@ -178,57 +211,38 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
             const int32_t nrows = std::min(pa::kTileRows, rows - row0);
             const int32_t last_q = (row0 + nrows - 1) / G;
             const int32_t kv1 = L - n + last_q + 1;
-            Item it{};
-            it.w = {r, g, row0, nrows, 0, kv1, -1, 0};
-            it.cost = int64_t(kv1) * nrows;
-            head_tiles[g].push_back(it);
-            ++n_tile;
+            head_tiles[g].push_back({r, g, row0, nrows, 0, kv1, -1, 0});
+            tile_cost[g].push_back(int64_t(kv1) * nrows);
           }
         }
       }
     }
-    // Tile items: per-head lists, longest first, dealt to the head's XCD queues.
+    // Tile items: per head, longest first, dealt round robin to the head's
+    // XCD queues (which stay longest first).
+    std::vector<std::vector<Rec>> tile_q(kXcds);
     for (int32_t g = 0; g < num_kv_heads; ++g) {
-      auto& v = head_tiles[g];
-      std::stable_sort(v.begin(), v.end(), [](const Item& a, const Item& b) { return a.cost > b.cost; });
       const auto xs = xcds_of_head(g, num_kv_heads);
-      for (size_t i = 0; i < v.size(); ++i) tile_q[xs[i % xs.size()]].push_back(v[i]);
+      const auto ord = order_longest_first(tile_cost[g]);
+      for (size_t i = 0; i < ord.size(); ++i) tile_q[xs[i % xs.size()]].push_back(head_tiles[g][ord[i]]);
     }
-    for (auto& q : tile_q)
-      std::stable_sort(q.begin(), q.end(), [](const Item& a, const Item& b) { return a.cost > b.cost; });
-    // Row items: per head, longest first, packed four to a workgroup (padded
-    // with empty items) so a workgroup's waves share one kv-head.
+    tiles = interleave(tile_q);
+    // Row items: per head, longest first, four to a workgroup (padded with
+    // empty items) so a workgroup's waves share one kv-head.
+    std::vector<std::vector<std::array<Rec, 4>>> quad_q(kXcds);
+    const Rec empty = {-1, 0, 0, 0, 0, 0, -1, 0};
     for (int32_t g = 0; g < num_kv_heads; ++g) {
-      std::vector<Item> flat;
-      for (auto& its : head_rows[g]) flat.insert(flat.end(), its.begin(), its.end());
-      std::stable_sort(flat.begin(), flat.end(), [](const Item& a, const Item& b) { return a.cost > b.cost; });
       const auto xs = xcds_of_head(g, num_kv_heads);
+      const auto ord = order_longest_first(row_cost[g]);
       size_t quad = 0;
-      for (size_t i = 0; i < flat.size(); i += 4, ++quad) {
-        auto& q = row_q[xs[quad % xs.size()]];
-        for (size_t k = 0; k < 4; ++k) {
-          if (i + k < flat.size()) {
-            q.push_back(flat[i + k]);
-          } else {
-            Item e{};
-            e.w = {-1, 0, 0, 0, 0, 0, -1, 0};
-            q.push_back(e);
-          }
-        }
+      for (size_t i = 0; i < ord.size(); i += 4, ++quad) {
+        std::array<Rec, 4> qd;
+        for (size_t k = 0; k < 4; ++k) qd[k] = i + k < ord.size() ? head_rows[g][ord[i + k]] : empty;
+        quad_q[xs[quad % xs.size()]].push_back(qd);
       }
     }
+    quads = interleave(quad_q);
   }
 
-  // Flatten: tile items one per workgroup; row items as quads.
-  std::vector<Item> tiles = interleave(tile_q);
-  std::vector<std::array<Item, 4>> quads;
-  {
-    std::vector<std::vector<std::array<Item, 4>>> qq(kXcds);
-    for (int x = 0; x < kXcds; ++x)
-      for (size_t i = 0; i < row_q[x].size(); i += 4)
-        qq[x].push_back({row_q[x][i], row_q[x][i + 1], row_q[x][i + 2], row_q[x][i + 3]});
-    quads = interleave(qq);
-  }
   const int64_t n_row = int64_t(quads.size()) * 4;
   const int64_t n_groups = int64_t(groups.size());
   const int64_t tile_off = pa::kHeaderWords;
@@ -239,8 +253,6 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
                                        : int64_t(tiles.size()) + int64_t(quads.size());
   if (words >= (int64_t{1} << 31) || grid >= (int64_t{1} << 31) || partial_rows >= (int64_t{1} << 31))
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: launch too large");
-  (void)n_tile;
-  (void)n_row_real;
 
   info->kind = kind;
   info->n_q = n_q;
@@ -275,9 +287,9 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   h[pa::H_GROUP_OFF] = int32_t(group_off);
   h[pa::H_PARTIAL_ROWS] = int32_t(partial_rows);
   int32_t* p = plan + tile_off;
-  for (auto& it : tiles) p = std::copy(it.w.begin(), it.w.end(), p);
+  for (auto& it : tiles) p = std::copy(it.begin(), it.end(), p);
   for (auto& q : quads)
-    for (auto& it : q) p = std::copy(it.w.begin(), it.w.end(), p);
+    for (auto& it : q) p = std::copy(it.begin(), it.end(), p);
   for (auto& g : groups) p = std::copy(g.begin(), g.end(), p);
   return PA_OK;
 }

@@ -9,9 +9,10 @@
 // A cached block is identified by (predecessor block, its block_size tokens).
 // Because a block is cached only when its predecessor is cached, that pair
 // stands for the whole token prefix up to the block, so a match on it is a
-// match on the full prefix.  The hash only narrows candidates: every hit is
-// confirmed by comparing the predecessor id and the stored tokens, so hash
-// collisions cannot produce a false hit.
+// match on the full prefix.  The hash only narrows candidates (open
+// addressing, linear probing): every hit is confirmed by comparing the
+// predecessor id and the stored tokens, so hash collisions cannot produce a
+// false hit.
 #include <algorithm>
 #include <cstring>
 #include <deque>
@@ -29,7 +30,12 @@ struct pa_pool {
   std::vector<uint8_t> cached;       // block is in the prefix index
   std::vector<int32_t> pred;         // cached block's predecessor (-1: first block)
   std::vector<int32_t> content;      // cached block's tokens, [num_blocks][bs]
-  std::unordered_multimap<uint64_t, int32_t> index;
+  // Open-addressing index of cached blocks: slot_hash 0 = empty, otherwise the
+  // (never zero) key hash; slot_block the cached block.  Capacity is a power
+  // of two >= 2 * num_blocks, so the load factor stays <= 1/2.
+  std::vector<uint64_t> slot_hash;
+  std::vector<int32_t> slot_block;
+  uint64_t slot_mask = 0;
 
   struct Seq {
     std::vector<int32_t> tokens;
@@ -41,25 +47,38 @@ struct pa_pool {
   static int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
   uint64_t key_hash(int32_t p, const int32_t* t) const {
+    // two tokens per 64-bit mixing round
     uint64_t h = 0x9E3779B97F4A7C15ull ^ static_cast<uint32_t>(p);
-    for (int32_t i = 0; i < bs; ++i) {
-      h ^= static_cast<uint32_t>(t[i]);
-      h *= 0x100000001B3ull;
-      h ^= h >> 29;
+    int32_t i = 0;
+    for (; i + 1 < bs; i += 2) {
+      const uint64_t w = static_cast<uint32_t>(t[i]) | (uint64_t(static_cast<uint32_t>(t[i + 1])) << 32);
+      h = (h ^ w) * 0xFF51AFD7ED558CCDull;
+      h ^= h >> 32;
     }
-    return h;
+    if (i < bs) h = ((h ^ static_cast<uint32_t>(t[i])) * 0xC4CEB9FE1A85EC53ull) ^ (h >> 29);
+    h ^= h >> 29;
+    return h | 1;  // never 0 (the empty-slot marker)
   }
 
   // Cached block whose predecessor is p and whose tokens are t[0..bs), or -1.
   int32_t find(int32_t p, const int32_t* t) const {
-    auto range = index.equal_range(key_hash(p, t));
-    for (auto it = range.first; it != range.second; ++it) {
-      const int32_t b = it->second;
+    const uint64_t h = key_hash(p, t);
+    for (uint64_t i = h & slot_mask;; i = (i + 1) & slot_mask) {
+      const uint64_t sh = slot_hash[i];
+      if (sh == 0) return -1;
+      if (sh != h) continue;
+      const int32_t b = slot_block[i];
       if (pred[b] == p &&
           std::memcmp(&content[static_cast<size_t>(b) * bs], t, sizeof(int32_t) * bs) == 0)
         return b;
     }
-    return -1;
+  }
+
+  void insert(uint64_t h, int32_t b) {
+    uint64_t i = h & slot_mask;
+    while (slot_hash[i] != 0) i = (i + 1) & slot_mask;
+    slot_hash[i] = h;
+    slot_block[i] = b;
   }
 
   // Cache the sequence's full blocks after its cached run, in logical order,
@@ -75,7 +94,7 @@ struct pa_pool {
       cached[b] = 1;
       pred[b] = p;
       std::memcpy(&content[static_cast<size_t>(b) * bs], t, sizeof(int32_t) * bs);
-      index.emplace(key_hash(p, t), b);
+      insert(key_hash(p, t), b);
       ++j;
     }
     s.n_cached_run = j;
@@ -111,6 +130,11 @@ int pa_pool_create(int32_t num_blocks, int32_t block_size, const int32_t* free_o
   p->cached.assign(num_blocks, 0);
   p->pred.assign(num_blocks, -1);
   p->content.assign(static_cast<size_t>(num_blocks) * block_size, 0);
+  uint64_t cap = 16;
+  while (cap < 2 * static_cast<uint64_t>(num_blocks)) cap <<= 1;
+  p->slot_hash.assign(cap, 0);
+  p->slot_block.assign(cap, -1);
+  p->slot_mask = cap - 1;
   *out = p;
   return PA_OK;
 }
@@ -274,6 +298,33 @@ int pa_seqs_truncate(pa_pool* pool, int32_t n, const int64_t* seq_ids, const int
 int pa_seqs_free(pa_pool* pool, int32_t n, const int64_t* seq_ids, int32_t* n_done) {
   return batch("pa_seqs_free", n, seq_ids, n_done,
                [&](int32_t i) { return pa_seq_free(pool, seq_ids[i]); });
+}
+
+int pa_pool_apply(pa_pool* pool, int32_t n, const int32_t* ops, const int64_t* seq_ids,
+                  const int32_t* token_offsets, const int32_t* tokens, const int32_t* new_lens,
+                  int32_t* n_cached_out, int32_t* n_done) {
+  if (n > 0 && (!ops || !token_offsets))
+    return pa::fail(PA_ERR_ARG, "pa_pool_apply: NULL ops or token offsets");
+  if (!offsets_ok(n, token_offsets, tokens))
+    return pa::fail(PA_ERR_ARG, "pa_pool_apply: invalid token offsets");
+  return batch("pa_pool_apply", n, seq_ids, n_done, [&](int32_t i) {
+    const int32_t* t = tokens ? tokens + token_offsets[i] : nullptr;
+    const int32_t cnt = token_offsets[i + 1] - token_offsets[i];
+    if (n_cached_out) n_cached_out[i] = 0;
+    switch (ops[i]) {
+      case PA_OP_ADD:
+        return pa_seq_add(pool, seq_ids[i], t, cnt, n_cached_out ? n_cached_out + i : nullptr);
+      case PA_OP_EXTEND:
+        return pa_seq_extend(pool, seq_ids[i], t, cnt);
+      case PA_OP_TRUNCATE:
+        if (!new_lens) return pa::fail(PA_ERR_ARG, "pa_pool_apply: NULL new_lens");
+        return pa_seq_truncate(pool, seq_ids[i], new_lens[i]);
+      case PA_OP_FREE:
+        return pa_seq_free(pool, seq_ids[i]);
+      default:
+        return pa::fail(PA_ERR_ARG, "pa_pool_apply: unknown operation %d", ops[i]);
+    }
+  });
 }
 
 int pa_seq_len(const pa_pool* pool, int64_t seq_id, int32_t* len_out) {

@@ -26,31 +26,26 @@ class Prepared:
         self.__dict__.update(kw)
 
 
+_OPCODE = {"add": B.OP_ADD, "extend": B.OP_EXTEND, "truncate": B.OP_TRUNCATE, "free": B.OP_FREE}
+
+
 def batch_ops(ops):
-    """Group consecutive add/extend/free/truncate ops into batched calls
-    (computed once per launch and cached on it)."""
-    groups = []
-    for op in ops:
-        if op.kind == "write_kv" or not groups or groups[-1][0] != op.kind:
-            groups.append((op.kind, [op]))
-        else:
-            groups[-1][1].append(op)
-    packed = []
-    for kind, g in groups:
-        if kind == "write_kv":
-            packed.append((kind, g[0]))
-            continue
-        ids = np.array([op.seq_id for op in g], dtype=np.int64)
-        if kind in ("add", "extend"):
-            lens = np.array([len(op.tokens) for op in g], dtype=np.int32)
-            off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
-            toks = np.concatenate([op.tokens for op in g]).astype(np.int32)
-            packed.append((kind, (ids, off, toks)))
-        elif kind == "truncate":
-            packed.append((kind, (ids, np.array([op.n for op in g], dtype=np.int32))))
-        else:
-            packed.append((kind, (ids,)))
-    return packed
+    """Pack a list of pool ops into the arrays of one pa_pool_apply call
+    (write_kv ops, which only occur in setup, are kept apart)."""
+    pool_ops = [op for op in ops if op.kind != "write_kv"]
+    if len(pool_ops) != len(ops):
+        raise ValueError("write_kv ops cannot be batched")
+    n = len(pool_ops)
+    codes = np.array([_OPCODE[op.kind] for op in pool_ops], dtype=np.int32)
+    ids = np.array([op.seq_id for op in pool_ops], dtype=np.int64)
+    lens = np.array([len(op.tokens) if op.tokens is not None else 0 for op in pool_ops],
+                    dtype=np.int64)
+    off = np.zeros(n + 1, dtype=np.int32)
+    np.cumsum(lens, out=off[1:])
+    toks = [op.tokens for op in pool_ops if op.tokens is not None and len(op.tokens)]
+    toks = np.concatenate(toks).astype(np.int32) if toks else np.zeros(0, np.int32)
+    new_lens = np.array([op.n if op.kind == "truncate" else 0 for op in pool_ops], dtype=np.int32)
+    return codes, ids, off, toks, new_lens
 
 
 class Staging:
@@ -116,22 +111,17 @@ class DeviceReplay:
             raise ValueError(op.kind)
 
     def apply_batched(self, launch, which: str):
+        """Apply the launch's pre or post pool ops in one library call."""
         cache = launch.__dict__.setdefault("_batched", {})
         if which not in cache:
             cache[which] = batch_ops(getattr(launch, which))
-        p = self.pool
-        for kind, args in cache[which]:
-            if kind == "add":
-                hits = p.add_many(*args)
-                self.n_cached.update(zip(args[0].tolist(), hits.tolist()))
-            elif kind == "extend":
-                p.extend_many(*args)
-            elif kind == "truncate":
-                p.truncate_many(*args)
-            elif kind == "free":
-                p.free_many(*args)
-            else:
-                self.apply(args)
+        codes, ids, off, toks, new_lens = cache[which]
+        if len(codes) == 0:
+            return
+        hits = self.pool.apply(codes, ids, off, toks, new_lens)
+        added = codes == B.OP_ADD
+        if added.any():
+            self.n_cached.update(zip(ids[added].tolist(), hits[added].tolist()))
 
     def setup(self):
         for op in self.wl.setup:

@@ -282,3 +282,36 @@ def test_batched_pool_calls_match_single_calls():
     o.free_seq(1)
     assert o.free_list() == lib_pool.free_list()
     assert lib_pool.seq_len(2) == o.seq_len(2)
+
+
+@pytest.mark.parametrize("name", ["mixed", "verify"])
+def test_pool_apply_matches_oracle_on_steps(name):
+    """pa_pool_apply (one call per step phase) against the oracle applying the
+    same operations one by one, over several steps of a workload."""
+    from paper_2605_11232_amd.runtime import batch_ops
+    wl = synth.workload(name, scale=0.25, steps=4)
+    o = PrefixCacheOracle(wl.num_blocks, wl.cfg.block_size, wl.free_order)
+    lp = B.Pool(wl.num_blocks, wl.cfg.block_size, wl.free_order)
+    for op in wl.setup:
+        if op.kind == "add":
+            assert o.add(op.seq_id, op.tokens) == lp.add(op.seq_id, op.tokens)
+        elif op.kind == "free":
+            o.free_seq(op.seq_id)
+            lp.free(op.seq_id)
+    for st in range(3):
+        launch = wl.step(st)
+        hits = lp.apply(*batch_ops(launch.pre))
+        want = [o.add(op.seq_id, op.tokens) if op.kind == "add" else
+                (o.extend(op.seq_id, op.tokens) or 0) for op in launch.pre]
+        assert hits.tolist() == want
+        mo = o.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
+        ml = lp.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
+        for k in mo:
+            np.testing.assert_array_equal(mo[k], ml[k])
+        lp.apply(*batch_ops(launch.post))
+        for op in launch.post:
+            if op.kind == "free":
+                o.free_seq(op.seq_id)
+            else:
+                o.truncate(op.seq_id, op.n)
+        assert o.free_list() == lp.free_list()
