@@ -124,8 +124,8 @@ def main():
     # plan size bound: tile items + single-wave items (key splits of >= 256) +
     # split groups, plus per-XCD padding
     max_keys = wl.max_blocks_per_seq * cfg.block_size
-    plan_words = 16 + 8 * (cfg.num_kv_heads * (T * cfg.group // 128 + n)
-                           + cfg.num_kv_heads * n * (max_keys // 256 + 2) + 64)
+    plan_words = 32 + 8 * (cfg.num_kv_heads * (T * cfg.group // 128 + n)
+                           + 2 * cfg.num_kv_heads * n * (max_keys // 256 + 2) + 64)
     stagings = [Staging("cuda", n, wl.max_blocks_per_seq, T, plan_words) for _ in range(2)]
     stream = torch.cuda.current_stream()
 

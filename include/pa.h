@@ -180,27 +180,36 @@ typedef enum { PA_KIND_PREFILL = 0, PA_KIND_DECODE = 1, PA_KIND_VERIFY = 2 } pa_
 typedef struct pa_plan_info {
   int32_t kind;            /* pa_kind the plan was built for                      */
   int32_t n_q;             /* query tokens per sequence (decode 1, verify n_q)    */
+  int32_t n_shared_items;  /* shared-prefix (cascade) items, one workgroup each   */
   int32_t n_tile_items;    /* 128-row work items (one workgroup each)             */
   int32_t n_row_items;     /* <=48-row work items (one wavefront each)            */
   int32_t n_groups;        /* split groups the merge step combines                */
   int32_t n_merge_rows;    /* (token, head) rows produced by the merge step       */
   int32_t grid;            /* workgroups of the attention launch                  */
   int32_t variant;         /* kernel instantiation (internal)                     */
+  int32_t reserved;
   int64_t plan_words;      /* int32 words of the plan array                       */
   int64_t workspace_bytes; /* device scratch the attention call needs             */
 } pa_plan_info;
 
-/* Split one attention launch into work items from HOST copies of seq_lens and
- * cu_seqlens_q (as produced by pa_build_metadata).  With plan == NULL only
+/* Split one attention launch into work items from HOST copies of seq_lens,
+ * cu_seqlens_q and (optionally) block_table[n_seqs][max_blocks_per_seq], as
+ * produced by pa_build_metadata.  With a block table, sequences of at most
+ * 64 query rows per kv-head (decode, verification) whose tables start with
+ * the same blocks form shared-prefix groups: their attention over the shared
+ * keys is computed once for all their rows and merged with each sequence's
+ * private part by log-sum-exp (pass NULL to disable).  With plan == NULL only
  * *info is filled (size query).  Otherwise the int32 plan (plan_capacity
  * words, host memory) is written; the caller copies it to device memory and
- * passes the device copy and *info to the attention call.
+ * passes the device copy and *info to the attention call.  If plan_capacity
+ * is too small the call fails with PA_ERR_ARG and *info holds the size.
  * kind PA_KIND_DECODE requires every q_len == 1, PA_KIND_VERIFY every q_len ==
  * n_q (1..8); PA_KIND_PREFILL takes any q_len >= 0 (prefill chunks and decode
  * tokens may be mixed).  num_cus = compute units to fill (0: 256).
  * Errors: PA_ERR_ARG, PA_ERR_UNSUPPORTED. */
 int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int32_t* seq_lens,
-                 const int32_t* cu_seqlens_q, int32_t num_q_heads, int32_t num_kv_heads,
+                 const int32_t* cu_seqlens_q, const int32_t* block_table,
+                 int32_t max_blocks_per_seq, int32_t num_q_heads, int32_t num_kv_heads,
                  int32_t head_dim, int32_t block_size, int32_t dtype, int32_t num_cus,
                  int32_t* plan, int64_t plan_capacity, pa_plan_info* info);
 
@@ -226,7 +235,8 @@ int pa_kv_append(const void* k_new, const void* v_new, const int32_t* slot_mappi
  *   lse = log sum_{t<=a} exp(scale * q . k_t).
  * Device inputs: q, caches, block_table[n_seqs][max_blocks_per_seq],
  * seq_lens[n_seqs], cu_seqlens_q[n_seqs+1] (the same values the plan was built
- * from), plan (device copy of pa_attn_plan's output) with its *info,
+ * from), plan (device copy of pa_attn_plan's output) with its *info (the
+ * block table must be the one the plan's shared-prefix groups were found in),
  * workspace of at least info->workspace_bytes bytes (any contents) or NULL if
  * that is 0.  Block ids must lie in [0, num_blocks); out-of-range ids are
  * clamped so no access leaves the cache (results are then undefined).

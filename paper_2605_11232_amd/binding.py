@@ -38,10 +38,10 @@ class PaError(RuntimeError):
 
 
 class PlanInfo(C.Structure):
-    _fields_ = [("kind", C.c_int32), ("n_q", C.c_int32), ("n_tile_items", C.c_int32),
-                ("n_row_items", C.c_int32), ("n_groups", C.c_int32), ("n_merge_rows", C.c_int32),
-                ("grid", C.c_int32), ("variant", C.c_int32), ("plan_words", C.c_int64),
-                ("workspace_bytes", C.c_int64)]
+    _fields_ = [("kind", C.c_int32), ("n_q", C.c_int32), ("n_shared_items", C.c_int32),
+                ("n_tile_items", C.c_int32), ("n_row_items", C.c_int32), ("n_groups", C.c_int32),
+                ("n_merge_rows", C.c_int32), ("grid", C.c_int32), ("variant", C.c_int32),
+                ("reserved", C.c_int32), ("plan_words", C.c_int64), ("workspace_bytes", C.c_int64)]
 
 
 _lib = None
@@ -78,8 +78,8 @@ def lib():
         "pa_seq_blocks": (C.c_int, [_P, i64, _I32P, i32, _I32P]),
         "pa_pool_free_list": (C.c_int, [_P, _I32P, i32, _I32P]),
         "pa_build_metadata": (C.c_int, [_P, i32, _I64P, _I32P, i32, _I32P, _I32P, _I32P, _I32P, i64]),
-        "pa_attn_plan": (C.c_int, [i32, i32, i32, _I32P, _I32P, i32, i32, i32, i32, i32, i32, _I32P,
-                                   i64, C.POINTER(PlanInfo)]),
+        "pa_attn_plan": (C.c_int, [i32, i32, i32, _I32P, _I32P, _I32P, i32, i32, i32, i32, i32, i32,
+                                   i32, _I32P, i64, C.POINTER(PlanInfo)]),
         "pa_kv_append": (C.c_int, [_P, _P, _P, i32, _P, _P, i32, i32, i32, i32, i32, _P]),
     }
     attn = (C.c_int, [_P, _P, _P, i32, _P, i32, _P, _P, i32, i32, i32, i32, i32, i32, f32, i32, _P,
@@ -223,15 +223,24 @@ class Pool:
 
 
 def plan(kind: int, n_q: int, seq_lens, cu_seqlens_q, num_q_heads: int, num_kv_heads: int,
-         head_dim: int, block_size: int, dtype: int, num_cus: int = 0, out=None):
+         head_dim: int, block_size: int, dtype: int, num_cus: int = 0, out=None,
+         block_table=None):
     """Build the launch plan on the host; returns (int32 plan array, PlanInfo).
-    ``out`` (int32 array, e.g. a pinned staging view) is used when large enough."""
+    ``out`` (int32 array, e.g. a pinned staging view) is used when large
+    enough.  ``block_table`` (host [n_seqs, max_blocks] int32) enables
+    shared-prefix groups."""
     L = lib()
     sl, cu = _i32(seq_lens), _i32(cu_seqlens_q)
     n = sl.size
     info = PlanInfo()
-    args = (int(kind), int(n_q), n, _ptr(sl) if n else None, _ptr(cu), int(num_q_heads),
-            int(num_kv_heads), int(head_dim), int(block_size), int(dtype), int(num_cus))
+    if block_table is not None and n:
+        bt = _i32(block_table)
+        bt_ptr, mb = _ptr(bt), int(bt.shape[1])
+    else:
+        bt_ptr, mb = None, 0
+    args = (int(kind), int(n_q), n, _ptr(sl) if n else None, _ptr(cu), bt_ptr, mb,
+            int(num_q_heads), int(num_kv_heads), int(head_dim), int(block_size), int(dtype),
+            int(num_cus))
     if out is not None:
         rc = L.pa_attn_plan(*args, _ptr(out), out.size, C.byref(info))
         if rc == PA_OK:

@@ -42,14 +42,17 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False, jobs: int = 8) -> str:
+def build(verbose: bool = False, jobs: int = 8, defines=(), out_path: str = LIB_PATH) -> str:
+    """Compile every source and link libpa.so at ``out_path``; ``defines``
+    are extra -D options for the HIP sources (kernel tuning knobs)."""
     tmp = tempfile.mkdtemp(prefix="pa_build_")
     try:
         cmds = []
         objs = []
         for s in HIP_SOURCES:
             o = os.path.join(tmp, s + ".o")
-            cmds.append([HIPCC, *COMMON, *HIP_FLAGS, "-c", os.path.join(CSRC, s), "-o", o])
+            cmds.append([HIPCC, *COMMON, *HIP_FLAGS, *[f"-D{d}" for d in defines], "-c",
+                         os.path.join(CSRC, s), "-o", o])
             objs.append(o)
         for s in HOST_SOURCES:
             o = os.path.join(tmp, s + ".o")
@@ -63,10 +66,10 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
                     print(o)
         tmp_lib = os.path.join(tmp, "libpa.so")
         _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp_lib])
-        shutil.move(tmp_lib, LIB_PATH)
+        shutil.move(tmp_lib, out_path)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
-    return LIB_PATH
+    return out_path
 
 
 if __name__ == "__main__":

@@ -72,7 +72,8 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
   } else {
     if (!plan) return fail(PA_ERR_ARG, "%s: NULL plan", fn);
     if (info->variant != 1 || info->grid < 0 || info->n_groups < 0 ||
-        info->n_tile_items < 0 || info->n_tile_items > info->grid)
+        info->n_tile_items < 0 || info->n_shared_items < 0 ||
+        int64_t(info->n_tile_items) + info->n_shared_items > info->grid)
       return fail(PA_ERR_ARG, "%s: corrupt plan info", fn);
     if (static_cast<int64_t>(workspace_bytes) < info->workspace_bytes ||
         (info->workspace_bytes > 0 && !workspace))
@@ -81,7 +82,8 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
     const int64_t partial_rows = info->workspace_bytes / (int64_t(head_dim + 1) * 4);
     rc = dev::launch_attn_bf16(q, k_cache, v_cache, num_blocks, block_table, max_blocks_per_seq,
                                seq_lens, cu_seqlens_q, num_q_heads, num_kv_heads, head_dim, scale,
-                               plan, info->grid, info->n_tile_items, info->n_groups,
+                               plan, info->grid, info->n_shared_items + info->n_tile_items,
+                               info->n_groups,
                                partial_rows,
                                workspace, out, lse, st);
   }

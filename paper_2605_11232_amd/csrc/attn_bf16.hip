@@ -57,35 +57,76 @@ __device__ __forceinline__ int perm32(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
-template <int D>
+// Keys per step of a tile item: NSUB sub-tiles of 32 keys (NSUB * 2 blocks).
+#ifndef PA_TILE_SUB
+#define PA_TILE_SUB 2
+#endif
+constexpr int kTileSub = PA_TILE_SUB;
+// Raise the wavefront's issue priority while it feeds the matrix cores, so the
+// SIMD's other wavefront does its softmax in the gaps (0 disables).
+#ifndef PA_SETPRIO
+#define PA_SETPRIO 0
+#endif
+
+template <int D, int NSUB>
 struct TileSmem {
-  static constexpr int KS = D + 8;   // bf16 per K row   (row stride 16 B odd multiple)
-  static constexpr int VS = 32 + 8;  // bf16 per V^T row (80 B)
-  __bf16 k[2][32 * KS];
+  static constexpr int KT = 32 * NSUB;
+  static constexpr int KS = D + 8;   // bf16 per K row (row stride an odd multiple of 16 B)
+  static constexpr int VS = KT + 8;  // bf16 per V^T row
+  __bf16 k[2][KT * KS];
   __bf16 v[2][D * VS];
 };
 
-template <int D>
-__device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm) {
-  constexpr int KCH = D / 64;  // 16-byte K chunks per thread per tile (32 keys x D)
-  constexpr int VCH = D / 64;  // 16-byte V chunks per thread per tile (D x 32 keys)
-  const int r = it[I_SEQ], g = it[I_KVH], row0 = it[I_ROW0], nrows = it[I_NROWS];
-  const int kv0 = it[I_KV0], part = it[I_PART];
+// Tile item (SHARED = false): 128 rows of one sequence, causal.  Shared-prefix
+// item (SHARED = true): 128 gathered rows of a cascade group's members over
+// keys every one of them sees; results go to the members' partial rows.
+template <int D, int NSUB, bool SHARED>
+__device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB>& sm) {
+  using Sm = TileSmem<D, NSUB>;
+  constexpr int KT = Sm::KT;
+  constexpr int NB = KT / kBlock;          // blocks per step
+  constexpr int KCH = KT * D / 8 / 256;    // 16-byte K chunks per thread per step
+  constexpr int VCH = D * NB * 2 / 256;    // 16-byte V^T chunks per thread per step
+  // With D = 128 every chunk i of a thread lies in block i of the step, so
+  // its source address is a wave-uniform block base plus a fixed offset.
+  constexpr bool kChunkIsBlock = (KCH == NB) && (VCH == NB);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, j = lane & 31, hh = lane >> 5;
-  const int L = a.seq_lens[r];
-  const int qs = a.cu_q[r], n = a.cu_q[r + 1] - qs;
-  const int kend = min(it[I_KV1], L);
   const int G = a.group;
-
   const int lr = w * 32 + j;
+  const int g = it[I_KVH], row0 = it[I_ROW0], nrows = it[I_NROWS], kv0 = it[I_KV0];
   const bool valid = lr < nrows;
-  const int rho = row0 + lr;
-  const int qi = rho / G;
-  const int hq = g * G + (rho - qi * G);
-  const int apos = valid ? L - n + qi : -1;
-  // Rows are ordered by query, so the wave's first row has its smallest
-  // position: key tiles entirely at or below it need no causal mask.
-  const int wave_amin = L - n + (row0 + w * 32) / G;
+  int key_seq, kend, qs, qi, hq, apos, wave_amin, part;
+  if constexpr (SHARED) {
+    // gathered row -> member sequence and its own row
+    const int rpm = it[S_RPM];
+    const int rg = row0 + lr;
+    const int mi = rg / rpm, rl = rg - mi * rpm;
+    const int32_t* mem = a.plan + it[S_MEMBERS] + 2 * (valid ? mi : 0);
+    const int seq = mem[0];
+    qs = a.cu_q[seq];
+    qi = rl / G;
+    hq = g * G + (rl - qi * G);
+    part = mem[1] + rl;
+    key_seq = it[S_BLOCK_SEQ];
+    kend = it[S_KV1];
+    apos = valid ? kend - 1 : -1;  // every shared key is visible
+    wave_amin = kend - 1;          // only a partial last step is masked
+  } else {
+    const int r = it[I_SEQ];
+    const int L = a.seq_lens[r];
+    qs = a.cu_q[r];
+    const int n = a.cu_q[r + 1] - qs;
+    const int rho = row0 + lr;
+    qi = rho / G;
+    hq = g * G + (rho - qi * G);
+    part = it[I_PART] < 0 ? -1 : it[I_PART] + lr;
+    key_seq = r;
+    kend = min(it[I_KV1], L);
+    apos = valid ? L - n + qi : -1;
+    // Rows are ordered by query, so the wave's first row has its smallest
+    // position: key sub-tiles entirely at or below it need no causal mask.
+    wave_amin = L - n + (row0 + w * 32) / G;
+  }
 
   bf16x8 qf[D / 16];
   {
@@ -104,54 +145,80 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   const float c = a.scale_log2;
   float m = kNegInf, mc = 0.f, l = 0.f;
 
-  const int32_t* bt = a.bt + (int64_t)r * a.max_blocks;
-  const int64_t head_k = (int64_t)g * kBlock * D;  // offset of head g inside a K block
+  const int32_t* bt = a.bt + (int64_t)key_seq * a.max_blocks;
+  const __bf16* kbase = a.kc + (int64_t)g * kBlock * D;  // head g inside block 0
+  const __bf16* vbase = a.vc + (int64_t)g * D * kBlock;
   const int64_t blk_k = (int64_t)a.hkv * kBlock * D;
-  const int64_t head_v = (int64_t)g * D * kBlock;
   const int64_t blk_v = (int64_t)a.hkv * D * kBlock;
 
+  // Per-thread chunk geometry (fixed for the whole item).
+  int k_off[KCH], k_row[KCH], k_blk[KCH], v_off[VCH], v_lds[VCH], v_blk[VCH], v_key[VCH];
+#pragma unroll
+  for (int i = 0; i < KCH; ++i) {
+    const int c8 = tid + 256 * i;
+    const int kk = c8 / (D / 8), part8 = c8 % (D / 8);
+    k_blk[i] = kk / kBlock;
+    k_off[i] = (kk % kBlock) * D + part8 * 8;
+    k_row[i] = ((kk & ~31) + perm32(kk & 31)) * Sm::KS + part8 * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < VCH; ++i) {
+    const int c8 = tid + 256 * i;
+    const int b = c8 / (2 * D), d = (c8 % (2 * D)) >> 1, half = c8 & 1;
+    v_blk[i] = b;
+    v_off[i] = d * kBlock + 8 * half;
+    v_lds[i] = d * Sm::VS + 16 * b + 8 * half;
+    v_key[i] = 16 * b + 8 * half;
+  }
+
   u32x4 kr[KCH], vr[VCH];
-  // Gather one 32-key tile (two blocks, ids read once per tile) into
-  // registers.  Every load is in bounds: a missing second block aliases the
-  // first; values of keys at or past kend are zeroed (never-written slots may
-  // hold anything), keys there are masked in the scores.
+  // Gather one KT-key step (NB blocks, ids read once per step) into
+  // registers.  Every load is in bounds: blocks past kend alias the step's
+  // first block; values of keys at or past kend are zeroed (never-written
+  // slots may hold anything), keys there are masked in the scores.
+  BlockWindow win;
+  win.init(bt, a.max_blocks, kv0 / kBlock);
   auto load_tile = [&](int t0) {
     const int jb = t0 / kBlock;
-    const int b0 = clamp_block(bt[min(jb, a.max_blocks - 1)], a.num_blocks);
-    const int b1 = t0 + 16 < kend ? clamp_block(bt[min(jb + 1, a.max_blocks - 1)], a.num_blocks) : b0;
+    int blk[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      blk[b] = (b == 0 || t0 + kBlock * b < kend) ? clamp_block(win.get(jb + b), a.num_blocks)
+                                                   : blk[0];
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
-      const int c8 = tid + 256 * i;
-      const int kk = c8 / (D / 8), part8 = c8 % (D / 8);
-      const int blk = kk < 16 ? b0 : b1;
-      kr[i] = ld16(a.kc + blk * blk_k + head_k + (kk & 15) * D + part8 * 8);
+      int bsel = blk[0];
+      if constexpr (kChunkIsBlock) {
+        bsel = blk[i];
+      } else {
+#pragma unroll
+        for (int b = 1; b < NB; ++b) bsel = k_blk[i] == b ? blk[b] : bsel;
+      }
+      kr[i] = ld16(kbase + bsel * blk_k + k_off[i]);
     }
-    const bool tail = t0 + 32 > kend;
+    const bool tail = t0 + KT > kend;
 #pragma unroll
     for (int i = 0; i < VCH; ++i) {
-      const int c8 = tid + 256 * i;
-      const int b = c8 / (2 * D), d = (c8 % (2 * D)) >> 1, half = c8 & 1;
-      u32x4 x = ld16(a.vc + (b ? b1 : b0) * blk_v + head_v + d * kBlock + 8 * half);
-      if (tail) x = keep_bf16(x, min(max(kend - (t0 + 16 * b + 8 * half), 0), 8));
+      int bsel = blk[0];
+      if constexpr (kChunkIsBlock) {
+        bsel = blk[i];
+      } else {
+#pragma unroll
+        for (int b = 1; b < NB; ++b) bsel = v_blk[i] == b ? blk[b] : bsel;
+      }
+      u32x4 x = ld16(vbase + bsel * blk_v + v_off[i]);
+      if (tail) x = keep_bf16(x, min(max(kend - (t0 + v_key[i]), 0), 8));
       vr[i] = x;
     }
   };
   auto store_tile = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c8 = tid + 256 * i;
-      const int kk = c8 / (D / 8), part8 = c8 % (D / 8);
-      st16(&sm.k[buf][perm32(kk) * TileSmem<D>::KS + part8 * 8], kr[i]);
-    }
+    for (int i = 0; i < KCH; ++i) st16(&sm.k[buf][k_row[i]], kr[i]);
 #pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c8 = tid + 256 * i;
-      const int b = c8 / (2 * D), d = (c8 % (2 * D)) >> 1, half = c8 & 1;
-      st16(&sm.v[buf][d * TileSmem<D>::VS + 16 * b + 8 * half], vr[i]);
-    }
+    for (int i = 0; i < VCH; ++i) st16(&sm.v[buf][v_lds[i]], vr[i]);
   };
 
-  const int ntiles = kend > kv0 ? (kend - kv0 + 31) / 32 : 0;
+  const int ntiles = kend > kv0 ? (kend - kv0 + KT - 1) / KT : 0;
   if (ntiles > 0) {
     load_tile(kv0);
     store_tile(0);
@@ -159,63 +226,71 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   __syncthreads();
   for (int tI = 0; tI < ntiles; ++tI) {
     const int buf = tI & 1;
-    const int t0 = kv0 + 32 * tI;
+    const int t0 = kv0 + KT * tI;
     const bool more = tI + 1 < ntiles;
-    if (more) load_tile(t0 + 32);
+    if (more) load_tile(t0 + KT);
 
-    // S^T[key][row] for the wave's 32 rows.
-    f32x16 s;
+    // S^T[key][row] for the wave's 32 rows, one independent chain per sub-tile.
+    if (PA_SETPRIO) __builtin_amdgcn_s_setprio(1);
+    f32x16 s[NSUB];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) s[e] = 0.f;
-    const __bf16* kb = &sm.k[buf][j * TileSmem<D>::KS + 8 * hh];
+    for (int u = 0; u < NSUB; ++u)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[u][e] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks)
-      s = mfma32(as_bf16x8(ld16(kb + 16 * ks)), qf[ks], s);
+#pragma unroll
+      for (int u = 0; u < NSUB; ++u)
+        s[u] = mfma32(as_bf16x8(ld16(&sm.k[buf][(32 * u + j) * Sm::KS + 16 * ks + 8 * hh])), qf[ks],
+                      s[u]);
 
-    if (t0 + 31 > wave_amin) {  // wave-uniform: only diagonal / tail tiles
+    if (PA_SETPRIO) __builtin_amdgcn_s_setprio(0);
+    // Softmax and PV per 32-key sub-tile: the VALU work of sub-tile u only
+    // depends on its own score chain, so it overlaps the MFMAs still running
+    // for the next sub-tile (scores) or the previous one (PV).
+    const bool diag = t0 + KT - 1 > wave_amin;  // wave-uniform: diagonal / tail steps
+#pragma unroll
+    for (int u = 0; u < NSUB; ++u) {
+      if (diag) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = t0 + 32 * u + perm32(8 * (e >> 2) + 4 * hh + (e & 3));
+          s[u][e] = key <= apos ? s[u][e] : kNegInf;
+        }
+      }
+      float mx = fmaxf(s[u][0], s[u][1]);
+#pragma unroll
+      for (int e = 2; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[u][e]), s[u][e + 1]);
+      mx = fmaxf(mx, wave_xor(mx, 32));
+      // Move the reference max only when a score exceeds it by more than 2^8
+      // (probabilities stay <= 256, exact for float32 sums and bf16
+      // operands); decided for the whole wavefront so every lane skips the
+      // rescale together.
+      if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
+        const float mnew = fmaxf(m, mx);
+        const float mcn = mnew == kNegInf ? 0.f : mnew * c;
+        const float alpha = m == kNegInf ? 0.f : fast_exp2(mc - mcn);
+        l *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
+        m = mnew;
+        mc = mcn;
+      }
+      bf16x8 pb0, pb1;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int key = t0 + perm32(8 * (e >> 2) + 4 * hh + (e & 3));
-        s[e] = key <= apos ? s[e] : kNegInf;
+        const float p = fast_exp2(fmaf(s[u][e], c, -mc));
+        l += p;
+        if (e < 8) pb0[e] = (__bf16)p; else pb1[e - 8] = (__bf16)p;
       }
-    }
-    float mx = fmaxf(fmaxf(s[0], s[1]), s[2]);
 #pragma unroll
-    for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, s[e]), s[e + 1]);
-    mx = fmaxf(mx, s[15]);
-    mx = fmaxf(mx, wave_xor(mx, 32));
-    // Move the reference max only when a score exceeds it by more than 2^8
-    // (probabilities stay <= 256, exact for float32 sums and bf16 operands);
-    // the decision is taken for the whole wavefront so the rescale is skipped
-    // by every lane together.
-    if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
-      const float mnew = fmaxf(m, mx);
-      const float mcn = mnew == kNegInf ? 0.f : mnew * c;
-      const float alpha = m == kNegInf ? 0.f : fast_exp2(mc - mcn);
-      l *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
-      m = mnew;
-      mc = mcn;
-    }
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      s[e] = fast_exp2(fmaf(s[e], c, -mc));
-      l += s[e];
-    }
-    bf16x8 pb0, pb1;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      pb0[e] = (__bf16)s[e];
-      pb1[e] = (__bf16)s[8 + e];
-    }
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) {
-      const __bf16* vb = &sm.v[buf][(32 * dt + j) * TileSmem<D>::VS + 8 * hh];
-      acc[dt] = mfma32(as_bf16x8(ld16(vb)), pb0, acc[dt]);
-      acc[dt] = mfma32(as_bf16x8(ld16(vb + 16)), pb1, acc[dt]);
+      for (int dt = 0; dt < D / 32; ++dt) {
+        const __bf16* vb = &sm.v[buf][(32 * dt + j) * Sm::VS + 32 * u + 8 * hh];
+        acc[dt] = mfma32(as_bf16x8(ld16(vb)), pb0, acc[dt]);
+        acc[dt] = mfma32(as_bf16x8(ld16(vb + 16)), pb1, acc[dt]);
+      }
     }
     if (more) store_tile(buf ^ 1);
     __syncthreads();
@@ -239,7 +314,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
       }
     if (a.lse && hh == 0) a.lse[(int64_t)(qs + qi) * a.hq + hq] = lse_v;
   } else {
-    float* op = a.ws_o + (int64_t)(part + lr) * D;
+    float* op = a.ws_o + (int64_t)part * D;
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
@@ -250,7 +325,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
         for (int e = 0; e < 4; ++e) o4[e] = acc[dt][4 * q4 + e] * inv;
         *reinterpret_cast<f32x4*>(op + d) = o4;
       }
-    if (hh == 0) a.ws_lse[part + lr] = lse_v;
+    if (hh == 0) a.ws_lse[part] = lse_v;
   }
 }
 
@@ -303,10 +378,12 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   // second block aliases the first).
   u32x4 kreg[2][KS], vreg[DT];
   int b0 = 0, b1 = 0;
+  BlockWindow win;
+  win.init(bt, a.max_blocks, kv0 / kBlock);
   auto blocks_of = [&](int t0) {
     const int jb = t0 / kBlock;
-    b0 = clamp_block(bt[min(jb, a.max_blocks - 1)], a.num_blocks);
-    b1 = t0 + 16 < kv1 ? clamp_block(bt[min(jb + 1, a.max_blocks - 1)], a.num_blocks) : b0;
+    b0 = clamp_block(win.get(jb), a.num_blocks);
+    b1 = t0 + 16 < kv1 ? clamp_block(win.get(jb + 1), a.num_blocks) : b0;
   };
   auto load_k = [&]() {
 #pragma unroll
@@ -409,18 +486,23 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   }
 }
 
-// MIX: 1 = tile items only, 2 = row items only, 3 = both (a mixed launch).
+// MIX: 1 = tile and shared items only, 2 = row items only, 3 = both.
 // Separate instantiations keep a pure prefill or pure decode launch from
 // paying the other path's registers and LDS.
 template <int D, int MIX>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   const int32_t* plan = a.plan;
-  const int n_tile = plan[H_N_TILE];
+  const int n_tile = plan[H_N_SHARED] + plan[H_N_TILE];  // workgroups before the row quads
   const int b = blockIdx.x;
   if constexpr (MIX & 1) {
-    __shared__ TileSmem<D> sm;
+    __shared__ TileSmem<D, kTileSub> sm;
+    const int n_shared = plan[H_N_SHARED];
+    if (b < n_shared) {
+      tile_item<D, kTileSub, true>(plan + plan[H_SHARED_OFF] + b * kSharedWords, a, sm);
+      return;
+    }
     if (b < n_tile) {
-      tile_item<D>(plan + plan[H_TILE_OFF] + b * kItemWords, a, sm);
+      tile_item<D, kTileSub, false>(plan + plan[H_TILE_OFF] + (b - n_shared) * kItemWords, a, sm);
       return;
     }
   }
@@ -431,32 +513,69 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
   }
 }
 
-// Combine split partial results by log-sum-exp: one workgroup per group, one
-// wavefront per row, each lane D/64 dims.
+// Combine split partial results by log-sum-exp: one workgroup per merge
+// group, one wavefront per row.  Lane s reads part s's LSE, the wavefront
+// reduces them, and each lane then accumulates D/64 output dims over the
+// parts with the weights broadcast from their lanes; the part loads are
+// independent, so they are issued back to back.
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(AttnArgs a) {
   const int32_t* plan = a.plan;
   const int32_t* gr = plan + plan[H_GROUP_OFF] + blockIdx.x * kGroupWords;
   const int r = gr[G_SEQ], g = gr[G_KVH], row0 = gr[G_ROW0], nrows = gr[G_NROWS];
-  const int nsplit = gr[G_NSPLIT], part = gr[G_PART];
+  const int nsplit = gr[G_NSPLIT], part = gr[G_PART], stride = gr[G_STRIDE];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int qs = a.cu_q[r];
   for (int lr = w; lr < nrows; lr += 4) {
+    // pass 1: max and sum of exp over the parts' LSEs (64 parts per round)
     float mx = kNegInf;
-    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, a.ws_lse[part + s * nrows + lr]);
+    for (int s0 = 0; s0 < nsplit; s0 += 64) {
+      const int s = s0 + lane;
+      const float v = s < nsplit ? a.ws_lse[part + s * stride + lr] : kNegInf;
+      mx = fmaxf(mx, v);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    float sum = 0.f;
+    if (mx != kNegInf) {
+      for (int s0 = 0; s0 < nsplit; s0 += 64) {
+        const int s = s0 + lane;
+        if (s < nsplit) sum += exp2f((a.ws_lse[part + s * stride + lr] - mx) * kLog2e);
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
+    const float lse_v = mx == kNegInf ? kNegInf : mx + kLn2 * __log2f(sum);
+    // pass 2: weighted sum of the normalised partial outputs
     float o[D / 64];
 #pragma unroll
     for (int k = 0; k < D / 64; ++k) o[k] = 0.f;
-    float lse_v = kNegInf;
     if (mx != kNegInf) {
-      float sum = 0.f;
-      for (int s = 0; s < nsplit; ++s) sum += exp2f((a.ws_lse[part + s * nrows + lr] - mx) * kLog2e);
-      lse_v = mx + kLn2 * __log2f(sum);
-      for (int s = 0; s < nsplit; ++s) {
-        const int pr = part + s * nrows + lr;
-        const float wgt = exp2f((a.ws_lse[pr] - lse_v) * kLog2e);
+      for (int s0 = 0; s0 < nsplit; s0 += 64) {
+        const int sl = s0 + lane;
+        const float wl = sl < nsplit ? exp2f((a.ws_lse[part + sl * stride + lr] - lse_v) * kLog2e) : 0.f;
+        const int cnt = min(64, nsplit - s0);
+        int s = 0;
+        for (; s + 4 <= cnt; s += 4) {
+          float x[4][D / 64], wt[4];
 #pragma unroll
-        for (int k = 0; k < D / 64; ++k) o[k] += wgt * a.ws_o[(int64_t)pr * D + lane + 64 * k];
+          for (int u = 0; u < 4; ++u) {
+            wt[u] = __shfl(wl, s + u, 64);
+            const float* src = a.ws_o + (int64_t)(part + (s0 + s + u) * stride + lr) * D + lane;
+#pragma unroll
+            for (int k = 0; k < D / 64; ++k) x[u][k] = src[64 * k];
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int k = 0; k < D / 64; ++k) o[k] = fmaf(wt[u], x[u][k], o[k]);
+        }
+        for (; s < cnt; ++s) {
+          const float wt = __shfl(wl, s, 64);
+          const float* src = a.ws_o + (int64_t)(part + (s0 + s) * stride + lr) * D + lane;
+#pragma unroll
+          for (int k = 0; k < D / 64; ++k) o[k] = fmaf(wt, src[64 * k], o[k]);
+        }
       }
     }
     const int rho = row0 + lr;

@@ -54,6 +54,37 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 __device__ __forceinline__ float wave_xor(float v, int mask) { return __shfl_xor(v, mask, 64); }
 
+// A wavefront's view of 64 consecutive entries of a block-table row, one per
+// lane, with the next 64 loaded one window ahead: block ids are then read with
+// v_readlane (no scalar-memory wait inside the key loop).
+struct BlockWindow {
+  const int32_t* row;
+  int max_blocks;
+  int base;  // first block index held in `cur`
+  int cur, next;
+
+  __device__ __forceinline__ int fetch(int first) const {
+    const int j = first + (threadIdx.x & 63);
+    return row[j < max_blocks ? j : max_blocks - 1];
+  }
+  __device__ __forceinline__ void init(const int32_t* r, int mb, int first_block) {
+    row = r;
+    max_blocks = mb;
+    base = first_block;
+    cur = fetch(base);
+    next = fetch(base + 64);
+  }
+  // Block id of logical block jb (wave-uniform, jb >= base, non-decreasing).
+  __device__ __forceinline__ int get(int jb) {
+    while (jb - base >= 64) {
+      base += 64;
+      cur = next;
+      next = fetch(base + 64);
+    }
+    return __builtin_amdgcn_readlane(cur, jb - base);
+  }
+};
+
 __device__ __forceinline__ int clamp_block(int b, int num_blocks) {
   return b < 0 ? 0 : (b >= num_blocks ? num_blocks - 1 : b);
 }

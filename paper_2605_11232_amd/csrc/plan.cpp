@@ -9,7 +9,17 @@
 // rows whose key range is split so the launch has enough wavefronts in flight
 // to stream the cache at HBM bandwidth; the row groups of one key range sit
 // next to each other so their loads meet in cache, and split partial results
-// are combined by log-sum-exp in a merge pass.  Paper: Section 5.2 (split
+// are combined by log-sum-exp in a merge pass.
+//
+// Shared prefixes (cascade): single-wave sequences whose block tables start
+// with the same blocks read the same prefix keys (Section 2, Automatic Prefix
+// Caching; Section 5.3, the same policy prefix across thousands of requests).
+// Their attention over the shared keys is computed once, as 128-row MFMA tiles
+// of all the group's query rows (every such query sees every shared key), and
+// merged with each sequence's private-key part by log-sum-exp: the prefix is
+// read from memory once per launch instead of once per sequence.
+//
+// Paper: Section 5.2 (split
 // prefills under a batched-token budget, mixed prefill and decode), Section 6,
 // Table "playbook" (long prefills blocking short decodes).
 //
@@ -20,6 +30,9 @@
 // ordered longest first (coarse counting sort) to shorten the tail.
 #include <algorithm>
 #include <array>
+#include <climits>
+#include <cstdint>
+#include <unordered_map>
 #include <vector>
 
 #include "internal.h"
@@ -93,7 +106,8 @@ std::vector<U> interleave(const std::vector<std::vector<U>>& queues) {
 }  // namespace
 
 extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int32_t* seq_lens,
-                            const int32_t* cu_seqlens_q, int32_t num_q_heads,
+                            const int32_t* cu_seqlens_q, const int32_t* block_table,
+                            int32_t max_blocks_per_seq, int32_t num_q_heads,
                             int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                             int32_t dtype, int32_t num_cus, int32_t* plan,
                             int64_t plan_capacity, pa_plan_info* info) {
@@ -111,6 +125,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     return pa::fail(PA_ERR_UNSUPPORTED, "pa_attn_plan: block_size %d (supported: 16)", block_size);
   if (dtype != PA_F32 && dtype != PA_BF16)
     return pa::fail(PA_ERR_UNSUPPORTED, "pa_attn_plan: dtype %d", dtype);
+  if (block_table && max_blocks_per_seq < 1)
+    return pa::fail(PA_ERR_ARG, "pa_attn_plan: max_blocks_per_seq %d < 1", max_blocks_per_seq);
   if (kind == PA_KIND_DECODE) n_q = 1;
   if (kind == PA_KIND_VERIFY && (n_q < 1 || n_q > 8))
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: verify n_q %d outside [1, 8]", n_q);
@@ -127,39 +143,95 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     if (kind != PA_KIND_PREFILL && n != n_q)
       return pa::fail(PA_ERR_ARG, "pa_attn_plan: sequence %d has q_len %d, plan kind needs %d", r,
                       n, n_q);
+    if (block_table && cdiv(seq_lens[r], block_size) > max_blocks_per_seq)
+      return pa::fail(PA_ERR_ARG, "pa_attn_plan: sequence %d needs more than %d blocks", r,
+                      max_blocks_per_seq);
   }
   const int32_t total_q = n_seqs > 0 ? cu_seqlens_q[n_seqs] : 0;
 
   std::vector<std::array<int32_t, pa::kGroupWords>> groups;
+  std::vector<int32_t> members;  // cascade member tables, (sequence, partial base) pairs
   int64_t partial_rows = 0;
-  std::vector<Rec> tiles;
+  std::vector<Rec> shared, tiles;
   std::vector<std::array<Rec, 4>> quads;
 
   if (dtype == PA_BF16) {
-    // Key-range split of row items: aim for enough single-wave items to keep
-    // ~16 wavefronts per CU busy, never below 256 keys per item.
-    int64_t row_keys = 0;
-    for (int32_t r = 0; r < n_seqs; ++r) {
-      const int32_t n = cu_seqlens_q[r + 1] - cu_seqlens_q[r];
-      if (n > 0 && n * G <= pa::kRowSeqRows)
-        row_keys += int64_t(seq_lens[r]) * num_kv_heads * cdiv(n * G, pa::kRowItemRows);
+    auto qlen = [&](int32_t r) { return cu_seqlens_q[r + 1] - cu_seqlens_q[r]; };
+    auto is_row = [&](int32_t r) { return qlen(r) > 0 && qlen(r) * G <= pa::kRowSeqRows; };
+
+    // Cascade groups: single-wave sequences with the same first block and
+    // q_len whose leading blocks coincide share those keys; attention over
+    // them runs once for all the group's rows.
+    std::vector<int32_t> kstart(n_seqs, 0);       // first private key
+    std::vector<int32_t> cgroup(n_seqs, -1);      // cascade group of a sequence
+    std::vector<std::vector<int32_t>> cg_members;
+    std::vector<int32_t> cg_keys, cg_chunks;  // shared keys, key chunks (one merge part each)
+    if (block_table) {
+      std::unordered_map<int64_t, int32_t> by_key;
+      std::vector<std::vector<int32_t>> cand;
+      for (int32_t r = 0; r < n_seqs; ++r) {
+        if (!is_row(r)) continue;
+        const int64_t key = (int64_t(block_table[int64_t(r) * max_blocks_per_seq]) << 8) | qlen(r);
+        auto it = by_key.find(key);
+        if (it == by_key.end()) {
+          by_key.emplace(key, int32_t(cand.size()));
+          cand.push_back({r});
+        } else {
+          cand[it->second].push_back(r);
+        }
+      }
+      for (auto& mem : cand) {
+        if (mem.size() < 2) continue;
+        const int32_t* b0 = block_table + int64_t(mem[0]) * max_blocks_per_seq;
+        int64_t lcp = max_blocks_per_seq;
+        int64_t limit = INT64_MAX;
+        for (int32_t r : mem) {
+          const int32_t* br = block_table + int64_t(r) * max_blocks_per_seq;
+          const int64_t nb = std::min<int64_t>(lcp, cdiv(seq_lens[r], block_size));
+          int64_t k = 0;
+          while (k < nb && br[k] == b0[k]) ++k;
+          lcp = k;
+          limit = std::min<int64_t>(limit, seq_lens[r] - qlen(r));
+        }
+        int64_t S = std::min<int64_t>(lcp * block_size, limit);
+        S = S / pa::kTileStep * pa::kTileStep;
+        if (S < pa::kSharedMinKeys) continue;
+        for (int32_t r : mem) {
+          kstart[r] = int32_t(S);
+          cgroup[r] = int32_t(cg_members.size());
+        }
+        cg_members.push_back(mem);
+        cg_keys.push_back(int32_t(S));
+        cg_chunks.push_back(int32_t(cdiv(S, pa::kSharedChunk)));
+      }
     }
+
+    // Key-range split of row items (private keys only for cascade members):
+    // aim for enough single-wave items to keep ~16 wavefronts per CU busy,
+    // never below 256 keys per item.
+    int64_t row_keys = 0;
+    for (int32_t r = 0; r < n_seqs; ++r)
+      if (is_row(r))
+        row_keys += int64_t(seq_lens[r] - kstart[r]) * num_kv_heads *
+                    cdiv(qlen(r) * G, pa::kRowItemRows);
     const int64_t target_waves = int64_t(num_cus) * 16;
     int64_t chunk = std::max<int64_t>(256, cdiv(row_keys, std::max<int64_t>(1, target_waves)));
     chunk = cdiv(chunk, pa::kKeyStep) * pa::kKeyStep;
 
     std::vector<std::vector<Rec>> head_tiles(num_kv_heads), head_rows(num_kv_heads);
     std::vector<std::vector<int64_t>> tile_cost(num_kv_heads), row_cost(num_kv_heads);
+    // partial base of (cascade group member, kv-head): member_base[r * Hkv + g]
+    std::vector<int32_t> member_base(cg_members.empty() ? 0 : size_t(n_seqs) * num_kv_heads, -1);
     {
       // exact per-head item counts, so the lists are allocated once
       int64_t nt = 0, nr = 0;
       for (int32_t r = 0; r < n_seqs; ++r) {
-        const int32_t n = cu_seqlens_q[r + 1] - cu_seqlens_q[r];
-        if (n == 0) continue;
-        if (n * G <= pa::kRowSeqRows)
-          nr += cdiv(n * G, pa::kRowItemRows) * std::max<int64_t>(1, cdiv(seq_lens[r], chunk));
+        if (qlen(r) == 0) continue;
+        if (is_row(r))
+          nr += cdiv(qlen(r) * G, pa::kRowItemRows) *
+                std::max<int64_t>(1, cdiv(seq_lens[r] - kstart[r], chunk));
         else
-          nt += cdiv(int64_t(n) * G, pa::kTileRows);
+          nt += cdiv(int64_t(qlen(r)) * G, pa::kTileRows);
       }
       for (int32_t g = 0; g < num_kv_heads; ++g) {
         head_tiles[g].reserve(nt);
@@ -169,36 +241,42 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       }
     }
     for (int32_t r = 0; r < n_seqs; ++r) {
-      const int32_t n = cu_seqlens_q[r + 1] - cu_seqlens_q[r];
+      const int32_t n = qlen(r);
       const int32_t L = seq_lens[r];
       if (n == 0) continue;
       const int32_t rows = n * G;
-      if (rows <= pa::kRowSeqRows) {
-        const int32_t nsplit = static_cast<int32_t>(std::max<int64_t>(1, cdiv(L, chunk)));
-        // equal key ranges, multiples of the key step, covering [0, L)
-        const int64_t per = cdiv(cdiv(L, nsplit), pa::kKeyStep) * pa::kKeyStep;
+      if (is_row(r)) {
+        const int32_t k0s = kstart[r];
+        const int32_t nsplit = static_cast<int32_t>(std::max<int64_t>(1, cdiv(L - k0s, chunk)));
+        // equal private key ranges, multiples of the key step, covering [k0s, L)
+        const int64_t per = cdiv(cdiv(L - k0s, nsplit), pa::kKeyStep) * pa::kKeyStep;
         int32_t used = 0;
-        while (used < nsplit && int64_t(used) * per < L) ++used;
+        while (used < nsplit && k0s + int64_t(used) * per < L) ++used;
+        // parts 0 .. first-1 are the shared prefix's key chunks
+        const int32_t first = cgroup[r] >= 0 ? cg_chunks[cgroup[r]] : 0;
+        const int32_t parts = used + first;
         const int32_t ngroups = static_cast<int32_t>(cdiv(rows, pa::kRowItemRows));
         for (int32_t g = 0; g < num_kv_heads; ++g) {
-          int64_t base[pa::kRowSeqRows / pa::kRowItemRows];
-          for (int32_t gi = 0; gi < ngroups; ++gi) {
-            const int32_t row0 = gi * pa::kRowItemRows;
-            const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
-            base[gi] = used > 1 ? partial_rows : -1;
-            if (used > 1) {
-              groups.push_back({r, g, row0, nr, used, int32_t(partial_rows), 0, 0});
-              partial_rows += int64_t(used) * nr;
-            }
-          }
-          // per split, the row groups back to back
-          for (int32_t sp = 0; sp < used; ++sp) {
-            const int64_t k0 = sp * per, k1 = std::min<int64_t>(L, (sp + 1) * per);
+          int64_t base = -1;
+          if (parts > 1) {
+            base = partial_rows;
+            partial_rows += int64_t(parts) * rows;
             for (int32_t gi = 0; gi < ngroups; ++gi) {
               const int32_t row0 = gi * pa::kRowItemRows;
               const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
-              head_rows[g].push_back({r, g, row0, nr, int32_t(k0), int32_t(k1),
-                                      base[gi] < 0 ? -1 : int32_t(base[gi] + int64_t(sp) * nr), 0});
+              groups.push_back({r, g, row0, nr, parts, int32_t(base + row0), rows, 0});
+            }
+            if (first) member_base[size_t(r) * num_kv_heads + g] = int32_t(base);
+          }
+          // per split, the row groups back to back
+          for (int32_t sp = 0; sp < used; ++sp) {
+            const int64_t k0 = k0s + sp * per, k1 = std::min<int64_t>(L, k0s + (sp + 1) * per);
+            for (int32_t gi = 0; gi < ngroups; ++gi) {
+              const int32_t row0 = gi * pa::kRowItemRows;
+              const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
+              const int32_t part =
+                  base < 0 ? -1 : int32_t(base + int64_t(sp + first) * rows + row0);
+              head_rows[g].push_back({r, g, row0, nr, int32_t(k0), int32_t(k1), part, 0});
               row_cost[g].push_back(k1 - k0);
             }
           }
@@ -217,15 +295,52 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         }
       }
     }
-    // Tile items: per head, longest first, dealt round robin to the head's
-    // XCD queues (which stay longest first).
-    std::vector<std::vector<Rec>> tile_q(kXcds);
-    for (int32_t g = 0; g < num_kv_heads; ++g) {
-      const auto xs = xcds_of_head(g, num_kv_heads);
-      const auto ord = order_longest_first(tile_cost[g]);
-      for (size_t i = 0; i < ord.size(); ++i) tile_q[xs[i % xs.size()]].push_back(head_tiles[g][ord[i]]);
+    // Shared-prefix items: per cascade group and kv-head, a member table and
+    // 128-row tiles of the gathered rows over key chunks of the shared keys.
+    std::vector<std::vector<Rec>> head_shared(num_kv_heads);
+    std::vector<std::vector<int64_t>> shared_cost(num_kv_heads);
+    for (size_t cg = 0; cg < cg_members.size(); ++cg) {
+      const auto& mem = cg_members[cg];
+      const int32_t S = cg_keys[cg];
+      const int32_t rpm = qlen(mem[0]) * G;
+      const int64_t total_rows = int64_t(rpm) * mem.size();
+      const int32_t nch = cg_chunks[cg];
+      // chunk boundaries on the tile step; every chunk is non-empty because
+      // S / nch >= kSharedChunk / 2 > kTileStep
+      auto bound = [&](int64_t c) {
+        return c >= nch ? int64_t(S) : (c * S / nch) / pa::kTileStep * pa::kTileStep;
+      };
+      for (int32_t g = 0; g < num_kv_heads; ++g) {
+        for (int32_t ch = 0; ch < nch; ++ch) {
+          const int64_t k0 = bound(ch), k1 = bound(ch + 1);
+          // member table of this chunk: (sequence, partial row of its row 0)
+          const int32_t off = int32_t(members.size());
+          for (int32_t r : mem) {
+            members.push_back(r);
+            members.push_back(member_base[size_t(r) * num_kv_heads + g] + ch * rpm);
+          }
+          for (int64_t row0 = 0; row0 < total_rows; row0 += pa::kTileRows) {
+            const int32_t nrows = int32_t(std::min<int64_t>(pa::kTileRows, total_rows - row0));
+            head_shared[g].push_back({off, g, int32_t(row0), nrows, int32_t(k0), int32_t(k1), rpm,
+                                      mem[0]});
+            shared_cost[g].push_back((k1 - k0) * nrows);
+          }
+        }
+      }
     }
-    tiles = interleave(tile_q);
+    // Shared and tile items: per head, longest first, dealt round robin to the
+    // head's XCD queues (which stay longest first).
+    auto deal = [&](std::vector<std::vector<Rec>>& lists, std::vector<std::vector<int64_t>>& costs) {
+      std::vector<std::vector<Rec>> q(kXcds);
+      for (int32_t g = 0; g < num_kv_heads; ++g) {
+        const auto xs = xcds_of_head(g, num_kv_heads);
+        const auto ord = order_longest_first(costs[g]);
+        for (size_t i = 0; i < ord.size(); ++i) q[xs[i % xs.size()]].push_back(lists[g][ord[i]]);
+      }
+      return interleave(q);
+    };
+    shared = deal(head_shared, shared_cost);
+    tiles = deal(head_tiles, tile_cost);
     // Row items: per head, longest first, four to a workgroup (padded with
     // empty items) so a workgroup's waves share one kv-head.
     std::vector<std::vector<std::array<Rec, 4>>> quad_q(kXcds);
@@ -245,17 +360,20 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
 
   const int64_t n_row = int64_t(quads.size()) * 4;
   const int64_t n_groups = int64_t(groups.size());
-  const int64_t tile_off = pa::kHeaderWords;
+  const int64_t shared_off = pa::kHeaderWords;
+  const int64_t tile_off = shared_off + int64_t(shared.size()) * pa::kSharedWords;
   const int64_t row_off = tile_off + int64_t(tiles.size()) * pa::kItemWords;
   const int64_t group_off = row_off + n_row * pa::kItemWords;
-  const int64_t words = group_off + n_groups * pa::kGroupWords;
+  const int64_t member_off = group_off + n_groups * pa::kGroupWords;
+  const int64_t words = member_off + int64_t(members.size());
   const int64_t grid = dtype == PA_F32 ? int64_t(total_q) * num_q_heads
-                                       : int64_t(tiles.size()) + int64_t(quads.size());
+                                       : int64_t(shared.size() + tiles.size() + quads.size());
   if (words >= (int64_t{1} << 31) || grid >= (int64_t{1} << 31) || partial_rows >= (int64_t{1} << 31))
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: launch too large");
 
   info->kind = kind;
   info->n_q = n_q;
+  info->n_shared_items = int32_t(shared.size());
   info->n_tile_items = int32_t(tiles.size());
   info->n_row_items = int32_t(n_row);
   info->n_groups = int32_t(n_groups);
@@ -273,6 +391,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   std::fill(h, h + pa::kHeaderWords, 0);
   h[pa::H_MAGIC] = pa::kPlanMagic;
   h[pa::H_KIND] = kind;
+  h[pa::H_N_SHARED] = int32_t(shared.size());
   h[pa::H_N_TILE] = int32_t(tiles.size());
   h[pa::H_N_ROW] = int32_t(n_row);
   h[pa::H_N_GROUPS] = int32_t(n_groups);
@@ -282,14 +401,22 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   h[pa::H_D] = head_dim;
   h[pa::H_N_SEQS] = n_seqs;
   h[pa::H_TOTAL_Q] = total_q;
+  h[pa::H_SHARED_OFF] = int32_t(shared_off);
   h[pa::H_TILE_OFF] = int32_t(tile_off);
   h[pa::H_ROW_OFF] = int32_t(row_off);
   h[pa::H_GROUP_OFF] = int32_t(group_off);
+  h[pa::H_MEMBER_OFF] = int32_t(member_off);
   h[pa::H_PARTIAL_ROWS] = int32_t(partial_rows);
-  int32_t* p = plan + tile_off;
+  int32_t* p = plan + shared_off;
+  for (auto& it : shared) {
+    Rec w = it;
+    w[pa::S_MEMBERS] += int32_t(member_off);  // absolute word offset of the member table
+    p = std::copy(w.begin(), w.end(), p);
+  }
   for (auto& it : tiles) p = std::copy(it.begin(), it.end(), p);
   for (auto& q : quads)
     for (auto& it : q) p = std::copy(it.begin(), it.end(), p);
   for (auto& g : groups) p = std::copy(g.begin(), g.end(), p);
+  std::copy(members.begin(), members.end(), p);
   return PA_OK;
 }

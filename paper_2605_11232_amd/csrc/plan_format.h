@@ -12,21 +12,23 @@ constexpr int32_t kPlanMagic = 0x31304150;  // "PA01"
 enum : int32_t {
   H_MAGIC = 0,
   H_KIND,
+  H_N_SHARED,      // shared-prefix tile items (cascade), one workgroup each
   H_N_TILE,        // 128-row items, one workgroup each
   H_N_ROW,         // <= kRowItemRows-row items, one wavefront each (multiple of 4, padded)
-  H_N_GROUPS,      // split groups combined by the merge kernel
-  H_GRID,          // workgroups of the attention launch = N_TILE + N_ROW / 4
+  H_N_GROUPS,      // merge groups combined by the merge kernel
+  H_GRID,          // workgroups of the attention launch = N_SHARED + N_TILE + N_ROW / 4
   H_HQ,
   H_HKV,
   H_D,
   H_N_SEQS,
   H_TOTAL_Q,
-  H_RESERVED,
+  H_SHARED_OFF,    // word offset of the shared items
   H_TILE_OFF,      // word offset of the tile items
   H_ROW_OFF,       // word offset of the row items
-  H_GROUP_OFF,     // word offset of the split groups
+  H_GROUP_OFF,     // word offset of the merge groups
+  H_MEMBER_OFF,    // word offset of the cascade member tables
   H_PARTIAL_ROWS,  // rows of partial results in the workspace
-  kHeaderWords = 16
+  kHeaderWords = 24
 };
 
 // Work item (tile or row item): rows [row0, row0 + nrows) of sequence seq's
@@ -39,16 +41,31 @@ enum : int32_t {
   kItemWords = 8
 };
 
-// Split group: rows [row0, row0 + nrows) of (seq, kvh) were computed by
-// nsplit items whose partial rows start at part + s * nrows.
+// Shared-prefix item: gathered rows [row0, row0 + nrows) of a cascade group's
+// members (member m owns gathered rows m * rpm .. m * rpm + rpm - 1, its own
+// rows in order) for kv-head kvh, over the group's shared keys [kv0, kv1),
+// which every member's block table maps to the same blocks (read from
+// sequence block_seq's row).  The member table at word offset members holds
+// (sequence, partial base) pairs; member m's row rho goes to partial row
+// base + rho (split 0 of its merge group).
 enum : int32_t {
-  G_SEQ = 0, G_KVH, G_ROW0, G_NROWS, G_NSPLIT, G_PART, G_PAD0, G_PAD1,
+  S_MEMBERS = 0, S_KVH, S_ROW0, S_NROWS, S_KV0, S_KV1, S_RPM, S_BLOCK_SEQ,
+  kSharedWords = 8
+};
+
+// Merge group: rows [row0, row0 + nrows) of (seq, kvh) were computed by
+// nsplit parts; part s of row rho is at partial row part + s * stride + (rho - row0).
+enum : int32_t {
+  G_SEQ = 0, G_KVH, G_ROW0, G_NROWS, G_NSPLIT, G_PART, G_STRIDE, G_PAD1,
   kGroupWords = 8
 };
 
 constexpr int32_t kTileRows = 128;    // rows per tile item (4 waves x 32)
 constexpr int32_t kRowItemRows = 16;  // rows per single-wave item (one 16-column MFMA tile)
 constexpr int32_t kRowSeqRows = 64;   // sequences with at most this many rows use row items
-constexpr int32_t kKeyStep = 32;         // keys per inner iteration
+constexpr int32_t kKeyStep = 32;      // keys per row-item inner iteration
+constexpr int32_t kTileStep = 64;     // keys per tile-item inner iteration
+constexpr int32_t kSharedChunk = 2048;  // most shared keys one cascade item covers
+constexpr int32_t kSharedMinKeys = 256; // shorter shared prefixes are not split off
 
 }  // namespace pa

@@ -71,7 +71,8 @@ class Staging:
 
 
 class DeviceReplay:
-    def __init__(self, wl, device: str = "cuda", kind: str | None = None, num_cus: int = 0):
+    def __init__(self, wl, device: str = "cuda", kind: str | None = None, num_cus: int = 0,
+                 cascade: bool = True):
         cfg = wl.cfg
         self.wl, self.cfg, self.device = wl, cfg, torch.device(device)
         self.tdtype = torch_dtype(cfg.dtype)
@@ -84,6 +85,7 @@ class DeviceReplay:
         self.v_cache = torch.empty(shape_v, dtype=self.tdtype, device=self.device)
         self.kind = kind
         self.num_cus = num_cus
+        self.cascade = cascade
         self.n_cached = {}
 
     # -- host ops ------------------------------------------------------------
@@ -150,7 +152,8 @@ class DeviceReplay:
         kind = self.launch_kind(launch)
         n_q = launch.q_lens[0] if kind == "verify" else 1
         plan, info = B.plan(KIND[kind], n_q, md["seq_lens"], md["cu_seqlens_q"], cfg.num_q_heads,
-                            cfg.num_kv_heads, cfg.head_dim, cfg.block_size, self.dcode, self.num_cus)
+                            cfg.num_kv_heads, cfg.head_dim, cfg.block_size, self.dcode, self.num_cus,
+                            block_table=md["block_table"] if self.cascade else None)
         if q is None:
             q = torch.from_numpy(launch.q.get()).to(dev, self.tdtype)
         if k_new is None:
@@ -190,7 +193,8 @@ class DeviceReplay:
         n_q = launch.q_lens[0] if kind == "verify" else 1
         plan, info = B.plan(KIND[kind], n_q, md["seq_lens"], md["cu_seqlens_q"], cfg.num_q_heads,
                             cfg.num_kv_heads, cfg.head_dim, cfg.block_size, self.dcode,
-                            self.num_cus, out=st.plan[0].numpy())
+                            self.num_cus, out=st.plan[0].numpy(),
+                            block_table=md["block_table"] if self.cascade else None)
         if info.plan_words > st.plan[0].numel():
             raise RuntimeError("staging plan buffer too small")
         for (h, d), cnt in ((st.bt, n * st.max_blocks), (st.sl, n), (st.cu, n + 1),

@@ -166,11 +166,69 @@ def test_workload_tables_bit_exact(name):
         assert o.free_list() == l.free_list()
 
 
+# plan layout (plan_format.h): header words, record sizes
+H_N_SHARED, H_N_TILE, H_N_ROW, H_N_GROUPS, H_GRID = 2, 3, 4, 5, 6
+H_SHARED_OFF, H_TILE_OFF, H_ROW_OFF, H_GROUP_OFF, H_MEMBER_OFF, H_PARTIAL_ROWS = 12, 13, 14, 15, 16, 17
+
+
+def parse_plan(plan):
+    h = plan[:24]
+    rec = lambda off, n: plan[off:off + 8 * n].reshape(-1, 8).tolist()
+    return (h, rec(h[H_SHARED_OFF], h[H_N_SHARED]), rec(h[H_TILE_OFF], h[H_N_TILE]),
+            rec(h[H_ROW_OFF], h[H_N_ROW]), rec(h[H_GROUP_OFF], h[H_N_GROUPS]))
+
+
+def check_plan(plan, info, L, cu, G, hkv, D=128):
+    """Every (sequence, kv-head, row) is produced exactly once: by one item
+    covering all its visible keys, or by parts whose key ranges tile [0, L)
+    and whose partial rows are exactly those of its merge group."""
+    h, shared, tiles, rows, groups = parse_plan(plan)
+    assert h[0] == 0x31304150 and h[H_GRID] == info.grid
+    assert info.grid == h[H_N_SHARED] + h[H_N_TILE] + h[H_N_ROW] // 4
+    n = len(L)
+    q = np.diff(cu)
+    cover = {}      # (seq, kvh, rho) -> list of (kv0, kv1, partial row or -1)
+    writes = {}     # partial row -> count
+    def add(key, kv0, kv1, pr):
+        cover.setdefault(key, []).append((kv0, kv1, pr))
+        if pr >= 0:
+            writes[pr] = writes.get(pr, 0) + 1
+    for seq, kvh, row0, nrows, kv0, kv1, part, _ in tiles + rows:
+        if seq < 0:
+            continue
+        assert kv0 % 16 == 0 and 0 <= kv0 < kv1 <= L[seq]
+        for lr in range(nrows):
+            add((seq, kvh, row0 + lr), kv0, kv1, -1 if part < 0 else part + lr)
+    for moff, kvh, row0, nrows, kv0, kv1, rpm, bseq in shared:
+        assert kv0 % 64 == 0 and kv1 % 64 == 0
+        for lr in range(nrows):
+            rg = row0 + lr
+            m, rl = divmod(rg, rpm)
+            seq, base = plan[moff + 2 * m], plan[moff + 2 * m + 1]
+            assert kv1 <= L[seq] - q[seq]          # every shared key is visible
+            add((seq, kvh, rl), kv0, kv1, base + rl)
+    assert len(cover) == sum(int(q[s]) * G * hkv for s in range(n))
+    expected = {}
+    for seq, kvh, row0, nrows, nsplit, part, stride, _ in groups:
+        for lr in range(nrows):
+            expected[(seq, kvh, row0 + lr)] = {part + sp * stride + lr for sp in range(nsplit)}
+    for key, ranges in cover.items():
+        seq, kvh, rho = key
+        ranges.sort()
+        need = int(L[seq] - q[seq] + rho // G + 1)
+        if len(ranges) == 1 and ranges[0][2] == -1:
+            assert key not in expected and ranges[0][0] == 0 and ranges[0][1] >= need
+        else:
+            assert {pr for _, _, pr in ranges} == expected[key]
+            assert ranges[0][0] == 0 and ranges[-1][1] == L[seq]
+            assert all(ranges[i][1] == ranges[i + 1][0] for i in range(len(ranges) - 1))
+    assert set(writes) == set(range(h[H_PARTIAL_ROWS])) and set(writes.values()) <= {1}
+    assert int(info.workspace_bytes) == int(h[H_PARTIAL_ROWS]) * (D + 1) * 4
+
+
 def test_plan_covers_every_row_once():
-    """Each (token, head) row is produced exactly once: by one unsplit item or
-    by one split group whose items cover [0, seq_len) without overlap."""
     r = np.random.default_rng(5)
-    for trial in range(30):
+    for trial in range(40):
         n = int(r.integers(1, 40))
         hkv = int(r.choice([1, 2, 4, 8]))
         G = int(r.choice([1, 4, 7, 8]))
@@ -180,32 +238,56 @@ def test_plan_covers_every_row_once():
             q[:] = 1
         cu = np.concatenate([[0], np.cumsum(q)])
         kind = B.KIND_DECODE if trial % 3 == 0 else B.KIND_PREFILL
-        plan, info = B.plan(kind, 1, L, cu, hkv * G, hkv, 128, 16, B.PA_BF16, 256)
-        h = plan[:16]
-        assert h[0] == 0x31304150 and h[5] == info.grid == h[2] + h[3] // 4
-        items = plan[h[12]:h[12] + 8 * h[2]].reshape(-1, 8).tolist()
-        items += plan[h[13]:h[13] + 8 * h[3]].reshape(-1, 8).tolist()
-        groups = plan[h[14]:h[14] + 8 * h[4]].reshape(-1, 8)
-        cover = {}
-        for seq, kvh, row0, nrows, kv0, kv1, part, _ in items:
-            if seq < 0:
-                continue
-            assert kv0 % 32 == 0 and 0 <= kv0 < kv1 <= L[seq]
-            for rho in range(row0, row0 + nrows):
-                cover.setdefault((seq, kvh, rho), []).append((kv0, kv1, part))
-        assert len(cover) == sum(int(q[s]) * G * hkv for s in range(n))
-        for (seq, kvh, rho), ranges in cover.items():
-            ranges.sort()
-            last_q = rho // G
-            need = int(L[seq] - q[seq] + last_q + 1)
-            if len(ranges) == 1:
-                assert ranges[0][2] == -1 and ranges[0][0] == 0 and ranges[0][1] >= need
+        # block tables: a few prefix groups share leading blocks
+        mb = int((L.max() + 15) // 16)
+        bt = np.full((n, mb), -1, np.int32)
+        nxt = 0
+        prefixes = [r.integers(0, 200) for _ in range(3)]
+        shared_blocks = {}
+        for s_ in range(n):
+            nb = int((L[s_] + 15) // 16)
+            grp = int(r.integers(0, 4))
+            if grp < 3:
+                pb = min(nb - 1, int(prefixes[grp]))
+                base = shared_blocks.setdefault(grp, list(range(10 ** 6 + 1000 * grp, 10 ** 6 + 1000 * grp + 300)))
+                bt[s_, :pb] = base[:pb]
+                bt[s_, pb:nb] = np.arange(nxt, nxt + nb - pb)
+                nxt += nb - pb
             else:
-                assert all(p >= 0 for _, _, p in ranges)
-                assert ranges[0][0] == 0 and ranges[-1][1] == L[seq]
-                assert all(ranges[i][1] == ranges[i + 1][0] for i in range(len(ranges) - 1))
-        assert int(info.workspace_bytes) == int(h[15]) * (128 + 1) * 4
-        assert sum(int(g[3]) * int(g[4]) for g in groups) == h[15]
+                bt[s_, :nb] = np.arange(nxt, nxt + nb)
+                nxt += nb
+        for table in (None, bt):
+            plan, info = B.plan(kind, 1, L, cu, hkv * G, hkv, 128, 16, B.PA_BF16, 256,
+                                block_table=table)
+            check_plan(plan, info, L, cu, G, hkv)
+            if table is None:
+                assert info.n_shared_items == 0
+
+
+def test_plan_finds_shared_prefix_of_workloads():
+    """The decode and verify workloads share their whole cached prefix."""
+    for name, prefix in (("decode", 2048), ("verify", 16384)):
+        wl = synth.workload(name, scale=0.25)
+        o = PrefixCacheOracle(wl.num_blocks, wl.cfg.block_size, wl.free_order)
+        for op in wl.setup:
+            if op.kind == "add":
+                o.add(op.seq_id, op.tokens)
+            elif op.kind == "free":
+                o.free_seq(op.seq_id)
+        launch = wl.step(0)
+        for op in launch.pre:
+            o.extend(op.seq_id, op.tokens)
+        md = o.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
+        cfg = wl.cfg
+        kind = B.KIND_DECODE if name == "decode" else B.KIND_VERIFY
+        plan, info = B.plan(kind, launch.q_lens[0], md["seq_lens"], md["cu_seqlens_q"],
+                            cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 16, B.PA_BF16,
+                            block_table=md["block_table"])
+        h, shared, *_ = parse_plan(plan)
+        assert info.n_shared_items > 0
+        P = wl.notes["prefix"]
+        assert max(s[5] for s in shared) == P // 64 * 64
+        check_plan(plan, info, md["seq_lens"], md["cu_seqlens_q"], cfg.group, cfg.num_kv_heads)
 
 
 def test_device_calls_reject_bad_arguments_without_launching():

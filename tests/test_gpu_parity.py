@@ -233,3 +233,26 @@ def test_edge_cases():
         torch.cuda.synchronize()
         assert (p.info.n_tile_items > 0) == want_tiles
         close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"verify-G{G}")
+
+
+@pytest.mark.parametrize("name,scale", [("decode", 0.125), ("verify", 0.25), ("mixed", 0.125)])
+def test_shared_prefix_cascade_matches_per_sequence(name, scale):
+    """With shared-prefix groups (prefix attention once for all sequences,
+    merged by log-sum-exp) and without them, outputs agree within the bf16
+    tolerance and both match the oracle."""
+    _gpu()
+    from paper_2605_11232_amd.runtime import DeviceReplay
+    from tests.parity import TOL, close
+    outs = []
+    for cascade in (True, False):
+        wl = synth.workload(name, scale=scale, steps=2)
+        d = DeviceReplay(wl, cascade=cascade).setup()
+        p = d.run(wl.launches[0])
+        torch.cuda.synchronize()
+        if cascade:
+            assert p.info.n_shared_items > 0
+        else:
+            assert p.info.n_shared_items == 0
+        outs.append((p.out.float().cpu().numpy(), p.lse.cpu().numpy()))
+    close(outs[0][0], outs[1][0], *TOL["bf16"], f"{name} cascade vs per-sequence")
+    close(outs[0][1], outs[1][1], 2e-3, 1e-4, f"{name} lse cascade vs per-sequence")
