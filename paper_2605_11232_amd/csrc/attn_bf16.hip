@@ -151,10 +151,14 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
   const int64_t blk_k = (int64_t)a.hkv * kBlock * D;
   const int64_t blk_v = (int64_t)a.hkv * D * kBlock;
 
-  // Per-thread chunk geometry (fixed for the whole item).
-  int k_off[KCH], k_row[KCH], k_blk[KCH], v_off[VCH], v_lds[VCH], v_blk[VCH], v_key[VCH];
+  // Per-thread chunk geometry (fixed for the whole item).  With D = 128 chunk
+  // i of a thread is block i of the step at the same in-block offset, so one
+  // base offset and a compile-time stride describe all of a thread's chunks
+  // (fewer live registers); otherwise each chunk keeps its own.
+  constexpr int GK = kChunkIsBlock ? 1 : KCH, GV = kChunkIsBlock ? 1 : VCH;
+  int k_off[GK], k_row[GK], k_blk[GK], v_off[GV], v_lds[GV], v_blk[GV], v_key[GV];
 #pragma unroll
-  for (int i = 0; i < KCH; ++i) {
+  for (int i = 0; i < GK; ++i) {
     const int c8 = tid + 256 * i;
     const int kk = c8 / (D / 8), part8 = c8 % (D / 8);
     k_blk[i] = kk / kBlock;
@@ -162,7 +166,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     k_row[i] = ((kk & ~31) + perm32(kk & 31)) * Sm::KS + part8 * 8;
   }
 #pragma unroll
-  for (int i = 0; i < VCH; ++i) {
+  for (int i = 0; i < GV; ++i) {
     const int c8 = tid + 256 * i;
     const int b = c8 / (2 * D), d = (c8 % (2 * D)) >> 1, half = c8 & 1;
     v_blk[i] = b;
@@ -170,15 +174,20 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     v_lds[i] = d * Sm::VS + 16 * b + 8 * half;
     v_key[i] = 16 * b + 8 * half;
   }
+  // chunk i's entries: the stored one, or chunk 0's plus the fixed stride
+  auto K_OFF = [&](int i) { return kChunkIsBlock ? k_off[0] : k_off[i]; };
+  auto K_ROW = [&](int i) { return kChunkIsBlock ? k_row[0] + 16 * i * Sm::KS : k_row[i]; };
+  auto V_OFF = [&](int i) { return kChunkIsBlock ? v_off[0] : v_off[i]; };
+  auto V_LDS = [&](int i) { return kChunkIsBlock ? v_lds[0] + 16 * i : v_lds[i]; };
+  auto V_KEY = [&](int i) { return kChunkIsBlock ? v_key[0] + 16 * i : v_key[i]; };
 
-  u32x4 kr[KCH], vr[VCH];
   // Gather one KT-key step (NB blocks, ids read once per step) into
   // registers.  Every load is in bounds: blocks past kend alias the step's
   // first block; values of keys at or past kend are zeroed (never-written
   // slots may hold anything), keys there are masked in the scores.
   BlockWindow win;
   win.init(bt, a.max_blocks, kv0 / kBlock);
-  auto load_tile = [&](int t0) {
+  auto load_tile = [&](int t0, u32x4 (&kr)[KCH], u32x4 (&vr)[VCH]) {
     const int jb = t0 / kBlock;
     int blk[NB];
 #pragma unroll
@@ -194,7 +203,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
 #pragma unroll
         for (int b = 1; b < NB; ++b) bsel = k_blk[i] == b ? blk[b] : bsel;
       }
-      kr[i] = ld16(kbase + bsel * blk_k + k_off[i]);
+      kr[i] = ld16(kbase + bsel * blk_k + K_OFF(i));
     }
     const bool tail = t0 + KT > kend;
 #pragma unroll
@@ -206,29 +215,30 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
 #pragma unroll
         for (int b = 1; b < NB; ++b) bsel = v_blk[i] == b ? blk[b] : bsel;
       }
-      u32x4 x = ld16(vbase + bsel * blk_v + v_off[i]);
-      if (tail) x = keep_bf16(x, min(max(kend - (t0 + v_key[i]), 0), 8));
+      u32x4 x = ld16(vbase + bsel * blk_v + V_OFF(i));
+      if (tail) x = keep_bf16(x, min(max(kend - (t0 + V_KEY(i)), 0), 8));
       vr[i] = x;
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, const u32x4 (&kr)[KCH], const u32x4 (&vr)[VCH]) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) st16(&sm.k[buf][k_row[i]], kr[i]);
+    for (int i = 0; i < KCH; ++i) st16(&sm.k[buf][K_ROW(i)], kr[i]);
 #pragma unroll
-    for (int i = 0; i < VCH; ++i) st16(&sm.v[buf][v_lds[i]], vr[i]);
+    for (int i = 0; i < VCH; ++i) st16(&sm.v[buf][V_LDS(i)], vr[i]);
   };
 
+  // Two register sets of staged K/V: the loads of step t + 2 are issued at the
+  // start of step t and written to LDS at the end of step t + 1, so each load
+  // has two steps of compute to arrive (L2 misses included).  LDS is double
+  // buffered: step t reads buffer t % 2 while step t + 1's data is stored into
+  // the other one.
+  u32x4 krA[KCH], vrA[VCH], krB[KCH], vrB[VCH];
   const int ntiles = kend > kv0 ? (kend - kv0 + KT - 1) / KT : 0;
-  if (ntiles > 0) {
-    load_tile(kv0);
-    store_tile(0);
-  }
-  __syncthreads();
-  for (int tI = 0; tI < ntiles; ++tI) {
+  auto step = [&](int tI, u32x4 (&kr_issue)[KCH], u32x4 (&vr_issue)[VCH],
+                  const u32x4 (&kr_store)[KCH], const u32x4 (&vr_store)[VCH]) {
     const int buf = tI & 1;
     const int t0 = kv0 + KT * tI;
-    const bool more = tI + 1 < ntiles;
-    if (more) load_tile(t0 + KT);
+    if (tI + 2 < ntiles) load_tile(t0 + 2 * KT, kr_issue, vr_issue);
 
     // S^T[key][row] for the wave's 32 rows, one independent chain per sub-tile.
     if (PA_SETPRIO) __builtin_amdgcn_s_setprio(1);
@@ -292,8 +302,16 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
         acc[dt] = mfma32(as_bf16x8(ld16(vb + 16)), pb1, acc[dt]);
       }
     }
-    if (more) store_tile(buf ^ 1);
+    if (tI + 1 < ntiles) store_tile(buf ^ 1, kr_store, vr_store);
     __syncthreads();
+  };
+  if (ntiles > 0) load_tile(kv0, krA, vrA);
+  if (ntiles > 1) load_tile(kv0 + KT, krB, vrB);
+  if (ntiles > 0) store_tile(0, krA, vrA);
+  __syncthreads();
+  for (int tI = 0; tI < ntiles; tI += 2) {
+    step(tI, krA, vrA, krB, vrB);
+    if (tI + 1 < ntiles) step(tI + 1, krB, vrB, krA, vrA);
   }
 
   l += wave_xor(l, 32);
@@ -490,7 +508,7 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
 // Separate instantiations keep a pure prefill or pure decode launch from
 // paying the other path's registers and LDS.
 template <int D, int MIX>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_bf16_kernel(AttnArgs a) {
   const int32_t* plan = a.plan;
   const int n_tile = plan[H_N_SHARED] + plan[H_N_TILE];  // workgroups before the row quads
   const int b = blockIdx.x;
