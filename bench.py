@@ -17,6 +17,7 @@ of the same launch, on this host's cores.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -40,6 +41,36 @@ DESCRIPTIONS = {
               "5 causal query tokens; 64/8 heads, d128, bf16 (Llama-3-70B attention shape)",
     "tiny": "tiny fp32: 4 requests, 128-token shared prefix, suffix U[32,64]; 8/2 heads, d64",
 }
+
+
+# HBM traffic of one attention call (attention kernel + split merge), from
+# rocprofv3 FETCH_SIZE / WRITE_SIZE counter runs scaled by the factors a plain
+# copy of known size gives; valid only for the kernel sources it was taken on.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+KERNEL_SOURCES = ["attn_bf16.hip", "attn_f32.hip", "device_common.h", "plan.cpp",
+                  "plan_format.h", "api.hip"]
+
+
+def kernel_fingerprint() -> str:
+    h = hashlib.sha256()
+    for s in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2605_11232_amd", "csrc", s), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(name: str):
+    """Counter-measured HBM bytes per call for this workload, or None when no
+    record exists or the kernels changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_sources_sha256") != kernel_fingerprint():
+        return None
+    w = rec.get("workloads", {}).get(name)
+    return None if w is None else float(w["traffic_bytes"])
 
 
 def cpu_baseline(wl, launch, budget_s: float = 12.0):
@@ -206,7 +237,8 @@ def main():
                    "attn_logical_bytes": logical_bytes, "append_bytes": app_bytes,
                    "parallelism": "single GPU"},
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "frac": round(achieved / peak, 4), "traffic": measured_traffic(name),
+                     "traffic_unit": "HBM bytes per call (counters)",
                      "kernel": "pa_attn_" + ("prefill" if name in ("prefill", "mixed", "tiny") else name),
                      "avg_launch_ms": round(attn_ms, 4),
                      "effective_logical_gbs": round(logical_bytes / (attn_ms * 1e-3) / 1e9, 1)},
