@@ -57,45 +57,65 @@ __device__ __forceinline__ int perm32(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
-// Keys per step of a tile item: NSUB sub-tiles of 32 keys (NSUB * 2 blocks).
-#ifndef PA_TILE_SUB
-#define PA_TILE_SUB 2
-#endif
-constexpr int kTileSub = PA_TILE_SUB;
-// Raise the wavefront's issue priority while it feeds the matrix cores, so the
-// SIMD's other wavefront does its softmax in the gaps (0 disables).
-#ifndef PA_SETPRIO
-#define PA_SETPRIO 0
-#endif
+// Tile items walk the keys in 64-key steps (four cache blocks).
+constexpr int kTileKeys = 64;
 
-template <int D, int NSUB>
+// LDS of a tile item: K and V^T of two steps, each step held as the cache's
+// own four blocks ([16 keys][D] for K, [D][16 keys] for V^T).  Blocks are
+// copied straight from global memory into LDS (no register staging); the
+// 16-byte units are XOR-swizzled so that the MFMA operand reads of 16
+// consecutive lanes fall in distinct banks:
+//  K:   key row r, column unit c (8 dims)  -> unit r * D/8 + (c ^ (r % (D/8)))
+//  V^T: dim row d, half h (8 keys)         -> unit 2 d + (h ^ vswz(d))
+// Row r of a step's K holds key 32 * (r / 32) + perm32(r % 32).
+template <int D>
 struct TileSmem {
-  static constexpr int KT = 32 * NSUB;
-  static constexpr int KS = D + 8;   // bf16 per K row (row stride an odd multiple of 16 B)
-  static constexpr int VS = KT + 8;  // bf16 per V^T row
-  __bf16 k[2][KT * KS];
-  __bf16 v[2][D * VS];
+  static constexpr int BLK = kBlock * D;  // bf16 per block of K or V^T
+  __bf16 k[2][4 * BLK];
+  __bf16 v[2][4 * BLK];
 };
+
+__device__ __forceinline__ int vswz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
+
+// s_waitcnt vmcnt(0): every global load of this wavefront, including the
+// copies into LDS, has completed.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Asynchronous copy of 16 bytes per lane from global memory into LDS: lane l
+// writes bytes [16 l, 16 l + 16) after `lds` (a wave-uniform address).
+__device__ __forceinline__ void copy16_to_lds(const char* src, __bf16* lds) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+// max of a value over the two lane halves (lane l and l ^ 32)
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
 
 // Tile item (SHARED = false): 128 rows of one sequence, causal.  Shared-prefix
 // item (SHARED = true): 128 gathered rows of a cascade group's members over
 // keys every one of them sees; results go to the members' partial rows.
-template <int D, int NSUB, bool SHARED>
-__device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB>& sm) {
-  using Sm = TileSmem<D, NSUB>;
-  constexpr int KT = Sm::KT;
-  constexpr int NB = KT / kBlock;          // blocks per step
-  constexpr int KCH = KT * D / 8 / 256;    // 16-byte K chunks per thread per step
-  constexpr int VCH = D * NB * 2 / 256;    // 16-byte V^T chunks per thread per step
-  // With D = 128 every chunk i of a thread lies in block i of the step, so
-  // its source address is a wave-uniform block base plus a fixed offset.
-  constexpr bool kChunkIsBlock = (KCH == NB) && (VCH == NB);
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, j = lane & 31, hh = lane >> 5;
+//
+// Software pipeline over steps, one workgroup barrier per step: while the
+// softmax of step t runs on the VALU, the score MFMAs of step t + 1 run on the
+// matrix cores, and the PV MFMAs of step t overlap the row maxima of step
+// t + 1.  K of step t + 2 and V^T of step t + 1 are copied into the LDS
+// buffers freed by steps t and t - 1 during step t.
+template <int D, bool SHARED>
+__device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm) {
+  constexpr int KT = kTileKeys;
+  constexpr int NB = KT / kBlock;   // blocks per step
+  constexpr int CU = D / 8;         // 16-byte units per K row
+  constexpr int NI = D / 32;        // LDS copies per wavefront per step, for each of K and V^T
+  constexpr int BLK = TileSmem<D>::BLK;
+  const int tid = threadIdx.x, lane = tid & 63, j = lane & 31, hh = lane >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;
   const int G = a.group;
   const int lr = w * 32 + j;
   const int g = it[I_KVH], row0 = it[I_ROW0], nrows = it[I_NROWS], kv0 = it[I_KV0];
   const bool valid = lr < nrows;
-  int key_seq, kend, qs, qi, hq, apos, wave_amin, part;
+  int key_seq, kend, qs, qi, hq, apos, wg_amin, part;
   if constexpr (SHARED) {
     // gathered row -> member sequence and its own row
     const int rpm = it[S_RPM];
@@ -110,7 +130,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     key_seq = it[S_BLOCK_SEQ];
     kend = it[S_KV1];
     apos = valid ? kend - 1 : -1;  // every shared key is visible
-    wave_amin = kend - 1;          // only a partial last step is masked
+    wg_amin = kend - 1;            // only a partial last step is masked
   } else {
     const int r = it[I_SEQ];
     const int L = a.seq_lens[r];
@@ -123,9 +143,9 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     key_seq = r;
     kend = min(it[I_KV1], L);
     apos = valid ? L - n + qi : -1;
-    // Rows are ordered by query, so the wave's first row has its smallest
-    // position: key sub-tiles entirely at or below it need no causal mask.
-    wave_amin = L - n + (row0 + w * 32) / G;
+    // Rows are ordered by query, so the item's first row has the smallest
+    // position: steps entirely at or below it need no causal mask.
+    wg_amin = L - n + row0 / G;
   }
 
   bf16x8 qf[D / 16];
@@ -141,177 +161,200 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     for (int e = 0; e < 16; ++e) acc[dt][e] = 0.f;
   // Running reference max m (raw scores) and this lane's partial row sum l
   // (the two lane halves hold disjoint keys of the same row; they are added
-  // at the end).  p = exp2(c * (s - m)) with c = scale * log2(e).
+  // at the end).  p = exp2(c * s - mc) with c = scale * log2(e), mc = c * m.
   const float c = a.scale_log2;
   float m = kNegInf, mc = 0.f, l = 0.f;
 
+  // Per-lane byte offsets of this wavefront's LDS copies inside a block: copy
+  // i fills LDS units 64 * (4 i + w) + lane of the step buffer.
+  uint32_t koff[NI], voff[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int U = 64 * (4 * i + w) + lane;
+    const int r = U / CU, cs = U % CU;
+    const int col = cs ^ (r % CU);
+    const int key = 32 * (r / 32) + perm32(r % 32);
+    koff[i] = (uint32_t)(((key % kBlock) * D + 8 * col) * 2);
+    const int u = U % (2 * D), d = u >> 1, h = (u & 1) ^ vswz(d);
+    voff[i] = (uint32_t)((d * kBlock + 8 * h) * 2);
+  }
   const int32_t* bt = a.bt + (int64_t)key_seq * a.max_blocks;
-  const __bf16* kbase = a.kc + (int64_t)g * kBlock * D;  // head g inside block 0
-  const __bf16* vbase = a.vc + (int64_t)g * D * kBlock;
-  const int64_t blk_k = (int64_t)a.hkv * kBlock * D;
-  const int64_t blk_v = (int64_t)a.hkv * D * kBlock;
+  const char* kbase = reinterpret_cast<const char*>(a.kc + (int64_t)g * kBlock * D);
+  const char* vbase = reinterpret_cast<const char*>(a.vc + (int64_t)g * D * kBlock);
+  const int64_t blk_bytes = (int64_t)a.hkv * kBlock * D * 2;  // one block, all kv-heads
 
-  // Per-thread chunk geometry (fixed for the whole item).  With D = 128 chunk
-  // i of a thread is block i of the step at the same in-block offset, so one
-  // base offset and a compile-time stride describe all of a thread's chunks
-  // (fewer live registers); otherwise each chunk keeps its own.
-  constexpr int GK = kChunkIsBlock ? 1 : KCH, GV = kChunkIsBlock ? 1 : VCH;
-  int k_off[GK], k_row[GK], k_blk[GK], v_off[GV], v_lds[GV], v_blk[GV], v_key[GV];
-#pragma unroll
-  for (int i = 0; i < GK; ++i) {
-    const int c8 = tid + 256 * i;
-    const int kk = c8 / (D / 8), part8 = c8 % (D / 8);
-    k_blk[i] = kk / kBlock;
-    k_off[i] = (kk % kBlock) * D + part8 * 8;
-    k_row[i] = ((kk & ~31) + perm32(kk & 31)) * Sm::KS + part8 * 8;
-  }
-#pragma unroll
-  for (int i = 0; i < GV; ++i) {
-    const int c8 = tid + 256 * i;
-    const int b = c8 / (2 * D), d = (c8 % (2 * D)) >> 1, half = c8 & 1;
-    v_blk[i] = b;
-    v_off[i] = d * kBlock + 8 * half;
-    v_lds[i] = d * Sm::VS + 16 * b + 8 * half;
-    v_key[i] = 16 * b + 8 * half;
-  }
-  // chunk i's entries: the stored one, or chunk 0's plus the fixed stride
-  auto K_OFF = [&](int i) { return kChunkIsBlock ? k_off[0] : k_off[i]; };
-  auto K_ROW = [&](int i) { return kChunkIsBlock ? k_row[0] + 16 * i * Sm::KS : k_row[i]; };
-  auto V_OFF = [&](int i) { return kChunkIsBlock ? v_off[0] : v_off[i]; };
-  auto V_LDS = [&](int i) { return kChunkIsBlock ? v_lds[0] + 16 * i : v_lds[i]; };
-  auto V_KEY = [&](int i) { return kChunkIsBlock ? v_key[0] + 16 * i : v_key[i]; };
-
-  // Gather one KT-key step (NB blocks, ids read once per step) into
-  // registers.  Every load is in bounds: blocks past kend alias the step's
-  // first block; values of keys at or past kend are zeroed (never-written
-  // slots may hold anything), keys there are masked in the scores.
+  // Block ids of a step (wave-uniform).  Blocks at or past kend alias the
+  // step's first block, so every copy reads inside the cache; their keys are
+  // masked and their values zeroed before use.
   BlockWindow win;
   win.init(bt, a.max_blocks, kv0 / kBlock);
-  auto load_tile = [&](int t0, u32x4 (&kr)[KCH], u32x4 (&vr)[VCH]) {
+  auto step_blocks = [&](int t0, int (&blk)[NB]) {
     const int jb = t0 / kBlock;
-    int blk[NB];
+    blk[0] = clamp_block(win.get(jb), a.num_blocks);
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
-      blk[b] = (b == 0 || t0 + kBlock * b < kend) ? clamp_block(win.get(jb + b), a.num_blocks)
-                                                   : blk[0];
+    for (int b = 1; b < NB; ++b)
+      blk[b] = t0 + kBlock * b < kend ? clamp_block(win.get(jb + b), a.num_blocks) : blk[0];
+  };
+  // Copy slot i of wavefront w lands in block (4 i + w) * 64 / (2 D) of the
+  // step: block i for D = 128, block 2 i + w / 2 for D = 64.
+  static_assert(D == 64 || D == 128, "head_dim 64 or 128");
+  auto copy_block = [&](const int (&blk)[NB], int i) {
+    if constexpr (D == 128) return blk[i];
+    else return blk[2 * i] + ((w >> 1) & 1) * (blk[2 * i + 1] - blk[2 * i]);  // no indexed array
+  };
+  auto issue_k = [&](const int (&blk)[NB], int buf) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      int bsel = blk[0];
-      if constexpr (kChunkIsBlock) {
-        bsel = blk[i];
-      } else {
-#pragma unroll
-        for (int b = 1; b < NB; ++b) bsel = k_blk[i] == b ? blk[b] : bsel;
-      }
-      kr[i] = ld16(kbase + bsel * blk_k + K_OFF(i));
-    }
-    const bool tail = t0 + KT > kend;
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      int bsel = blk[0];
-      if constexpr (kChunkIsBlock) {
-        bsel = blk[i];
-      } else {
-#pragma unroll
-        for (int b = 1; b < NB; ++b) bsel = v_blk[i] == b ? blk[b] : bsel;
-      }
-      u32x4 x = ld16(vbase + bsel * blk_v + V_OFF(i));
-      if (tail) x = keep_bf16(x, min(max(kend - (t0 + V_KEY(i)), 0), 8));
-      vr[i] = x;
+    for (int i = 0; i < NI; ++i) {
+      const char* src = kbase + (int64_t)copy_block(blk, i) * blk_bytes;
+      copy16_to_lds(src + koff[i], &sm.k[buf][512 * (4 * i + w)]);
     }
   };
-  auto store_tile = [&](int buf, const u32x4 (&kr)[KCH], const u32x4 (&vr)[VCH]) {
+  auto issue_v = [&](const int (&blk)[NB], int buf) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) st16(&sm.k[buf][K_ROW(i)], kr[i]);
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) st16(&sm.v[buf][V_LDS(i)], vr[i]);
+    for (int i = 0; i < NI; ++i) {
+      const char* src = vbase + (int64_t)copy_block(blk, i) * blk_bytes;
+      copy16_to_lds(src + voff[i], &sm.v[buf][512 * (4 * i + w)]);
+    }
   };
 
-  // Two register sets of staged K/V: the loads of step t + 2 are issued at the
-  // start of step t and written to LDS at the end of step t + 1, so each load
-  // has two steps of compute to arrive (L2 misses included).  LDS is double
-  // buffered: step t reads buffer t % 2 while step t + 1's data is stored into
-  // the other one.
-  u32x4 krA[KCH], vrA[VCH], krB[KCH], vrB[VCH];
-  const int ntiles = kend > kv0 ? (kend - kv0 + KT - 1) / KT : 0;
-  auto step = [&](int tI, u32x4 (&kr_issue)[KCH], u32x4 (&vr_issue)[VCH],
-                  const u32x4 (&kr_store)[KCH], const u32x4 (&vr_store)[VCH]) {
-    const int buf = tI & 1;
-    const int t0 = kv0 + KT * tI;
-    if (tI + 2 < ntiles) load_tile(t0 + 2 * KT, kr_issue, vr_issue);
-
-    // S^T[key][row] for the wave's 32 rows, one independent chain per sub-tile.
-    if (PA_SETPRIO) __builtin_amdgcn_s_setprio(1);
-    f32x16 s[NSUB];
+  // S^T[key][row] of a step for the wave's 32 rows: two independent 32-key chains.
+  auto scores = [&](int buf, f32x16 (&s)[2]) {
 #pragma unroll
-    for (int u = 0; u < NSUB; ++u)
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[u][e] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks)
 #pragma unroll
-      for (int u = 0; u < NSUB; ++u)
-        s[u] = mfma32(as_bf16x8(ld16(&sm.k[buf][(32 * u + j) * Sm::KS + 16 * ks + 8 * hh])), qf[ks],
-                      s[u]);
-
-    if (PA_SETPRIO) __builtin_amdgcn_s_setprio(0);
-    // Softmax and PV per 32-key sub-tile: the VALU work of sub-tile u only
-    // depends on its own score chain, so it overlaps the MFMAs still running
-    // for the next sub-tile (scores) or the previous one (PV).
-    const bool diag = t0 + KT - 1 > wave_amin;  // wave-uniform: diagonal / tail steps
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u) {
-      if (diag) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = t0 + 32 * u + perm32(8 * (e >> 2) + 4 * hh + (e & 3));
-          s[u][e] = key <= apos ? s[u][e] : kNegInf;
-        }
+      for (int u = 0; u < 2; ++u) {
+        const int r = 32 * u + j, col = 2 * ks + hh;
+        s[u] = mfma32(as_bf16x8(ld16(&sm.k[buf][8 * (r * CU + (col ^ (r % CU)))])), qf[ks], s[u]);
       }
-      float mx = fmaxf(s[u][0], s[u][1]);
+  };
+  auto mask = [&](int t0, f32x16 (&s)[2]) {
 #pragma unroll
-      for (int e = 2; e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[u][e]), s[u][e + 1]);
-      mx = fmaxf(mx, wave_xor(mx, 32));
-      // Move the reference max only when a score exceeds it by more than 2^8
-      // (probabilities stay <= 256, exact for float32 sums and bf16
-      // operands); decided for the whole wavefront so every lane skips the
-      // rescale together.
-      if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
-        const float mnew = fmaxf(m, mx);
-        const float mcn = mnew == kNegInf ? 0.f : mnew * c;
-        const float alpha = m == kNegInf ? 0.f : fast_exp2(mc - mcn);
-        l *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
-        m = mnew;
-        mc = mcn;
-      }
-      bf16x8 pb0, pb1;
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float p = fast_exp2(fmaf(s[u][e], c, -mc));
-        l += p;
-        if (e < 8) pb0[e] = (__bf16)p; else pb1[e - 8] = (__bf16)p;
+        const int key = t0 + 32 * u + perm32(8 * (e >> 2) + 4 * hh + (e & 3));
+        s[u][e] = key <= apos ? s[u][e] : kNegInf;
       }
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-        const __bf16* vb = &sm.v[buf][(32 * dt + j) * Sm::VS + 32 * u + 8 * hh];
-        acc[dt] = mfma32(as_bf16x8(ld16(vb)), pb0, acc[dt]);
-        acc[dt] = mfma32(as_bf16x8(ld16(vb + 16)), pb1, acc[dt]);
-      }
-    }
-    if (tI + 1 < ntiles) store_tile(buf ^ 1, kr_store, vr_store);
-    __syncthreads();
   };
-  if (ntiles > 0) load_tile(kv0, krA, vrA);
-  if (ntiles > 1) load_tile(kv0 + KT, krB, vrB);
-  if (ntiles > 0) store_tile(0, krA, vrA);
-  __syncthreads();
-  for (int tI = 0; tI < ntiles; tI += 2) {
-    step(tI, krA, vrA, krB, vrB);
-    if (tI + 1 < ntiles) step(tI + 1, krB, vrB, krA, vrA);
+  auto rowmax = [&](const f32x16 (&s)[2]) {
+    float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int e = (u == 0 ? 2 : 0); e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[u][e]), s[u][e + 1]);
+    return max_halves(mx);
+  };
+  // Move the reference max only when a score exceeds it by more than 2^8
+  // (probabilities stay <= 256, exact in float32 sums and bf16 operands);
+  // decided for the whole wavefront so every lane skips the rescale together.
+  auto rebase = [&](float mx) {
+    if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
+      const float mnew = fmaxf(m, mx);
+      const float mcn = mnew == kNegInf ? 0.f : mnew * c;
+      const float alpha = m == kNegInf ? 0.f : fast_exp2(mc - mcn);
+      l *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
+      m = mnew;
+      mc = mcn;
+    }
+  };
+  // Probabilities of a step as bf16 B operands: p[u][kk] holds keys
+  // 32 u + 16 kk + 8 hh + 0..7 (the perm32 order makes them consecutive).
+  auto probs = [&](const f32x16 (&s)[2], bf16x8 (&p)[2][2]) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float x = fast_exp2(fmaf(s[u][e], c, -mc));
+        l += x;
+        p[u][e >> 3][e & 7] = (__bf16)x;
+      }
+  };
+  auto pv = [&](int buf, const bf16x8 (&p)[2][2]) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) {
+          const int d = 32 * dt + j;
+          const __bf16* vb = &sm.v[buf][(2 * u + kk) * BLK + 8 * (2 * d + (hh ^ vswz(d)))];
+          acc[dt] = mfma32(as_bf16x8(ld16(vb)), p[u][kk], acc[dt]);
+        }
+  };
+  // Values of keys at or past kend in the last step: zero (never-written cache
+  // slots may hold anything, and 0 * NaN would reach the output).
+  auto zero_tail = [&](int t0, int buf) {
+    const int nz = t0 + KT - kend;
+    for (int x = tid; x < D * nz; x += 256) {
+      const int d = x % D, k = kend - t0 + x / D;
+      const int b = k / kBlock, kk = k % kBlock;
+      sm.v[buf][b * BLK + 8 * (2 * d + ((kk >> 3) ^ vswz(d))) + (kk & 7)] = (__bf16)0.f;
+    }
+  };
+
+  const int ntiles = kend > kv0 ? (kend - kv0 + KT - 1) / KT : 0;
+  // steps [0, n_plain) need no causal or tail mask for any row of the item
+  const int n_plain = min(ntiles, max(0, (wg_amin + 1 - kv0) / KT));
+  if (ntiles > 0) {
+    int bk[NB] = {}, bv[NB];
+    step_blocks(kv0, bv);
+    issue_k(bv, 0);
+    issue_v(bv, 0);
+    if (ntiles > 1) {
+      step_blocks(kv0 + KT, bv);
+      issue_k(bv, 1);
+    }
+    wait_vmem();
+    __syncthreads();
+    f32x16 s[2];
+    scores(0, s);
+    if (n_plain == 0) mask(kv0, s);
+    rebase(rowmax(s));
+    __syncthreads();  // K buffer 0 is refilled next
+
+    // One pipelined step: softmax + PV of step t, scores + max of step t + 1.
+    auto step = [&](int t, auto mask_next) {
+      const int t0 = kv0 + KT * t;
+      if (t + 2 < ntiles) {
+        step_blocks(t0 + 2 * KT, bk);
+        issue_k(bk, t & 1);
+      }
+      issue_v(bv, (t + 1) & 1);  // blocks of step t + 1, found one step earlier
+#pragma unroll
+      for (int b = 0; b < NB; ++b) bv[b] = bk[b];
+      bf16x8 p[2][2];
+      f32x16 sn[2];
+      probs(s, p);
+      scores((t + 1) & 1, sn);
+      pv(t & 1, p);
+      if constexpr (decltype(mask_next)::value) mask(t0 + KT, sn);
+      const float mx = rowmax(sn);
+      wait_vmem();
+      __syncthreads();
+      rebase(mx);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) s[u] = sn[u];
+    };
+    int t = 0;
+    for (; t + 1 < min(n_plain, ntiles); ++t) step(t, std::false_type{});
+    for (; t + 1 < ntiles; ++t) step(t, std::true_type{});
+    // last step: softmax + PV only
+    const int t0 = kv0 + KT * t;
+    bf16x8 p[2][2];
+    probs(s, p);
+    if (t0 + KT > kend) {
+      zero_tail(t0, t & 1);
+      __syncthreads();
+    }
+    pv(t & 1, p);
   }
 
   l += wave_xor(l, 32);
@@ -513,14 +556,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   const int n_tile = plan[H_N_SHARED] + plan[H_N_TILE];  // workgroups before the row quads
   const int b = blockIdx.x;
   if constexpr (MIX & 1) {
-    __shared__ TileSmem<D, kTileSub> sm;
+    __shared__ TileSmem<D> sm;
     const int n_shared = plan[H_N_SHARED];
     if (b < n_shared) {
-      tile_item<D, kTileSub, true>(plan + plan[H_SHARED_OFF] + b * kSharedWords, a, sm);
+      tile_item<D, true>(plan + plan[H_SHARED_OFF] + b * kSharedWords, a, sm);
       return;
     }
     if (b < n_tile) {
-      tile_item<D, kTileSub, false>(plan + plan[H_TILE_OFF] + (b - n_shared) * kItemWords, a, sm);
+      tile_item<D, false>(plan + plan[H_TILE_OFF] + (b - n_shared) * kItemWords, a, sm);
       return;
     }
   }
