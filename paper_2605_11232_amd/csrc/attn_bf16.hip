@@ -267,15 +267,18 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   };
   // Probabilities of a step as bf16 B operands: p[u][kk] holds keys
   // 32 u + 16 kk + 8 hh + 0..7 (the perm32 order makes them consecutive).
+  // Row sums in four short chains.
   auto probs = [&](const f32x16 (&s)[2], bf16x8 (&p)[2][2]) {
+    float ls[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const float x = fast_exp2(fmaf(s[u][e], c, -mc));
-        l += x;
+        ls[e & 3] += x;
         p[u][e >> 3][e & 7] = (__bf16)x;
       }
+    l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
   };
   auto pv = [&](int buf, const bf16x8 (&p)[2][2]) {
 #pragma unroll
@@ -334,6 +337,9 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
       f32x16 sn[2];
       probs(s, p);
       scores((t + 1) & 1, sn);
+      // keep the row-sum additions in this region, where they overlap the
+      // score MFMAs, instead of letting them sink past the barrier
+      asm volatile("" : "+v"(l));
       pv(t & 1, p);
       if constexpr (decltype(mask_next)::value) mask(t0 + KT, sn);
       const float mx = rowmax(sn);
