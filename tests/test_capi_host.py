@@ -169,6 +169,9 @@ def test_workload_tables_bit_exact(name):
 # plan layout (plan_format.h): header words, record sizes
 H_N_SHARED, H_N_TILE, H_N_ROW, H_N_GROUPS, H_GRID = 2, 3, 4, 5, 6
 H_SHARED_OFF, H_TILE_OFF, H_ROW_OFF, H_GROUP_OFF, H_MEMBER_OFF, H_PARTIAL_ROWS = 12, 13, 14, 15, 16, 17
+WAVES = 4                 # wavefronts per workgroup: row items come WAVES to a workgroup
+TILE_ROWS = 32 * WAVES    # rows of a tile or shared item (32 per wavefront)
+ROW_ITEM_ROWS = 16
 
 
 def parse_plan(plan):
@@ -184,7 +187,7 @@ def check_plan(plan, info, L, cu, G, hkv, D=128):
     and whose partial rows are exactly those of its merge group."""
     h, shared, tiles, rows, groups = parse_plan(plan)
     assert h[0] == 0x31304150 and h[H_GRID] == info.grid
-    assert info.grid == h[H_N_SHARED] + h[H_N_TILE] + h[H_N_ROW] // 4
+    assert info.grid == h[H_N_SHARED] + h[H_N_TILE] + h[H_N_ROW] // WAVES
     n = len(L)
     q = np.diff(cu)
     cover = {}      # (seq, kvh, rho) -> list of (kv0, kv1, partial row or -1)
@@ -193,6 +196,9 @@ def check_plan(plan, info, L, cu, G, hkv, D=128):
         cover.setdefault(key, []).append((kv0, kv1, pr))
         if pr >= 0:
             writes[pr] = writes.get(pr, 0) + 1
+    assert h[H_N_ROW] % WAVES == 0
+    assert all(0 < t[3] <= TILE_ROWS for t in tiles) and all(0 < t[3] <= TILE_ROWS for t in shared)
+    assert all(t[3] <= ROW_ITEM_ROWS for t in rows if t[0] >= 0)
     for seq, kvh, row0, nrows, kv0, kv1, part, _ in tiles + rows:
         if seq < 0:
             continue
