@@ -172,8 +172,14 @@ def main():
     stagings = [Staging("cuda", n, wl.max_blocks_per_seq, T, plan_words) for _ in range(2)]
     stream = torch.cuda.current_stream()
 
+    kv_memory = {}
+
     def step(s, record=None):
         p = dev.prepare_staged(launches[s], stagings[s % 2], q, k_new, v_new, out, lse)
+        if s == 0 and record is None:
+            # KV memory of the live batch: blocks versus contiguous reservations
+            # of the block-table capacity (outside the timed steps)
+            kv_memory.update(dev.pool.kv_waste(wl.max_blocks_per_seq * cfg.block_size))
         dev.append(p)
         if record is not None:
             record[0].record(stream)
@@ -236,6 +242,7 @@ def main():
                    "attn_flops": flops, "attn_unique_bytes": attn_bytes,
                    "attn_logical_bytes": logical_bytes, "append_bytes": app_bytes,
                    "parallelism": "single GPU"},
+        "kv_memory": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in kv_memory.items()},
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                      "frac": round(achieved / peak, 4), "traffic": measured_traffic(name),
                      "traffic_unit": "HBM bytes per call (counters)",

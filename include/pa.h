@@ -110,10 +110,54 @@ int pa_seq_extend(pa_pool* pool, int64_t seq_id, const int32_t* tokens, int32_t 
 int pa_seq_truncate(pa_pool* pool, int64_t seq_id, int32_t new_len);
 
 /* Release a finished sequence.  Its full blocks are cached first (same rule as
- * at admission); cached blocks stay resident with no owner (no eviction);
- * uncached blocks return to the back of the free list.
+ * at admission); cached blocks stay resident with no owner (idle) until
+ * evicted; uncached blocks return to the back of the free list.
  * Errors: PA_ERR_UNKNOWN_SEQ. */
 int pa_seq_free(pa_pool* pool, int64_t seq_id);
+
+/* Least-recently-used eviction of idle cached blocks (paper: Section 2, APC
+ * keeps reusable prefix blocks resident; Section 5.3, a prefix identical
+ * across many requests stays hot).  Off by default: an admission or extension
+ * needing more blocks than the free list holds then fails with
+ * PA_ERR_NO_BLOCKS.  On: the free list is used first, then idle cached blocks
+ * (held by no live sequence) are evicted one at a time, always a block that
+ * no other cached block continues, the one released longest ago first
+ * (blocks released by one pa_seq_free count as released last block first).
+ * An evicted block leaves the prefix cache and goes to the request; a later
+ * request with that prefix recomputes it.  The failure check counts idle
+ * blocks, so a failing request still leaves the pool unchanged. */
+int pa_pool_set_eviction(pa_pool* pool, int32_t enabled);
+
+/* Occupancy counters of a pool. */
+typedef struct {
+  int64_t num_blocks;
+  int64_t free_blocks;        /* on the free list */
+  int64_t cached_blocks;      /* in the prefix cache, held or idle */
+  int64_t idle_cached_blocks; /* cached and held by no live sequence */
+  int64_t evictions;          /* cached blocks evicted since creation */
+  int64_t live_seqs;
+  int64_t live_tokens;        /* sum of live sequence lengths */
+  int64_t logical_blocks;     /* sum of live block-table lengths */
+  int64_t physical_blocks;    /* distinct blocks held by live sequences */
+} pa_pool_stats;
+int pa_pool_get_stats(const pa_pool* pool, pa_pool_stats* out);
+
+/* KV memory accounting of the live sequences (paper: Section 2, paged KV
+ * memory against contiguous per-request reservations, Table "playbook"):
+ * slots allocated in blocks versus reserving max_seq_len contiguous slots per
+ * request.  Paged waste per sequence is below block_size / length; shared
+ * prefix blocks count once in physical_slots.  Errors: PA_ERR_ARG when
+ * max_seq_len is below the longest live sequence. */
+typedef struct {
+  int64_t tokens;           /* sum of live sequence lengths */
+  int64_t paged_slots;      /* block_size x sum of block-table lengths */
+  int64_t physical_slots;   /* block_size x distinct blocks held */
+  int64_t contiguous_slots; /* live sequences x max_seq_len */
+  double paged_waste;       /* 1 - tokens / paged_slots (0 with no sequences) */
+  double contiguous_waste;  /* 1 - tokens / contiguous_slots */
+  double sharing_factor;    /* paged_slots / physical_slots (1 with no sequences) */
+} pa_kv_waste;
+int pa_pool_kv_waste(const pa_pool* pool, int32_t max_seq_len, pa_kv_waste* out);
 
 /* Batched forms for a serving step: n operations applied in order, exactly as
  * n calls of the single-sequence function would (sequence i owns tokens
@@ -170,6 +214,30 @@ int pa_build_metadata(const pa_pool* pool, int32_t n_seqs, const int64_t* seq_id
                       const int32_t* q_lens, int32_t max_blocks_per_seq, int32_t* block_table,
                       int32_t* seq_lens, int32_t* cu_seqlens_q, int32_t* slot_mapping,
                       int64_t slot_capacity);
+
+/* Adapter-first, length-bucketed batch forming (paper: Section 6,
+ * "Multi-Adapter and Length-Aware Batching", and Table "casec_adapter"): item
+ * i is (adapter_ids[i], prompt_lens[i], i).  Items are grouped by adapter
+ * (groups in the order of their first item) and each group is split into
+ * length buckets by the strictly ascending upper bounds bucket_bounds[0 ..
+ * n_bounds): bucket k holds lengths below bucket_bounds[k] that no earlier
+ * bucket holds, bucket n_bounds the rest.  Every non-empty (adapter, bucket)
+ * is one batch; batches run adapter group by adapter group, short buckets
+ * first, items in original order inside a batch.  Outputs (host,
+ * caller-owned):
+ *   order[n]            original index of the item at execution position p
+ *   position[n]         execution position of original item i (restores the
+ *                       original order: result i = executed result position[i])
+ *   batch_offsets[n+1]  batch b is order[batch_offsets[b] .. batch_offsets[b+1])
+ *   batch_adapter[n]    adapter of batch b
+ *   batch_bucket[n]     length bucket of batch b (0 = shortest)
+ *   *n_batches          number of batches (<= n)
+ * Errors: PA_ERR_ARG (NULL or negative argument, negative length, bounds not
+ * strictly ascending). */
+int pa_form_batches(int32_t n, const int32_t* adapter_ids, const int32_t* prompt_lens,
+                    int32_t n_bounds, const int32_t* bucket_bounds, int32_t* order,
+                    int32_t* position, int32_t* batch_offsets, int32_t* batch_adapter,
+                    int32_t* batch_bucket, int32_t* n_batches);
 
 /* ------------------------------------------------------------------------ *
  * Launch plan (host).                                                        *

@@ -22,8 +22,14 @@ the design notes:
   blocks when it is released, each only if the block before it is registered
   and its prefix is not registered yet (the first registration wins; a
   duplicate stays private);
-* released blocks that are registered stay cached with refcount 0 (no eviction);
+* released blocks that are registered stay cached with refcount 0 (idle);
   unregistered ones return to the back of the free list;
+* with eviction enabled, an allocation that the free list cannot serve evicts
+  idle cached blocks one at a time: only trie leaves (no cached block
+  continues them), the least recently released first, where one release
+  stamps its newly idle blocks last block first; an evicted block leaves the
+  trie and goes straight to the request.  Without eviction such a request
+  fails.  Capacity is checked before anything changes;
 * truncation (rolling back draft or chunk tokens) may only drop unregistered
   blocks; they return to the *front* of the free list, so ``extend`` followed
   by ``truncate`` restores the pool exactly.
@@ -65,6 +71,11 @@ class PrefixCacheOracle:
         self.registered = set()  # physical blocks present in the trie
         self.ref = [0] * num_blocks
         self.seqs = {}           # seq_id -> {"tokens": list, "blocks": list, "n_reg": int}
+        self.evict = False
+        self.node = {}           # registered block -> (trie level holding it, its key)
+        self.stamp = {}          # idle registered block -> release stamp
+        self.clock = 0
+        self.evictions = 0
 
     # -- helpers -----------------------------------------------------------
     def _seq(self, seq_id):
@@ -91,9 +102,27 @@ class PrefixCacheOracle:
                 break
             level[key] = [blocks[j], {}]
             self.registered.add(blocks[j])
+            self.node[blocks[j]] = (level, key)
             level = level[key][1]
             j += 1
         st["n_reg"] = j
+
+    def _obtainable(self, held_idle=0):
+        return len(self.free) + (len(self.stamp) - held_idle if self.evict else 0)
+
+    def _take(self):
+        """Next block of an allocation: the free list's front, else evict the
+        least recently released idle trie leaf."""
+        if self.free:
+            return self.free.popleft()
+        leaves = [b for b in self.stamp if not self.node[b][0][self.node[b][1]][1]]
+        b = min(leaves, key=lambda x: self.stamp[x])
+        level, key = self.node.pop(b)
+        del level[key]
+        self.registered.discard(b)
+        del self.stamp[b]
+        self.evictions += 1
+        return b
 
     # -- operations ----------------------------------------------------------
     def add(self, seq_id, tokens) -> int:
@@ -113,11 +142,14 @@ class PrefixCacheOracle:
             hits.append(level[key][0])
             level = level[key][1]
         need = -(-L // bs) - len(hits)
-        if need > len(self.free):
-            raise NoBlocksError(f"need {need} blocks, {len(self.free)} free")
+        idle_hits = sum(1 for b in hits if self.ref[b] == 0)
+        if need > self._obtainable(idle_hits):
+            raise NoBlocksError(f"need {need} blocks, {self._obtainable(idle_hits)} obtainable")
         for b in hits:
+            if self.ref[b] == 0:
+                del self.stamp[b]
             self.ref[b] += 1
-        new = [self.free.popleft() for _ in range(need)]
+        new = [self._take() for _ in range(need)]
         for b in new:
             self.ref[b] = 1
         st = {"tokens": toks, "blocks": hits + new, "n_reg": len(hits)}
@@ -130,10 +162,10 @@ class PrefixCacheOracle:
         toks = [int(t) for t in tokens]
         newL = len(st["tokens"]) + len(toks)
         need = -(-newL // self.bs) - len(st["blocks"])
-        if need > len(self.free):
-            raise NoBlocksError(f"need {need} blocks, {len(self.free)} free")
+        if need > self._obtainable():
+            raise NoBlocksError(f"need {need} blocks, {self._obtainable()} obtainable")
         for _ in range(need):
-            b = self.free.popleft()
+            b = self._take()
             self.ref[b] = 1
             st["blocks"].append(b)
         st["tokens"].extend(toks)
@@ -160,6 +192,10 @@ class PrefixCacheOracle:
             self.ref[b] -= 1
             if self.ref[b] == 0 and b not in self.registered:
                 self.free.append(b)
+        for b in reversed(st["blocks"]):
+            if self.ref[b] == 0 and b in self.registered:
+                self.clock += 1
+                self.stamp[b] = self.clock
         del self.seqs[seq_id]
 
     def seq_len(self, seq_id) -> int:
@@ -197,6 +233,31 @@ class PrefixCacheOracle:
     # -- introspection used by invariant tests --------------------------------
     def free_list(self):
         return list(self.free)
+
+    def stats(self):
+        held = {b for st in self.seqs.values() for b in st["blocks"]}
+        return {"num_blocks": self.num_blocks, "free_blocks": len(self.free),
+                "cached_blocks": len(self.registered), "idle_cached_blocks": len(self.stamp),
+                "evictions": self.evictions, "live_seqs": len(self.seqs),
+                "live_tokens": sum(len(st["tokens"]) for st in self.seqs.values()),
+                "logical_blocks": sum(len(st["blocks"]) for st in self.seqs.values()),
+                "physical_blocks": len(held)}
+
+    def kv_waste(self, max_seq_len: int):
+        """Slots allocated in blocks versus a contiguous max-length reservation
+        per live sequence (Section 2, paged KV memory)."""
+        if any(len(st["tokens"]) > max_seq_len for st in self.seqs.values()):
+            raise ArgError("max_seq_len below the longest live sequence")
+        s = self.stats()
+        tokens = s["live_tokens"]
+        paged = s["logical_blocks"] * self.bs
+        phys = s["physical_blocks"] * self.bs
+        contig = s["live_seqs"] * max_seq_len
+        return {"tokens": tokens, "paged_slots": paged, "physical_slots": phys,
+                "contiguous_slots": contig,
+                "paged_waste": 1 - tokens / paged if paged else 0.0,
+                "contiguous_waste": 1 - tokens / contig if contig else 0.0,
+                "sharing_factor": paged / phys if phys else 1.0}
 
     def blocks_of(self, seq_id):
         return list(self._seq(seq_id)["blocks"])

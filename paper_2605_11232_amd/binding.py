@@ -27,7 +27,8 @@ EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy
            "pa_seq_extend", "pa_seq_truncate", "pa_seq_free", "pa_seqs_add", "pa_seqs_extend",
            "pa_seqs_truncate", "pa_seqs_free", "pa_pool_apply", "pa_seq_len", "pa_seq_blocks",
            "pa_pool_free_list", "pa_build_metadata", "pa_attn_plan", "pa_kv_append",
-           "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify"]
+           "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify", "pa_pool_set_eviction",
+           "pa_pool_get_stats", "pa_pool_kv_waste", "pa_form_batches"]
 
 
 class PaError(RuntimeError):
@@ -35,6 +36,18 @@ class PaError(RuntimeError):
         super().__init__(f"[{_CODES.get(rc, rc)}] {msg}")
         self.rc = rc
         self.code = _CODES.get(rc, str(rc))
+
+
+class PoolStats(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in ("num_blocks", "free_blocks", "cached_blocks",
+                                         "idle_cached_blocks", "evictions", "live_seqs",
+                                         "live_tokens", "logical_blocks", "physical_blocks")]
+
+
+class KvWaste(C.Structure):
+    _fields_ = [("tokens", C.c_int64), ("paged_slots", C.c_int64), ("physical_slots", C.c_int64),
+                ("contiguous_slots", C.c_int64), ("paged_waste", C.c_double),
+                ("contiguous_waste", C.c_double), ("sharing_factor", C.c_double)]
 
 
 class PlanInfo(C.Structure):
@@ -81,6 +94,11 @@ def lib():
         "pa_attn_plan": (C.c_int, [i32, i32, i32, _I32P, _I32P, _I32P, i32, i32, i32, i32, i32, i32,
                                    i32, _I32P, i64, C.POINTER(PlanInfo)]),
         "pa_kv_append": (C.c_int, [_P, _P, _P, i32, _P, _P, i32, i32, i32, i32, i32, _P]),
+        "pa_pool_set_eviction": (C.c_int, [_P, i32]),
+        "pa_pool_get_stats": (C.c_int, [_P, C.POINTER(PoolStats)]),
+        "pa_pool_kv_waste": (C.c_int, [_P, i32, C.POINTER(KvWaste)]),
+        "pa_form_batches": (C.c_int, [i32, _I32P, _I32P, i32, _I32P, _I32P, _I32P, _I32P, _I32P,
+                                      _I32P, _I32P]),
     }
     attn = (C.c_int, [_P, _P, _P, i32, _P, i32, _P, _P, i32, i32, i32, i32, i32, i32, f32, i32, _P,
                       C.POINTER(PlanInfo), _P, C.c_size_t, _P, _P, _P])
@@ -110,7 +128,7 @@ def _ptr(a: np.ndarray, ctype=C.c_int32):
 class Pool:
     """Host block manager (prefix-hit lookup, allocation, tables, slots)."""
 
-    def __init__(self, num_blocks: int, block_size: int, free_order):
+    def __init__(self, num_blocks: int, block_size: int, free_order, evict: bool = False):
         self._lib = lib()
         fo = _i32(free_order)
         h = _P()
@@ -118,6 +136,21 @@ class Pool:
                                         _ptr(fo) if fo.size else None, C.byref(h)))
         self._h = h
         self.num_blocks, self.block_size = int(num_blocks), int(block_size)
+        if evict:
+            self.set_eviction(True)
+
+    def set_eviction(self, enabled: bool):
+        _check(self._lib.pa_pool_set_eviction(self._h, int(bool(enabled))))
+
+    def stats(self) -> dict:
+        st = PoolStats()
+        _check(self._lib.pa_pool_get_stats(self._h, C.byref(st)))
+        return {n: int(getattr(st, n)) for n, _ in PoolStats._fields_}
+
+    def kv_waste(self, max_seq_len: int) -> dict:
+        w = KvWaste()
+        _check(self._lib.pa_pool_kv_waste(self._h, int(max_seq_len), C.byref(w)))
+        return {n: (float if t is C.c_double else int)(getattr(w, n)) for n, t in KvWaste._fields_}
 
     def close(self):
         if getattr(self, "_h", None):
@@ -220,6 +253,25 @@ class Pool:
             int(max_blocks_per_seq), _ptr(bt) if n else None, _ptr(sl) if n else None, _ptr(cu),
             _ptr(sm) if sm.size else None, sm.size))
         return out
+
+
+def form_batches(adapter_ids, prompt_lens, bucket_bounds):
+    """pa_form_batches: returns (order, position, batches) where batches is a
+    list of (adapter, bucket, original indices)."""
+    a, ln, bb = _i32(adapter_ids), _i32(prompt_lens), _i32(bucket_bounds)
+    n = a.size
+    if ln.size != n:
+        raise ValueError("adapter_ids and prompt_lens differ in length")
+    order, position = np.zeros(max(n, 1), np.int32), np.zeros(max(n, 1), np.int32)
+    offs = np.zeros(n + 1, np.int32)
+    badp, bbuck = np.zeros(max(n, 1), np.int32), np.zeros(max(n, 1), np.int32)
+    nb = C.c_int32(0)
+    _check(lib().pa_form_batches(n, _ptr(a) if n else None, _ptr(ln) if n else None, bb.size,
+                                 _ptr(bb) if bb.size else None, _ptr(order), _ptr(position),
+                                 _ptr(offs), _ptr(badp), _ptr(bbuck), C.byref(nb)))
+    batches = [(int(badp[b]), int(bbuck[b]), order[offs[b]:offs[b + 1]].tolist())
+               for b in range(nb.value)]
+    return order[:n].tolist(), position[:n].tolist(), batches
 
 
 def plan(kind: int, n_q: int, seq_lens, cu_seqlens_q, num_q_heads: int, num_kv_heads: int,

@@ -13,10 +13,19 @@
 // addressing, linear probing): every hit is confirmed by comparing the
 // predecessor id and the stored tokens, so hash collisions cannot produce a
 // false hit.
+//
+// Eviction (optional, least recently used): a cached block that no live
+// sequence holds is idle.  Because a sequence holds every block of its own
+// chain, the blocks continuing an idle block are idle too, so idle blocks
+// without cached successors (leaves) can always be evicted first; each
+// release stamps the blocks that became idle, tail first, and the leaf with
+// the oldest stamp goes first.  An evicted block leaves the index before its
+// id is reused, so (predecessor, tokens) keys never refer to stale content.
 #include <algorithm>
 #include <cstring>
 #include <deque>
 #include <new>
+#include <set>
 #include <unordered_map>
 #include <vector>
 
@@ -36,6 +45,14 @@ struct pa_pool {
   std::vector<uint64_t> slot_hash;
   std::vector<int32_t> slot_block;
   uint64_t slot_mask = 0;
+
+  // eviction state
+  bool evict = false;
+  std::vector<int32_t> n_succ;     // cached blocks whose predecessor is this block
+  std::vector<uint64_t> stamp;     // release stamp of an idle cached block
+  uint64_t clock = 0;
+  int64_t n_cached = 0, n_idle = 0, n_evicted = 0;
+  std::set<std::pair<uint64_t, int32_t>> leaves;  // idle cached blocks without successors
 
   struct Seq {
     std::vector<int32_t> tokens;
@@ -81,6 +98,64 @@ struct pa_pool {
     slot_block[i] = b;
   }
 
+  // Remove cached block b from the index (backward-shift deletion keeps every
+  // remaining key reachable from its home slot without tombstones).
+  void erase(int32_t b) {
+    const uint64_t h = key_hash(pred[b], &content[static_cast<size_t>(b) * bs]);
+    uint64_t i = h & slot_mask;
+    while (!(slot_hash[i] == h && slot_block[i] == b)) i = (i + 1) & slot_mask;
+    for (uint64_t j = (i + 1) & slot_mask; slot_hash[j] != 0; j = (j + 1) & slot_mask) {
+      const uint64_t home = slot_hash[j] & slot_mask;
+      const bool movable = i <= j ? (home <= i || home > j) : (home <= i && home > j);
+      if (movable) {
+        slot_hash[i] = slot_hash[j];
+        slot_block[i] = slot_block[j];
+        i = j;
+      }
+    }
+    slot_hash[i] = 0;
+    slot_block[i] = -1;
+  }
+
+  // A cached block's holder count went 1 -> 0 (idle) or 0 -> 1 (reused).
+  void make_idle(int32_t b) {
+    stamp[b] = ++clock;
+    ++n_idle;
+    if (n_succ[b] == 0) leaves.insert({stamp[b], b});
+  }
+  void reuse(int32_t b) {
+    --n_idle;
+    leaves.erase({stamp[b], b});
+  }
+
+  // Blocks an allocation can obtain: the free list, plus idle cached blocks
+  // other than `held_idle` ones about to be reused when eviction is on.
+  int64_t obtainable(int64_t held_idle) const {
+    return static_cast<int64_t>(free_list.size()) + (evict ? n_idle - held_idle : 0);
+  }
+
+  // Next block for an allocation: the free list's front, else the least
+  // recently released idle leaf (callers check obtainable() first).
+  int32_t take() {
+    if (!free_list.empty()) {
+      const int32_t b = free_list.front();
+      free_list.pop_front();
+      return b;
+    }
+    const auto it = leaves.begin();
+    const int32_t b = it->second;
+    leaves.erase(it);
+    erase(b);
+    cached[b] = 0;
+    --n_cached;
+    --n_idle;
+    ++n_evicted;
+    const int32_t p = pred[b];
+    pred[b] = -1;
+    if (p >= 0 && --n_succ[p] == 0 && cached[p] && ref[p] == 0) leaves.insert({stamp[p], p});
+    return b;
+  }
+
   // Cache the sequence's full blocks after its cached run, in logical order,
   // while the chain is unbroken and each prefix is new.
   void cache_run(Seq& s) {
@@ -92,7 +167,9 @@ struct pa_pool {
       if (find(p, t) >= 0) break;
       const int32_t b = s.blocks[j];
       cached[b] = 1;
+      ++n_cached;
       pred[b] = p;
+      if (p >= 0) ++n_succ[p];
       std::memcpy(&content[static_cast<size_t>(b) * bs], t, sizeof(int32_t) * bs);
       insert(key_hash(p, t), b);
       ++j;
@@ -130,6 +207,8 @@ int pa_pool_create(int32_t num_blocks, int32_t block_size, const int32_t* free_o
   p->cached.assign(num_blocks, 0);
   p->pred.assign(num_blocks, -1);
   p->content.assign(static_cast<size_t>(num_blocks) * block_size, 0);
+  p->n_succ.assign(num_blocks, 0);
+  p->stamp.assign(num_blocks, 0);
   uint64_t cap = 16;
   while (cap < 2 * static_cast<uint64_t>(num_blocks)) cap <<= 1;
   p->slot_hash.assign(cap, 0);
@@ -158,17 +237,19 @@ int pa_seq_add(pa_pool* pool, int64_t seq_id, const int32_t* tokens, int32_t n_t
     prev = b;
   }
   const int64_t need = pa_pool::cdiv(n_tokens, bs) - static_cast<int64_t>(hits.size());
-  if (need > static_cast<int64_t>(pool->free_list.size()))
-    return pa::fail(PA_ERR_NO_BLOCKS, "pa_seq_add: need %lld blocks, %zu free", (long long)need,
-                    pool->free_list.size());
+  int64_t idle_hits = 0;
+  for (int32_t b : hits) idle_hits += pool->ref[b] == 0;
+  if (need > pool->obtainable(idle_hits))
+    return pa::fail(PA_ERR_NO_BLOCKS, "pa_seq_add: need %lld blocks, %lld obtainable",
+                    (long long)need, (long long)pool->obtainable(idle_hits));
   pa_pool::Seq s;
   s.tokens.assign(tokens, tokens + n_tokens);
   s.blocks = hits;
   s.n_cached_run = static_cast<int32_t>(hits.size());
-  for (int32_t b : hits) ++pool->ref[b];
+  for (int32_t b : hits)
+    if (pool->ref[b]++ == 0) pool->reuse(b);
   for (int64_t i = 0; i < need; ++i) {
-    const int32_t b = pool->free_list.front();
-    pool->free_list.pop_front();
+    const int32_t b = pool->take();
     pool->ref[b] = 1;
     s.blocks.push_back(b);
   }
@@ -190,12 +271,11 @@ int pa_seq_extend(pa_pool* pool, int64_t seq_id, const int32_t* tokens, int32_t 
   if (new_len >= (int64_t{1} << 31))
     return pa::fail(PA_ERR_ARG, "pa_seq_extend: sequence length overflows int32");
   const int64_t need = pa_pool::cdiv(new_len, pool->bs) - static_cast<int64_t>(s.blocks.size());
-  if (need > static_cast<int64_t>(pool->free_list.size()))
-    return pa::fail(PA_ERR_NO_BLOCKS, "pa_seq_extend: need %lld blocks, %zu free", (long long)need,
-                    pool->free_list.size());
+  if (need > pool->obtainable(0))
+    return pa::fail(PA_ERR_NO_BLOCKS, "pa_seq_extend: need %lld blocks, %lld obtainable",
+                    (long long)need, (long long)pool->obtainable(0));
   for (int64_t i = 0; i < need; ++i) {
-    const int32_t b = pool->free_list.front();
-    pool->free_list.pop_front();
+    const int32_t b = pool->take();
     pool->ref[b] = 1;
     s.blocks.push_back(b);
   }
@@ -236,6 +316,11 @@ int pa_seq_free(pa_pool* pool, int64_t seq_id) {
   pool->cache_run(s);
   for (int32_t b : s.blocks) {
     if (--pool->ref[b] == 0 && !pool->cached[b]) pool->free_list.push_back(b);
+  }
+  // blocks that became idle are stamped tail first
+  for (size_t j = s.blocks.size(); j-- > 0;) {
+    const int32_t b = s.blocks[j];
+    if (pool->ref[b] == 0 && pool->cached[b]) pool->make_idle(b);
   }
   pool->seqs.erase(it);
   return PA_OK;
@@ -350,6 +435,57 @@ int pa_seq_blocks(const pa_pool* pool, int64_t seq_id, int32_t* out, int32_t cap
   if (static_cast<int64_t>(b.size()) > capacity)
     return pa::fail(PA_ERR_ARG, "pa_seq_blocks: capacity %d < %zu", capacity, b.size());
   std::copy(b.begin(), b.end(), out);
+  return PA_OK;
+}
+
+int pa_pool_set_eviction(pa_pool* pool, int32_t enabled) {
+  pa::clear_error();
+  if (!pool) return pa::fail(PA_ERR_ARG, "pa_pool_set_eviction: NULL pool");
+  pool->evict = enabled != 0;
+  return PA_OK;
+}
+
+int pa_pool_get_stats(const pa_pool* pool, pa_pool_stats* out) {
+  pa::clear_error();
+  if (!pool || !out) return pa::fail(PA_ERR_ARG, "pa_pool_get_stats: NULL argument");
+  pa_pool_stats st{};
+  st.num_blocks = pool->num_blocks;
+  st.free_blocks = static_cast<int64_t>(pool->free_list.size());
+  st.cached_blocks = pool->n_cached;
+  st.idle_cached_blocks = pool->n_idle;
+  st.evictions = pool->n_evicted;
+  st.live_seqs = static_cast<int64_t>(pool->seqs.size());
+  for (const auto& kv : pool->seqs) {
+    st.live_tokens += static_cast<int64_t>(kv.second.tokens.size());
+    st.logical_blocks += static_cast<int64_t>(kv.second.blocks.size());
+  }
+  for (int32_t b = 0; b < pool->num_blocks; ++b) st.physical_blocks += pool->ref[b] > 0;
+  *out = st;
+  return PA_OK;
+}
+
+int pa_pool_kv_waste(const pa_pool* pool, int32_t max_seq_len, pa_kv_waste* out) {
+  pa::clear_error();
+  if (!pool || !out) return pa::fail(PA_ERR_ARG, "pa_pool_kv_waste: NULL argument");
+  pa_pool_stats st;
+  int rc = pa_pool_get_stats(pool, &st);
+  if (rc) return rc;
+  int64_t longest = 0;
+  for (const auto& kv : pool->seqs)
+    longest = std::max<int64_t>(longest, static_cast<int64_t>(kv.second.tokens.size()));
+  if (max_seq_len < longest)
+    return pa::fail(PA_ERR_ARG, "pa_pool_kv_waste: max_seq_len %d below the longest live sequence %lld",
+                    max_seq_len, (long long)longest);
+  pa_kv_waste w{};
+  w.tokens = st.live_tokens;
+  w.paged_slots = st.logical_blocks * pool->bs;
+  w.physical_slots = st.physical_blocks * pool->bs;
+  w.contiguous_slots = st.live_seqs * static_cast<int64_t>(max_seq_len);
+  w.paged_waste = w.paged_slots ? 1.0 - double(w.tokens) / double(w.paged_slots) : 0.0;
+  w.contiguous_waste =
+      w.contiguous_slots ? 1.0 - double(w.tokens) / double(w.contiguous_slots) : 0.0;
+  w.sharing_factor = w.physical_slots ? double(w.paged_slots) / double(w.physical_slots) : 1.0;
+  *out = w;
   return PA_OK;
 }
 

@@ -58,9 +58,10 @@ def test_worked_example_library():
 class _Both:
     """Apply every operation to the oracle and the library and compare."""
 
-    def __init__(self, nb, bs, order):
+    def __init__(self, nb, bs, order, evict=False):
         self.o = PrefixCacheOracle(nb, bs, order)
-        self.l = B.Pool(nb, bs, order)
+        self.l = B.Pool(nb, bs, order, evict=evict)
+        self.o.evict = evict
 
     def do(self, name, *args):
         res = []
@@ -73,6 +74,7 @@ class _Both:
                 res.append(("error", e.code))
         assert res[0] == res[1], (name, args, res)
         assert self.o.free_list() == self.l.free_list()
+        assert self.o.stats() == self.l.stats()
         return res[0]
 
     def meta(self, ids, q_lens, mb):
@@ -85,10 +87,26 @@ class _Both:
 
 @pytest.mark.parametrize("seed", range(25))
 def test_random_operation_sequences_bit_exact(seed):
+    _random_operations(seed, evict=False)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_random_operation_sequences_with_eviction_bit_exact(seed):
+    """Small pools force least-recently-used evictions of idle cached blocks;
+    tables, free lists, hit counts and counters stay identical."""
+    both = _random_operations(seed, evict=True)
+    assert both.o.evictions == both.l.stats()["evictions"]
+
+
+def test_eviction_happens_in_random_sequences():
+    assert sum(_random_operations(s, evict=True).o.evictions for s in range(6)) > 0
+
+
+def _random_operations(seed, evict):
     r = np.random.default_rng(1000 + seed)
     bs = int(r.choice([2, 4, 16]))
-    nb = int(r.integers(8, 120))
-    both = _Both(nb, bs, r.permutation(nb).tolist())
+    nb = int(r.integers(8, 40 if evict else 120))
+    both = _Both(nb, bs, r.permutation(nb).tolist(), evict=evict)
     prefixes, reqs = _random_batch(seed, bs=bs, vocab=int(r.choice([2, 3, 50])))
     live = {}
     next_id = 0
@@ -126,6 +144,11 @@ def test_random_operation_sequences_bit_exact(seed):
             if live:
                 sid = next(iter(live))
                 both.do("add", sid, [1, 2, 3])
+        if step % 13 == 0 and live:
+            mx = max(both.o.seq_len(i) for i in live)
+            for m in (mx, mx + 7, mx - 1):
+                both.do("kv_waste", m)
+    return both
 
 
 @pytest.mark.parametrize("name", ["tiny", "prefill", "decode", "mixed", "verify"])
@@ -403,3 +426,61 @@ def test_pool_apply_matches_oracle_on_steps(name):
             else:
                 o.truncate(op.seq_id, op.n)
         assert o.free_list() == lp.free_list()
+
+
+# -- prefix-cache lifecycle and batch forming (library against the oracle) ----
+
+def _lib_evict_op(pool, st):
+    from tests.test_oracle_next import eviction_tokens
+    try:
+        if st["op"] == "add":
+            return pool.add(st["seq"], eviction_tokens(st["tokens"]))
+        if st["op"] == "free":
+            return pool.free(st["seq"])
+        if st["op"] == "kv_waste":
+            return pool.kv_waste(st["max_seq_len"])
+    except B.PaError as e:
+        return ("error", e.code)
+    raise ValueError(st["op"])
+
+
+def test_eviction_worked_example_library():
+    from tests.test_oracle_next import run_eviction_golden
+    run_eviction_golden(lambda nb, bs, order: B.Pool(nb, bs, order, evict=True), _lib_evict_op,
+                        lambda p: p.stats(), lambda p, s: p.blocks_of(s), lambda p: p.free_list())
+
+
+def test_eviction_off_by_default_fails_cleanly():
+    p = B.Pool(4, 4, [0, 1, 2, 3])
+    p.add(0, list(range(12)))
+    p.free(0)
+    with pytest.raises(B.PaError) as e:
+        p.add(1, list(range(100, 116)))
+    assert e.value.code == "no_blocks" and p.free_list() == [3]
+    p.set_eviction(True)
+    assert p.add(1, list(range(100, 116))) == 0
+    assert p.stats()["evictions"] == 3
+
+
+def test_batch_former_library_matches_oracle():
+    import json
+    from oracle.batching import form_batches
+    with open(os.path.join(os.path.dirname(__file__), "golden", "batch_former_example.json")) as f:
+        g = json.load(f)
+    order, position, batches = B.form_batches(g["adapter_ids"], g["prompt_lens"], g["bucket_bounds"])
+    assert [[a, k, idx] for a, k, idx in batches] == g["batches"]
+    assert order == g["order"] and position == g["position"]
+    r = np.random.default_rng(3)
+    for _ in range(200):
+        n = int(r.integers(0, 80))
+        ad = r.integers(-3, int(r.integers(1, 10)), size=n).tolist()
+        ln = r.integers(0, 6000, size=n).tolist()
+        bounds = sorted(set(r.integers(0, 6000, size=int(r.integers(0, 5))).tolist()))
+        assert B.form_batches(ad, ln, bounds) == form_batches(ad, ln, bounds)
+
+
+def test_batch_former_rejects_bad_arguments():
+    for ad, ln, bb in (([0], [1], [10, 10]), ([0], [-1], []), ([0, 1], [1, 2], [5, 3])):
+        with pytest.raises(B.PaError) as e:
+            B.form_batches(ad, ln, bb)
+        assert e.value.code == "arg"
