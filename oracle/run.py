@@ -19,6 +19,7 @@ class OracleReplay:
         cfg = wl.cfg
         self.wl = wl
         self.pool = PrefixCacheOracle(wl.num_blocks, cfg.block_size, wl.free_order)
+        self.pool.evict = wl.evict
         self.store_values = store_values
         if store_values:
             self.k_cache, self.v_cache = new_cache(wl.num_blocks, cfg.num_kv_heads,

@@ -77,7 +77,7 @@ class DeviceReplay:
         self.wl, self.cfg, self.device = wl, cfg, torch.device(device)
         self.tdtype = torch_dtype(cfg.dtype)
         self.dcode = B.PA_BF16 if cfg.dtype == "bf16" else B.PA_F32
-        self.pool = B.Pool(wl.num_blocks, cfg.block_size, wl.free_order)
+        self.pool = B.Pool(wl.num_blocks, cfg.block_size, wl.free_order, evict=wl.evict)
         shape_k = (wl.num_blocks, cfg.num_kv_heads, cfg.block_size, cfg.head_dim)
         shape_v = (wl.num_blocks, cfg.num_kv_heads, cfg.head_dim, cfg.block_size)
         # Uninitialised on purpose: the kernels must never read unwritten slots.

@@ -78,6 +78,10 @@ CONFIGS = {
     "verify": AttnConfig("verify", "bf16", 64, 8, 128, 16, 1005,
                          "32 requests, 16384 shared prefix + 4096 cached suffix, "
                          "5 query tokens (4 draft + 1)"),
+    "evict": AttnConfig("evict", "bf16", 8, 2, 128, 16, 1006,
+                        "two cached 64-token prefixes in a 12-block pool with eviction: "
+                        "requests on one prefix evict the other's tail, which a later "
+                        "request recomputes (cold miss)"),
 }
 CONFIG_NAMES = list(CONFIGS)
 
@@ -148,6 +152,7 @@ class Workload:
     step: Optional[Callable[[int], Launch]] = None
     max_blocks_per_seq: int = 0
     notes: dict = field(default_factory=dict)
+    evict: bool = False   # the pool evicts idle cached blocks when it runs out
 
 
 def _kv_values(cfg: AttnConfig, idx: tuple, n: int):
@@ -389,8 +394,35 @@ def _verify(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
                     {"prefix": P, "suffix": Sx, "n_q": NQ})
 
 
+def _evict(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
+    """Prefix-cache lifecycle: two 64-token prefixes are cached in a pool of 12
+    blocks (block size 16) with least-recently-used eviction.  Launch 0 admits
+    two 104-token requests on the second prefix; the second request finds one
+    free block and evicts the first prefix's last two blocks.  Launch 1 admits
+    a request on the first prefix: it reuses the two surviving blocks (32
+    tokens) and computes the other 72 tokens, the evicted 32 prefix tokens
+    included, with the prefill kernel.  The hit counts follow from the
+    eviction rules by hand (least recently released idle leaf first)."""
+    s, bs = cfg.seed, cfg.block_size
+    P, S = 64, 40
+    p1, p2 = tokens(s, TAG_PREFIX_TOK, (0,), P), tokens(s, TAG_PREFIX_TOK, (1,), P)
+    setup = _prefix_setup(cfg, [p1, p2])
+    suf = [tokens(s, TAG_SUFFIX_TOK, (r,), S) for r in range(3)]
+    k0, v0 = _kv_values(cfg, (2, 0), 2 * S)
+    l0 = Launch([Op("add", 0, _concat(p2, suf[0])), Op("add", 1, _concat(p2, suf[1]))], [0, 1],
+                [S, S], _q_values(cfg, (0,), 2 * S), k0, v0, [Op("free", 0), Op("free", 1)])
+    q1 = P + S - 32
+    k1, v1 = _kv_values(cfg, (2, 1), q1)
+    l1 = Launch([Op("add", 2, _concat(p1, suf[2]))], [2], [q1], _q_values(cfg, (1,), q1), k1, v1,
+                [Op("free", 2)])
+    nb = 12
+    free_order = rng(s, TAG_FREE).permutation(nb).astype(np.int32)
+    return Workload(cfg, nb, free_order, setup, [l0, l1], None, _cdiv(P + S, bs),
+                    {"prefix": P, "suffix": S, "expected_hits": [[P, P], [32]]}, evict=True)
+
+
 _BUILDERS = {"tiny": _tiny, "prefill": _prefill, "decode": _decode,
-             "mixed": _mixed, "verify": _verify}
+             "mixed": _mixed, "verify": _verify, "evict": _evict}
 
 
 def workload(name: str, scale: float = 1.0, steps: int = 1, **overrides) -> Workload:

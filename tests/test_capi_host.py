@@ -151,13 +151,14 @@ def _random_operations(seed, evict):
     return both
 
 
-@pytest.mark.parametrize("name", ["tiny", "prefill", "decode", "mixed", "verify"])
+@pytest.mark.parametrize("name", ["tiny", "prefill", "decode", "mixed", "verify", "evict"])
 def test_workload_tables_bit_exact(name):
     """Setup + first launch of every workload at full size: tables, slots and
     prefix hits agree exactly (values are not drawn; tables only)."""
     wl = synth.workload(name, steps=2)
     o = PrefixCacheOracle(wl.num_blocks, wl.cfg.block_size, wl.free_order)
-    l = B.Pool(wl.num_blocks, wl.cfg.block_size, wl.free_order)
+    o.evict = wl.evict
+    l = B.Pool(wl.num_blocks, wl.cfg.block_size, wl.free_order, evict=wl.evict)
 
     def apply(op):
         if op.kind == "write_kv":
@@ -175,8 +176,10 @@ def test_workload_tables_bit_exact(name):
     for op in wl.setup:
         apply(op)
     extra = [wl.step(1)] if wl.step and name != "tiny" else []
-    for launch in wl.launches[:2] + extra:
+    for li, launch in enumerate(wl.launches[:2] + extra):
         hits = [apply(op) for op in launch.pre]
+        if name == "evict":   # hand-derived from the eviction rules
+            assert hits == wl.notes["expected_hits"][li]
         mo = o.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
         ml = l.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
         for k in mo:
@@ -187,6 +190,9 @@ def test_workload_tables_bit_exact(name):
         for op in launch.post:
             apply(op)
         assert o.free_list() == l.free_list()
+        assert o.stats() == l.stats()
+    if name == "evict":
+        assert o.evictions == 5
 
 
 # plan layout (plan_format.h): header words, record sizes

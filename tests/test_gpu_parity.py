@@ -33,6 +33,17 @@ def test_tiny_in_bf16():
     run_parity(synth.workload("tiny", dtype="bf16"), label="tiny-bf16")
 
 
+def test_eviction_and_cold_miss_recompute():
+    """Least-recently-used eviction shortens a cached prefix; the next request
+    on it recomputes the evicted prefix tokens with the prefill kernel.  Hits,
+    tables, appended cache and outputs match the oracle."""
+    _gpu()
+    wl = synth.workload("evict")
+    errs, _, _ = run_parity(wl, label="evict")
+    say("evict normalized errors", errs)
+    assert len(errs) == 2
+
+
 @pytest.mark.parametrize("name,scale", [("prefill", 0.125), ("decode", 0.0625),
                                         ("mixed", 0.0625), ("verify", 0.125)])
 def test_reduced(name, scale):
