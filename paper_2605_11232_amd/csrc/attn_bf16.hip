@@ -57,22 +57,29 @@ __device__ __forceinline__ int perm32(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
-// Tile items walk the keys in 64-key steps (four cache blocks).
-constexpr int kTileKeys = 64;
+// Tile items walk the keys in steps of kTileSub 32-key sub-tiles (2 kTileSub
+// cache blocks).  Smaller steps halve the LDS and registers a workgroup holds,
+// so more workgroups share a CU.
+#ifndef PA_TILE_SUB
+#define PA_TILE_SUB 2
+#endif
+constexpr int kTileSub = PA_TILE_SUB;
+static_assert(kTileSub == 1 || kTileSub == 2, "32- or 64-key tile steps");
+constexpr int kTileWavesPerEu = kTileSub == 1 ? 3 : 2;
 
 // LDS of a tile item: K and V^T of two steps, each step held as the cache's
-// own four blocks ([16 keys][D] for K, [D][16 keys] for V^T).  Blocks are
+// own 2 NSUB blocks ([16 keys][D] for K, [D][16 keys] for V^T).  Blocks are
 // copied straight from global memory into LDS (no register staging); the
 // 16-byte units are XOR-swizzled so that the MFMA operand reads of 16
 // consecutive lanes fall in distinct banks:
 //  K:   key row r, column unit c (8 dims)  -> unit r * D/8 + (c ^ (r % (D/8)))
 //  V^T: dim row d, half h (8 keys)         -> unit 2 d + (h ^ vswz(d))
 // Row r of a step's K holds key 32 * (r / 32) + perm32(r % 32).
-template <int D>
+template <int D, int NSUB>
 struct TileSmem {
   static constexpr int BLK = kBlock * D;  // bf16 per block of K or V^T
-  __bf16 k[2][4 * BLK];
-  __bf16 v[2][4 * BLK];
+  __bf16 k[2][2 * NSUB * BLK];
+  __bf16 v[2][2 * NSUB * BLK];
 };
 
 __device__ __forceinline__ int vswz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
@@ -102,13 +109,13 @@ __device__ __forceinline__ float max_halves(float x) {
 // matrix cores, and the PV MFMAs of step t overlap the row maxima of step
 // t + 1.  K of step t + 2 and V^T of step t + 1 are copied into the LDS
 // buffers freed by steps t and t - 1 during step t.
-template <int D, bool SHARED>
-__device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm) {
-  constexpr int KT = kTileKeys;
+template <int D, int NSUB, bool SHARED>
+__device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB>& sm) {
+  constexpr int KT = 32 * NSUB;     // keys per step
   constexpr int NB = KT / kBlock;   // blocks per step
   constexpr int CU = D / 8;         // 16-byte units per K row
-  constexpr int NI = D / 32;        // LDS copies per wavefront per step, for each of K and V^T
-  constexpr int BLK = TileSmem<D>::BLK;
+  constexpr int NI = NSUB * D / 64; // LDS copies per wavefront per step, for each of K and V^T
+  constexpr int BLK = TileSmem<D, NSUB>::BLK;
   const int tid = threadIdx.x, lane = tid & 63, j = lane & 31, hh = lane >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;
   const int G = a.group;
@@ -197,6 +204,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   };
   // Copy slot i of wavefront w lands in block (4 i + w) * 64 / (2 D) of the
   // step: block i for D = 128, block 2 i + w / 2 for D = 64.
+  static_assert(NI >= 1, "at least one copy per wavefront");
   static_assert(D == 64 || D == 128, "head_dim 64 or 128");
   auto copy_block = [&](const int (&blk)[NB], int i) {
     if constexpr (D == 128) return blk[i];
@@ -217,33 +225,33 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
     }
   };
 
-  // S^T[key][row] of a step for the wave's 32 rows: two independent 32-key chains.
-  auto scores = [&](int buf, f32x16 (&s)[2]) {
+  // S^T[key][row] of a step for the wave's 32 rows: NSUB independent 32-key chains.
+  auto scores = [&](int buf, f32x16 (&s)[NSUB]) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < NSUB; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[u][e] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks)
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+      for (int u = 0; u < NSUB; ++u) {
         const int r = 32 * u + j, col = 2 * ks + hh;
         s[u] = mfma32(as_bf16x8(ld16(&sm.k[buf][8 * (r * CU + (col ^ (r % CU)))])), qf[ks], s[u]);
       }
   };
-  auto mask = [&](int t0, f32x16 (&s)[2]) {
+  auto mask = [&](int t0, f32x16 (&s)[NSUB]) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < NSUB; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int key = t0 + 32 * u + perm32(8 * (e >> 2) + 4 * hh + (e & 3));
         s[u][e] = key <= apos ? s[u][e] : kNegInf;
       }
   };
-  auto rowmax = [&](const f32x16 (&s)[2]) {
+  auto rowmax = [&](const f32x16 (&s)[NSUB]) {
     float mx = fmaxf(s[0][0], s[0][1]);
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < NSUB; ++u)
 #pragma unroll
       for (int e = (u == 0 ? 2 : 0); e < 16; e += 2) mx = fmaxf(fmaxf(mx, s[u][e]), s[u][e + 1]);
     return max_halves(mx);
@@ -268,10 +276,10 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
   // Probabilities of a step as bf16 B operands: p[u][kk] holds keys
   // 32 u + 16 kk + 8 hh + 0..7 (the perm32 order makes them consecutive).
   // Row sums in four short chains.
-  auto probs = [&](const f32x16 (&s)[2], bf16x8 (&p)[2][2]) {
+  auto probs = [&](const f32x16 (&s)[NSUB], bf16x8 (&p)[NSUB][2]) {
     float ls[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < NSUB; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const float x = fast_exp2(fmaf(s[u][e], c, -mc));
@@ -280,9 +288,9 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
       }
     l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
   };
-  auto pv = [&](int buf, const bf16x8 (&p)[2][2]) {
+  auto pv = [&](int buf, const bf16x8 (&p)[NSUB][2]) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int u = 0; u < NSUB; ++u)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
@@ -317,7 +325,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
     }
     wait_vmem();
     __syncthreads();
-    f32x16 s[2];
+    f32x16 s[NSUB];
     scores(0, s);
     if (n_plain == 0) mask(kv0, s);
     rebase(rowmax(s));
@@ -333,8 +341,8 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
       issue_v(bv, (t + 1) & 1);  // blocks of step t + 1, found one step earlier
 #pragma unroll
       for (int b = 0; b < NB; ++b) bv[b] = bk[b];
-      bf16x8 p[2][2];
-      f32x16 sn[2];
+      bf16x8 p[NSUB][2];
+      f32x16 sn[NSUB];
       probs(s, p);
       scores((t + 1) & 1, sn);
       // keep the row-sum additions in this region, where they overlap the
@@ -347,14 +355,14 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D>& sm)
       __syncthreads();
       rebase(mx);
 #pragma unroll
-      for (int u = 0; u < 2; ++u) s[u] = sn[u];
+      for (int u = 0; u < NSUB; ++u) s[u] = sn[u];
     };
     int t = 0;
     for (; t + 1 < min(n_plain, ntiles); ++t) step(t, std::false_type{});
     for (; t + 1 < ntiles; ++t) step(t, std::true_type{});
     // last step: softmax + PV only
     const int t0 = kv0 + KT * t;
-    bf16x8 p[2][2];
+    bf16x8 p[NSUB][2];
     probs(s, p);
     if (t0 + KT > kend) {
       zero_tail(t0, t & 1);
@@ -557,19 +565,19 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
 // Separate instantiations keep a pure prefill or pure decode launch from
 // paying the other path's registers and LDS.
 template <int D, int MIX>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kTileWavesPerEu))) void attn_bf16_kernel(AttnArgs a) {
   const int32_t* plan = a.plan;
   const int n_tile = plan[H_N_SHARED] + plan[H_N_TILE];  // workgroups before the row quads
   const int b = blockIdx.x;
   if constexpr (MIX & 1) {
-    __shared__ TileSmem<D> sm;
+    __shared__ TileSmem<D, kTileSub> sm;
     const int n_shared = plan[H_N_SHARED];
     if (b < n_shared) {
-      tile_item<D, true>(plan + plan[H_SHARED_OFF] + b * kSharedWords, a, sm);
+      tile_item<D, kTileSub, true>(plan + plan[H_SHARED_OFF] + b * kSharedWords, a, sm);
       return;
     }
     if (b < n_tile) {
-      tile_item<D, false>(plan + plan[H_TILE_OFF] + (b - n_shared) * kItemWords, a, sm);
+      tile_item<D, kTileSub, false>(plan + plan[H_TILE_OFF] + (b - n_shared) * kItemWords, a, sm);
       return;
     }
   }
