@@ -109,7 +109,7 @@ __device__ __forceinline__ float max_halves(float x) {
 // matrix cores, and the PV MFMAs of step t overlap the row maxima of step
 // t + 1.  K of step t + 2 and V^T of step t + 1 are copied into the LDS
 // buffers freed by steps t and t - 1 during step t.
-template <int D, int NSUB, bool SHARED>
+template <int D, int NSUB, bool SHARED, bool FULL>
 __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB>& sm) {
   constexpr int KT = 32 * NSUB;     // keys per step
   constexpr int NB = KT / kBlock;   // blocks per step
@@ -325,10 +325,15 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     }
     wait_vmem();
     __syncthreads();
+    // Wavefronts without rows (items of fewer than kTileRows rows) only help
+    // with the copies and pass the barriers.
+    const bool active = FULL || w * 32 < nrows;
     f32x16 s[NSUB];
-    scores(0, s);
-    if (n_plain == 0) mask(kv0, s);
-    rebase(rowmax(s));
+    if (active) {
+      scores(0, s);
+      if (n_plain == 0) mask(kv0, s);
+      rebase(rowmax(s));
+    }
     __syncthreads();  // K buffer 0 is refilled next
 
     // One pipelined step: softmax + PV of step t, scores + max of step t + 1.
@@ -357,18 +362,34 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
 #pragma unroll
       for (int u = 0; u < NSUB; ++u) s[u] = sn[u];
     };
+    auto idle_step = [&](int t) {
+      const int t0 = kv0 + KT * t;
+      if (t + 2 < ntiles) {
+        step_blocks(t0 + 2 * KT, bk);
+        issue_k(bk, t & 1);
+      }
+      issue_v(bv, (t + 1) & 1);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) bv[b] = bk[b];
+      wait_vmem();
+      __syncthreads();
+    };
     int t = 0;
-    for (; t + 1 < min(n_plain, ntiles); ++t) step(t, std::false_type{});
-    for (; t + 1 < ntiles; ++t) step(t, std::true_type{});
+    if (active) {
+      for (; t + 1 < min(n_plain, ntiles); ++t) step(t, std::false_type{});
+      for (; t + 1 < ntiles; ++t) step(t, std::true_type{});
+    } else {
+      for (; t + 1 < ntiles; ++t) idle_step(t);
+    }
     // last step: softmax + PV only
     const int t0 = kv0 + KT * t;
     bf16x8 p[NSUB][2];
-    probs(s, p);
+    if (active) probs(s, p);
     if (t0 + KT > kend) {
       zero_tail(t0, t & 1);
       __syncthreads();
     }
-    pv(t & 1, p);
+    if (active) pv(t & 1, p);
   }
 
   l += wave_xor(l, 32);
@@ -573,11 +594,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kTileWavesP
     __shared__ TileSmem<D, kTileSub> sm;
     const int n_shared = plan[H_N_SHARED];
     if (b < n_shared) {
-      tile_item<D, kTileSub, true>(plan + plan[H_SHARED_OFF] + b * kSharedWords, a, sm);
+      const int32_t* it = plan + plan[H_SHARED_OFF] + b * kSharedWords;
+      if (it[S_NROWS] > kTileRows - 32) tile_item<D, kTileSub, true, true>(it, a, sm);
+      else tile_item<D, kTileSub, true, false>(it, a, sm);
       return;
     }
     if (b < n_tile) {
-      tile_item<D, kTileSub, false>(plan + plan[H_TILE_OFF] + (b - n_shared) * kItemWords, a, sm);
+      const int32_t* it = plan + plan[H_TILE_OFF] + (b - n_shared) * kItemWords;
+      // every wavefront has rows: the plain path; otherwise idle ones skip compute
+      if (it[I_NROWS] > kTileRows - 32) tile_item<D, kTileSub, false, true>(it, a, sm);
+      else tile_item<D, kTileSub, false, false>(it, a, sm);
       return;
     }
   }

@@ -157,7 +157,12 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
 
   if (dtype == PA_BF16) {
     auto qlen = [&](int32_t r) { return cu_seqlens_q[r + 1] - cu_seqlens_q[r]; };
+    // Sequences with few rows (decode, verification) get split key ranges and
+    // may join a cascade group; their private keys run on single-wave row
+    // items when a 16-row MFMA tile holds all their rows, else on tile items
+    // (the keys are then streamed once for all rows instead of once per 16).
     auto is_row = [&](int32_t r) { return qlen(r) > 0 && qlen(r) * G <= pa::kRowSeqRows; };
+    auto on_tiles = [&](int32_t r) { return qlen(r) * G > pa::kRowItemRows; };
 
     // Cascade groups: single-wave sequences with the same first block and
     // q_len whose leading blocks coincide share those keys; attention over
@@ -211,7 +216,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     // never below 256 keys per item.
     int64_t row_keys = 0;
     for (int32_t r = 0; r < n_seqs; ++r)
-      if (is_row(r))
+      if (is_row(r) && !on_tiles(r))
         row_keys += int64_t(seq_lens[r] - kstart[r]) * num_kv_heads *
                     cdiv(qlen(r) * G, pa::kRowItemRows);
     const int64_t target_waves = int64_t(num_cus) * 16;
@@ -227,7 +232,9 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       int64_t nt = 0, nr = 0;
       for (int32_t r = 0; r < n_seqs; ++r) {
         if (qlen(r) == 0) continue;
-        if (is_row(r))
+        if (is_row(r) && on_tiles(r))
+          nt += cdiv(seq_lens[r] - kstart[r], pa::kPrivateTileKeys);
+        else if (is_row(r))
           nr += cdiv(qlen(r) * G, pa::kRowItemRows) *
                 std::max<int64_t>(1, cdiv(seq_lens[r] - kstart[r], chunk));
         else
@@ -247,9 +254,12 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       const int32_t rows = n * G;
       if (is_row(r)) {
         const int32_t k0s = kstart[r];
-        const int32_t nsplit = static_cast<int32_t>(std::max<int64_t>(1, cdiv(L - k0s, chunk)));
+        const bool tiled = on_tiles(r);
+        const int64_t split = tiled ? pa::kPrivateTileKeys : chunk;
+        const int64_t step = tiled ? pa::kTileStep : pa::kKeyStep;
+        const int32_t nsplit = static_cast<int32_t>(std::max<int64_t>(1, cdiv(L - k0s, split)));
         // equal private key ranges, multiples of the key step, covering [k0s, L)
-        const int64_t per = cdiv(cdiv(L - k0s, nsplit), pa::kKeyStep) * pa::kKeyStep;
+        const int64_t per = cdiv(cdiv(L - k0s, nsplit), step) * step;
         int32_t used = 0;
         while (used < nsplit && k0s + int64_t(used) * per < L) ++used;
         // parts 0 .. first-1 are the shared prefix's key chunks
@@ -268,9 +278,15 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
             }
             if (first) member_base[size_t(r) * num_kv_heads + g] = int32_t(base);
           }
-          // per split, the row groups back to back
+          // per split, the row groups back to back (or one tile item with all rows)
           for (int32_t sp = 0; sp < used; ++sp) {
             const int64_t k0 = k0s + sp * per, k1 = std::min<int64_t>(L, k0s + (sp + 1) * per);
+            if (tiled) {
+              const int32_t part = base < 0 ? -1 : int32_t(base + int64_t(sp + first) * rows);
+              head_tiles[g].push_back({r, g, 0, rows, int32_t(k0), int32_t(k1), part, 0});
+              tile_cost[g].push_back((k1 - k0) * rows);
+              continue;
+            }
             for (int32_t gi = 0; gi < ngroups; ++gi) {
               const int32_t row0 = gi * pa::kRowItemRows;
               const int32_t nr = std::min(pa::kRowItemRows, rows - row0);

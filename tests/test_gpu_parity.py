@@ -231,9 +231,10 @@ def test_edge_cases():
         torch.cuda.synchronize()
         if sum(ql):
             close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"edge{ci}")
-    # verify with n_q = 8: G = 8 gives 64 rows per sequence (four 16-row
-    # items over the same keys); G = 16 gives 128 rows (one tile item)
-    for G, want_tiles in ((8, False), (16, True)):
+    # verify with n_q = 8: G = 2 gives 16 rows per sequence (single-wave row
+    # items); G = 8 gives 64 rows (tile items with split private key ranges,
+    # two of the four wavefronts idle); G = 16 gives 128 rows (one tile item)
+    for G, want_tiles in ((2, False), (8, True), (16, True)):
         cfg8 = synth.AttnConfig(f"edge-g{G}", "bf16", 2 * G, 2, 128, 16, 78)
         setup, launch = mk([8, 8], [40, 517], 9, cfg=cfg8)
         wl = synth.Workload(cfg8, 128, np.arange(128, dtype=np.int32), setup, [launch], None, 40)
@@ -243,6 +244,7 @@ def test_edge_cases():
         p = dv.run(wl.launches[0])
         torch.cuda.synchronize()
         assert (p.info.n_tile_items > 0) == want_tiles
+        assert (p.info.n_row_items > 0) == (not want_tiles)
         close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"verify-G{G}")
 
 
