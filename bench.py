@@ -52,10 +52,16 @@ KERNEL_SOURCES = ["attn_bf16.hip", "attn_f32.hip", "device_common.h", "plan.cpp"
 
 
 def kernel_fingerprint() -> str:
+    """sha256 of the kernel and planner sources without comments and blank
+    lines (a comment edit does not change the kernels)."""
+    import re
     h = hashlib.sha256()
     for s in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2605_11232_amd", "csrc", s), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2605_11232_amd", "csrc", s)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update("\n".join(ln.rstrip() for ln in text.splitlines() if ln.strip()).encode())
     return h.hexdigest()
 
 

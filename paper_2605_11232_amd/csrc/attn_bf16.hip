@@ -14,10 +14,9 @@
 //    in each lane, so the online-softmax row max / sum needs a single
 //    cross-lane exchange, and the probabilities are already laid out as the
 //    B operand of the PV product (no LDS round trip for P).
-//  * row items, one wavefront each: <= 16 rows (decode's G rows; verification's
-//    n_q * G rows as several items over the same keys) on 16x16x32 MFMA with K
-//    and V^T streamed straight from HBM into registers over a split of the key
-//    range.
+//  * row items, one wavefront each: <= 16 rows (decode's G rows) on 16x16x32
+//    MFMA with K and V^T streamed straight from HBM into registers over a
+//    split of the key range.
 //
 // The key order inside a tile is permuted so that each lane's eight PV
 // k-elements are eight consecutive keys: then V^T operands are single 16-byte
@@ -426,8 +425,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
 }
 
 // Row item: one wavefront, up to 16 rows (one 16-column MFMA tile), keys
-// [kv0, kv1).  Rows beyond 16 (verification: n_q * G) are separate items over
-// the same keys, placed next to each other so their loads meet in cache.
+// [kv0, kv1).  Sequences with more rows use tile items instead.
 template <int D>
 __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   constexpr int KS = D / 32;  // k-steps of the QK product (32 dims each)
