@@ -6,14 +6,17 @@
 // keys 0..a of its sequence, where a is the query's logical position, keys
 // and values gathered block by block through the block table.
 //
-// Two item kinds run in one launch (see plan.cpp):
-//  * tile items, one workgroup of 4 wavefronts x 32 rows: a 32-key tile of K
-//    and V^T is gathered from the paged cache into LDS (double buffered) and
-//    shared by the four wavefronts; S^T = K Q^T and O^T += V^T P^T run on
+// Item kinds of one launch (see plan.cpp):
+//  * tile items, one workgroup of 4 wavefronts x 32 rows: 64-key steps of K
+//    and V^T are copied from the paged cache straight into LDS (two stages)
+//    and shared by the four wavefronts; S^T = K Q^T and O^T += V^T P^T run on
 //    32x32x16 MFMA.  Computing the transposed score tile puts one query row
-//    in each lane, so the online-softmax row max / sum needs a single
-//    cross-lane exchange, and the probabilities are already laid out as the
-//    B operand of the PV product (no LDS round trip for P).
+//    in each lane, so the online-softmax row max needs a single cross-lane
+//    exchange, and the probabilities are already laid out as the B operand
+//    of the PV product (no LDS round trip for P).  Tile items also carry the
+//    private keys of few-row sequences with more than 16 rows (verification).
+//  * shared-prefix items: the tile path over gathered rows of sequences whose
+//    leading blocks coincide (cascade); partial results are merged.
 //  * row items, one wavefront each: <= 16 rows (decode's G rows) on 16x16x32
 //    MFMA with K and V^T streamed straight from HBM into registers over a
 //    split of the key range.
