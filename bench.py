@@ -125,6 +125,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="run only this many steps without the CPU baseline (profiling)")
+    ap.add_argument("--cold-steps", type=int, default=5,
+                    help="extra steps, after the timed ones, whose attention call runs after a "
+                         "1 GiB device read has flushed the caches (0 skips them)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, 5 times "
                          "(calibrates the HBM byte counters against a known transfer)")
@@ -151,12 +154,13 @@ def main():
     torch.cuda.set_device(0)
     name = args.workload
     W, K = args.warmup, args.steps
+    C = 0 if args.profile_steps else max(0, args.cold_steps)
     if args.profile_steps:
         W, K = 1, args.profile_steps
-    wl = synth.workload(name, steps=W + K + 2)
+    wl = synth.workload(name, steps=W + K + C + 2)
     cfg = wl.cfg
     dev = DeviceReplay(wl).setup()
-    launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K)]
+    launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K + C)]
     # pack each step's token batches (input marshalling) before timing
     from paper_2605_11232_amd.runtime import batch_ops
     for ln in launches:
@@ -180,6 +184,9 @@ def main():
 
     kv_memory = {}
 
+    scrub = None
+    scrub_sink = []
+
     def step(s, record=None):
         p = dev.prepare_staged(launches[s], stagings[s % 2], q, k_new, v_new, out, lse)
         if s == 0 and record is None:
@@ -187,6 +194,10 @@ def main():
             # of the block-table capacity (outside the timed steps)
             kv_memory.update(dev.pool.kv_waste(wl.max_blocks_per_seq * cfg.block_size))
         dev.append(p)
+        if scrub is not None:
+            # read 1 GiB: L2 and MALL then hold none of the inputs (a read leaves
+            # no dirty lines whose write-back would compete with the call)
+            scrub_sink.append(scrub.sum())
         if record is not None:
             record[0].record(stream)
         dev.attend(p)
@@ -208,7 +219,19 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     meta = {k: np.array(v, copy=True) for k, v in p.meta.items()}
-    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
+    per_ms = [a.elapsed_time(b) for a, b in events]
+    attn_ms = float(np.mean(per_ms))
+    cold_ms = None
+    if C:
+        # cold caches: the same call after a 1 GiB read, outside the timed steps
+        scrub = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
+        cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(C)]
+        for i in range(C):
+            step(W + K + i, cev[i])
+        torch.cuda.synchronize()
+        cold_ms = float(np.mean([a.elapsed_time(b) for a, b in cev]))
+        scrub = None
 
     flops = perf.attention_flops(meta["seq_lens"], meta["cu_seqlens_q"], cfg.num_q_heads,
                                  cfg.head_dim)
@@ -254,8 +277,19 @@ def main():
                      "traffic_unit": "HBM bytes per call (counters)",
                      "kernel": "pa_attn_" + ("prefill" if name in ("prefill", "mixed", "tiny") else name),
                      "avg_launch_ms": round(attn_ms, 4),
+                     "launch_ms_median": round(float(np.median(per_ms)), 4),
+                     "launch_ms_min": round(float(np.min(per_ms)), 4),
+                     "launch_ms_max": round(float(np.max(per_ms)), 4),
                      "effective_logical_gbs": round(logical_bytes / (attn_ms * 1e-3) / 1e9, 1)},
     }
+    if cold_ms is not None:
+        cold_ach = (flops if unit == "TFLOP/s" else attn_bytes) / (cold_ms * 1e-3) / (
+            1e12 if unit == "TFLOP/s" else 1e9)
+        rec["cold_caches"] = {"steps": C, "avg_launch_ms": round(cold_ms, 4),
+                              "achieved": round(cold_ach, 2), "unit": unit,
+                              "frac": round(cold_ach / peak, 4),
+                              "note": "attention call after a 1 GiB device read (L2 and MALL "
+                                      "flushed); not part of value or roofline"}
     if not args.no_cpu_baseline and not args.profile_steps:
         dt, done, cflops, threads, sub = cpu_baseline(synth.workload(name, steps=2), L0)
         if compute_bound or cfg.dtype == "f32":
