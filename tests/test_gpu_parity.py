@@ -269,3 +269,65 @@ def test_shared_prefix_cascade_matches_per_sequence(name, scale):
         outs.append((p.out.float().cpu().numpy(), p.lse.cpu().numpy()))
     close(outs[0][0], outs[1][0], *TOL["bf16"], f"{name} cascade vs per-sequence")
     close(outs[0][1], outs[1][1], 2e-3, 1e-4, f"{name} lse cascade vs per-sequence")
+
+
+def _random_workload(seed):
+    """A random small launch: random heads, group size and head_dim; one or
+    two cached prefixes (whole blocks) shared by some sequences; a launch
+    kind of suffix prefill, decode, verification or a mix of prefill and
+    decode sequences."""
+    r = np.random.default_rng(9000 + seed)
+    hkv = int(r.choice([1, 2, 4, 8]))
+    G = int(r.choice([1, 2, 4, 7, 8, 16]))
+    D = int(r.choice([64, 128]))
+    cfg = synth.AttnConfig(f"fuzz{seed}", "bf16", hkv * G, hkv, D, 16, 5000 + seed)
+    Val = synth.Values
+    bs = 16
+    prefixes = [r.integers(0, 1 << 17, size=16 * int(r.integers(1, 40))).astype(np.int32)
+                for _ in range(int(r.integers(1, 3)))]
+    setup = []
+    for pi, pt in enumerate(prefixes):
+        sid = synth.PREFIX_SEQ_BASE + pi
+        setup += [synth.Op("add", sid, pt),
+                  synth.Op("write_kv", sid, k=Val((cfg.seed, 15, 100 + pi), (len(pt), hkv, D), "bf16"),
+                           v=Val((cfg.seed, 16, 100 + pi), (len(pt), hkv, D), "bf16")),
+                  synth.Op("free", sid)]
+    kind = ["prefill", "decode", "verify", "mixed"][seed % 4]
+    n = int(r.integers(1, 9))
+    n_q = int(r.integers(2, 9))
+    pre, q_lens = [], []
+    for i in range(n):
+        pt = prefixes[int(r.integers(0, len(prefixes)))] if r.random() < 0.8 else np.zeros(0, np.int32)
+        body = r.integers(0, 1 << 17, size=int(r.integers(1, 400))).astype(np.int32)
+        toks = np.concatenate([pt, body])
+        sk = kind if kind != "mixed" else ("prefill" if r.random() < 0.5 else "decode")
+        if sk == "prefill":
+            pre.append(synth.Op("add", i, toks))
+            q_lens.append(len(body))
+        else:
+            q = 1 if sk == "decode" else n_q
+            # context in the cache (prefix hits, body written), then q new tokens
+            setup.append(synth.Op("add", i, toks))
+            setup.append(synth.Op("write_kv", i, k=Val((cfg.seed, 15, i), (len(body), hkv, D), "bf16"),
+                                  v=Val((cfg.seed, 16, i), (len(body), hkv, D), "bf16")))
+            pre.append(synth.Op("extend", i, r.integers(0, 1 << 17, size=q).astype(np.int32)))
+            q_lens.append(q)
+    T = sum(q_lens)
+    launch = synth.Launch(pre, list(range(n)), q_lens, Val((cfg.seed, 4), (T, hkv * G, D), "bf16"),
+                          Val((cfg.seed, 5), (T, hkv, D), "bf16"), Val((cfg.seed, 6), (T, hkv, D), "bf16"))
+    nb = 4096
+    max_len = max(len(p) for p in prefixes) + 400 + 16
+    return synth.Workload(cfg, nb, np.random.default_rng(seed).permutation(nb).astype(np.int32),
+                          setup, [launch], None, -(-max_len // bs))
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_launches(seed):
+    """Random shapes and launch kinds through the whole path (tables, cache,
+    outputs, LSE against the oracle)."""
+    _gpu()
+    wl = _random_workload(seed)
+    c = wl.cfg
+    say(f"[fuzz] seed {seed}: Hq {c.num_q_heads} Hkv {c.num_kv_heads} D {c.head_dim} "
+        f"q_lens {wl.launches[0].q_lens}")
+    run_parity(wl, label=f"fuzz{seed}")
