@@ -153,7 +153,12 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   std::vector<int32_t> members;  // cascade member tables, (sequence, partial base) pairs
   int64_t partial_rows = 0;
   std::vector<Rec> shared, tiles;
-  std::vector<std::array<Rec, 4>> quads;
+  // Row-item workgroups in dispatch order, as (kv-head, index of the group's
+  // first item in that head's longest-first order); records are written once,
+  // straight into the plan.
+  std::vector<std::pair<int32_t, int32_t>> quads;
+  std::vector<std::vector<Rec>> head_rows;
+  std::vector<std::vector<int32_t>> head_order;
 
   if (dtype == PA_BF16) {
     auto qlen = [&](int32_t r) { return cu_seqlens_q[r + 1] - cu_seqlens_q[r]; };
@@ -223,7 +228,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     int64_t chunk = std::max<int64_t>(256, cdiv(row_keys, std::max<int64_t>(1, target_waves)));
     chunk = cdiv(chunk, pa::kKeyStep) * pa::kKeyStep;
 
-    std::vector<std::vector<Rec>> head_tiles(num_kv_heads), head_rows(num_kv_heads);
+    std::vector<std::vector<Rec>> head_tiles(num_kv_heads);
+    head_rows.assign(num_kv_heads, {});
     std::vector<std::vector<int64_t>> tile_cost(num_kv_heads), row_cost(num_kv_heads);
     // partial base of (cascade group member, kv-head): member_base[r * Hkv + g]
     std::vector<int32_t> member_base(cg_members.empty() ? 0 : size_t(n_seqs) * num_kv_heads, -1);
@@ -246,6 +252,10 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         head_rows[g].reserve(nr);
         row_cost[g].reserve(nr);
       }
+      int64_t ng = 0;  // merge groups, at most one per 16 rows of a few-row sequence
+      for (int32_t r = 0; r < n_seqs; ++r)
+        if (is_row(r)) ng += cdiv(qlen(r) * G, pa::kRowItemRows);
+      groups.reserve(size_t(ng) * num_kv_heads);
     }
     for (int32_t r = 0; r < n_seqs; ++r) {
       const int32_t n = qlen(r);
@@ -359,17 +369,14 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     tiles = deal(head_tiles, tile_cost);
     // Row items: per head, longest first, four to a workgroup (padded with
     // empty items) so a workgroup's waves share one kv-head.
-    std::vector<std::vector<std::array<Rec, 4>>> quad_q(kXcds);
-    const Rec empty = {-1, 0, 0, 0, 0, 0, -1, 0};
+    std::vector<std::vector<std::pair<int32_t, int32_t>>> quad_q(kXcds);
+    head_order.resize(num_kv_heads);
     for (int32_t g = 0; g < num_kv_heads; ++g) {
       const auto xs = xcds_of_head(g, num_kv_heads);
-      const auto ord = order_longest_first(row_cost[g]);
-      size_t quad = 0;
-      for (size_t i = 0; i < ord.size(); i += 4, ++quad) {
-        std::array<Rec, 4> qd;
-        for (size_t k = 0; k < 4; ++k) qd[k] = i + k < ord.size() ? head_rows[g][ord[i + k]] : empty;
-        quad_q[xs[quad % xs.size()]].push_back(qd);
-      }
+      head_order[g] = order_longest_first(row_cost[g]);
+      const int32_t nq = int32_t(cdiv(int64_t(head_order[g].size()), 4));
+      for (auto x : xs) quad_q[x].reserve(quad_q[x].size() + size_t(nq) / xs.size() + 1);
+      for (int32_t q = 0; q < nq; ++q) quad_q[xs[q % xs.size()]].push_back({g, 4 * q});
     }
     quads = interleave(quad_q);
   }
@@ -430,8 +437,15 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     p = std::copy(w.begin(), w.end(), p);
   }
   for (auto& it : tiles) p = std::copy(it.begin(), it.end(), p);
-  for (auto& q : quads)
-    for (auto& it : q) p = std::copy(it.begin(), it.end(), p);
+  const Rec empty = {-1, 0, 0, 0, 0, 0, -1, 0};
+  for (const auto& q : quads) {
+    const auto& ord = head_order[q.first];
+    for (int32_t k = 0; k < 4; ++k) {
+      const size_t i = size_t(q.second) + k;
+      const Rec& it = i < ord.size() ? head_rows[q.first][ord[i]] : empty;
+      p = std::copy(it.begin(), it.end(), p);
+    }
+  }
   for (auto& g : groups) p = std::copy(g.begin(), g.end(), p);
   std::copy(members.begin(), members.end(), p);
   return PA_OK;
