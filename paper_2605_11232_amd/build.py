@@ -44,7 +44,7 @@ def _run(cmd):
 
 def build(verbose: bool = False, jobs: int = 8, defines=(), out_path: str = LIB_PATH) -> str:
     """Compile every source and link libpa.so at ``out_path``; ``defines``
-    are extra -D options for the HIP sources (kernel tuning knobs)."""
+    are extra -D options for all sources (kernel and planner tuning knobs)."""
     tmp = tempfile.mkdtemp(prefix="pa_build_")
     try:
         cmds = []
@@ -56,7 +56,8 @@ def build(verbose: bool = False, jobs: int = 8, defines=(), out_path: str = LIB_
             objs.append(o)
         for s in HOST_SOURCES:
             o = os.path.join(tmp, s + ".o")
-            cmds.append([CXX, *COMMON, "-c", os.path.join(CSRC, s), "-o", o])
+            cmds.append([CXX, *COMMON, *[f"-D{d}" for d in defines], "-c",
+                         os.path.join(CSRC, s), "-o", o])
             objs.append(o)
         with ThreadPoolExecutor(max_workers=jobs) as ex:
             outs = list(ex.map(_run, cmds))

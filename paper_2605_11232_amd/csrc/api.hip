@@ -11,7 +11,7 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
                      const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
                      const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
                      const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
-                     int64_t partial_rows, void* ws, void* out, float* lse,
+                     bool wide_rows, int64_t partial_rows, void* ws, void* out, float* lse,
                      hipStream_t stream);
 int launch_attn_f32(const void* q, const void* kc, const void* vc, int32_t num_blocks,
                     const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
@@ -71,7 +71,7 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
                               head_dim, scale, out, lse, st);
   } else {
     if (!plan) return fail(PA_ERR_ARG, "%s: NULL plan", fn);
-    if (info->variant != 1 || info->grid < 0 || info->n_groups < 0 ||
+    if ((info->variant & ~kVariantWideRows) != kVariantBf16 || info->grid < 0 || info->n_groups < 0 ||
         info->n_tile_items < 0 || info->n_shared_items < 0 ||
         int64_t(info->n_tile_items) + info->n_shared_items > info->grid)
       return fail(PA_ERR_ARG, "%s: corrupt plan info", fn);
@@ -83,7 +83,7 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
     rc = dev::launch_attn_bf16(q, k_cache, v_cache, num_blocks, block_table, max_blocks_per_seq,
                                seq_lens, cu_seqlens_q, num_q_heads, num_kv_heads, head_dim, scale,
                                plan, info->grid, info->n_shared_items + info->n_tile_items,
-                               info->n_groups,
+                               info->n_groups, (info->variant & kVariantWideRows) != 0,
                                partial_rows,
                                workspace, out, lse, st);
   }

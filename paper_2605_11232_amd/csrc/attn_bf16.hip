@@ -13,13 +13,13 @@
 //    32x32x16 MFMA.  Computing the transposed score tile puts one query row
 //    in each lane, so the online-softmax row max needs a single cross-lane
 //    exchange, and the probabilities are already laid out as the B operand
-//    of the PV product (no LDS round trip for P).  Tile items also carry the
-//    private keys of few-row sequences with more than 16 rows (verification).
+//    of the PV product (no LDS round trip for P).
 //  * shared-prefix items: the tile path over gathered rows of sequences whose
 //    leading blocks coincide (cascade); partial results are merged.
-//  * row items, one wavefront each: <= 16 rows (decode's G rows) on 16x16x32
-//    MFMA with K and V^T streamed straight from HBM into registers over a
-//    split of the key range.
+//  * row items, one wavefront each: up to 32 rows (decode's G rows, or a
+//    verification sequence's n_q * G rows cut in pieces) as one or two
+//    16-column tiles of 16x16x32 MFMA, with K and V^T streamed straight from
+//    HBM into registers over a split of the key range.
 //
 // The key order inside a tile is permuted so that each lane's eight PV
 // k-elements are eight consecutive keys: then V^T operands are single 16-byte
@@ -90,10 +90,25 @@ __device__ __forceinline__ int vswz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
 // copies into LDS, has completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// Asynchronous copy of 16 bytes per lane from global memory into LDS: lane l
-// writes bytes [16 l, 16 l + 16) after `lds` (a wave-uniform address).
-__device__ __forceinline__ void copy16_to_lds(const char* src, __bf16* lds) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+// Asynchronous copy of 16 bytes per lane into LDS: lane l reads bytes
+// [off, off + 16) of the wave-uniform block `base` (a buffer resource in
+// scalar registers, so the per-copy address work is scalar) and writes them
+// to bytes [16 l, 16 l + 16) after `lds` (wave-uniform).  Offsets at or past
+// `bytes` read zeros instead of faulting.
+__device__ __forceinline__ void copy16_to_lds(const void* base, int bytes, uint32_t off, __bf16* lds) {
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
+}
+
+// Sum of the eight bf16 values of a vector added to acc (v_dot2 with ones).
+__device__ __forceinline__ float add_bf16x8(bf16x8 v, float acc) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v[2 * i], v[2 * i + 1]}, one, acc, false);
+  return acc;
 }
 
 // max of a value over the two lane halves (lane l and l ^ 32)
@@ -212,19 +227,19 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     if constexpr (D == 128) return blk[i];
     else return blk[2 * i] + ((w >> 1) & 1) * (blk[2 * i + 1] - blk[2 * i]);  // no indexed array
   };
+  // one (block, kv-head) of K or V^T: kBlock * D bf16 at the block's address
+  constexpr int kHeadBytes = kBlock * D * 2;
   auto issue_k = [&](const int (&blk)[NB], int buf) {
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const char* src = kbase + (int64_t)copy_block(blk, i) * blk_bytes;
-      copy16_to_lds(src + koff[i], &sm.k[buf][512 * (4 * i + w)]);
-    }
+    for (int i = 0; i < NI; ++i)
+      copy16_to_lds(kbase + (int64_t)copy_block(blk, i) * blk_bytes, kHeadBytes, koff[i],
+                    &sm.k[buf][512 * (4 * i + w)]);
   };
   auto issue_v = [&](const int (&blk)[NB], int buf) {
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const char* src = vbase + (int64_t)copy_block(blk, i) * blk_bytes;
-      copy16_to_lds(src + voff[i], &sm.v[buf][512 * (4 * i + w)]);
-    }
+    for (int i = 0; i < NI; ++i)
+      copy16_to_lds(vbase + (int64_t)copy_block(blk, i) * blk_bytes, kHeadBytes, voff[i],
+                    &sm.v[buf][512 * (4 * i + w)]);
   };
 
   // S^T[key][row] of a step for the wave's 32 rows: NSUB independent 32-key chains.
@@ -277,18 +292,20 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
   };
   // Probabilities of a step as bf16 B operands: p[u][kk] holds keys
   // 32 u + 16 kk + 8 hh + 0..7 (the perm32 order makes them consecutive).
-  // Row sums in four short chains.
+  // The row sum adds the bf16 probabilities the PV product uses, two per
+  // v_dot2, in two chains.
   auto probs = [&](const f32x16 (&s)[NSUB], bf16x8 (&p)[NSUB][2]) {
-    float ls[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int u = 0; u < NSUB; ++u)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float x = fast_exp2(fmaf(s[u][e], c, -mc));
-        ls[e & 3] += x;
-        p[u][e >> 3][e & 7] = (__bf16)x;
-      }
-    l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      for (int e = 0; e < 16; ++e) p[u][e >> 3][e & 7] = (__bf16)fast_exp2(fmaf(s[u][e], c, -mc));
+    float l0 = l, l1 = 0.f;
+#pragma unroll
+    for (int u = 0; u < NSUB; ++u) {
+      l0 = add_bf16x8(p[u][0], l0);
+      l1 = add_bf16x8(p[u][1], l1);
+    }
+    l = l0 + l1;
   };
   auto pv = [&](int buf, const bf16x8 (&p)[NSUB][2]) {
 #pragma unroll
@@ -427,9 +444,12 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
   }
 }
 
-// Row item: one wavefront, up to 16 rows (one 16-column MFMA tile), keys
-// [kv0, kv1).  Sequences with more rows use tile items instead.
-template <int D>
+// Row item: one wavefront, up to 16 * NC rows (NC 16-column MFMA tiles that
+// share every K and V^T operand), keys [kv0, kv1).  Decode items hold a
+// sequence's G rows (NC = 1); verification items hold up to 32 of its
+// n_q * G rows (NC = 2), so the keys are streamed from memory once per 32
+// rows.  Sequences with more rows use tile items.
+template <int D, int NC>
 __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   constexpr int KS = D / 32;  // k-steps of the QK product (32 dims each)
   constexpr int DT = D / 16;  // 16-row tiles of O^T
@@ -443,24 +463,35 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   const int kv1 = min(it[I_KV1], L);
   const int G = a.group;
 
-  const bool valid = j < nrows;
-  const int rho = row0 + j;
-  const int qi = rho / G;
-  const int hq = g * G + (rho - qi * G);
-  const int apos = valid ? L - n + qi : -1;
+  // column j of tile c is the item's row 16 c + j
+  bool valid[NC];
+  int qi[NC], hq[NC], apos[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    valid[c] = 16 * c + j < nrows;
+    const int rho = row0 + 16 * c + j;
+    qi[c] = rho / G;
+    hq[c] = g * G + (rho - qi[c] * G);
+    apos[c] = valid[c] ? L - n + qi[c] : -1;
+  }
   const int amin = L - n + row0 / G;  // smallest position among the item's rows
 
-  bf16x8 qf[KS];
-  {
-    const __bf16* qp = a.q + ((int64_t)(qs + qi) * a.hq + hq) * D + 8 * g4;
+  bf16x8 qf[NC][KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = as_bf16x8(valid ? ld16(qp + 32 * ks) : zero16());
+  for (int c = 0; c < NC; ++c) {
+    const __bf16* qp = a.q + ((int64_t)(qs + qi[c]) * a.hq + hq[c]) * D + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[c][ks] = as_bf16x8(valid[c] ? ld16(qp + 32 * ks) : zero16());
   }
-  f32x4 acc[DT];
+  f32x4 acc[NC][DT];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const float c = a.scale_log2;
-  float m = kNegInf, mc = 0.f, l = 0.f;
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[c][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const float cs = a.scale_log2;
+  float m[NC], mc[NC], l[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) m[c] = kNegInf, mc[c] = 0.f, l[c] = 0.f;
 
   const int32_t* bt = a.bt + (int64_t)r * a.max_blocks;
   const int64_t blk_k = (int64_t)a.hkv * kBlock * D, head_k = (int64_t)g * kBlock * D;
@@ -505,14 +536,16 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   }
   for (int t0 = kv0; t0 < kv1; t0 += 32) {
     const bool more = t0 + 32 < kv1;
-    f32x4 s[2];
+    f32x4 s[NC][2];
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      f32x4 acc_s = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) acc_s = mfma16(as_bf16x8(kreg[tt][ks]), qf[ks], acc_s);
-      s[tt] = acc_s;
-    }
+      for (int c = 0; c < NC; ++c) {
+        f32x4 acc_s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) acc_s = mfma16(as_bf16x8(kreg[tt][ks]), qf[c][ks], acc_s);
+        s[c][tt] = acc_s;
+      }
     if (more) {
       blocks_of(t0 + 32);
       load_k();
@@ -521,73 +554,91 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
     const bool masked = t0 + 31 > amin || !more;  // wave-uniform
     if (masked) {
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+      for (int c = 0; c < NC; ++c)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = t0 + 8 * g4 + 4 * tt + e;
-          s[tt][e] = (key <= apos && key < kv1) ? s[tt][e] : kNegInf;
-        }
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int key = t0 + 8 * g4 + 4 * tt + e;
+            s[c][tt][e] = (key <= apos[c] && key < kv1) ? s[c][tt][e] : kNegInf;
+          }
       // zero values of keys at or past kv1 (slots that may never have been written)
       const int keep = min(max(kv1 - (t0 + 8 * g4), 0), 8);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) vreg[dt] = keep_bf16(vreg[dt], keep);
     }
-    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3]));
-    mx = fmaxf(mx, fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-    mx = fmaxf(mx, wave_xor(mx, 16));
-    mx = fmaxf(mx, wave_xor(mx, 32));
-    if (__any(mx != kNegInf && (m == kNegInf || mx * c > mc + 8.f))) {
-      const float mnew = fmaxf(m, mx);
-      const float mcn = mnew == kNegInf ? 0.f : mnew * c;
-      const float alpha = m == kNegInf ? 0.f : fast_exp2(mc - mcn);
-      l *= alpha;
+    bf16x8 pb[NC];
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) acc[dt] *= alpha;
-      m = mnew;
-      mc = mcn;
-    }
-    bf16x8 pb;
+    for (int c = 0; c < NC; ++c) {
+      float mx = fmaxf(fmaxf(s[c][0][0], s[c][0][1]), fmaxf(s[c][0][2], s[c][0][3]));
+      mx = fmaxf(mx, fmaxf(fmaxf(s[c][1][0], s[c][1][1]), fmaxf(s[c][1][2], s[c][1][3])));
+      mx = fmaxf(mx, wave_xor(mx, 16));
+      mx = fmaxf(mx, wave_xor(mx, 32));
+      if (__any(mx != kNegInf && (m[c] == kNegInf || mx * cs > mc[c] + 8.f))) {
+        const float mnew = fmaxf(m[c], mx);
+        const float mcn = mnew == kNegInf ? 0.f : mnew * cs;
+        const float alpha = m[c] == kNegInf ? 0.f : fast_exp2(mc[c] - mcn);
+        l[c] *= alpha;
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p = fast_exp2(fmaf(s[tt][e], c, -mc));
-        l += p;
-        pb[4 * tt + e] = (__bf16)p;
+        for (int dt = 0; dt < DT; ++dt) acc[c][dt] *= alpha;
+        m[c] = mnew;
+        mc[c] = mcn;
       }
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) acc[dt] = mfma16(as_bf16x8(vreg[dt]), pb, acc[dt]);
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float p = fast_exp2(fmaf(s[c][tt][e], cs, -mc[c]));
+          l[c] += p;
+          pb[c][4 * tt + e] = (__bf16)p;
+        }
+    }
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int c = 0; c < NC; ++c) acc[c][dt] = mfma16(as_bf16x8(vreg[dt]), pb[c], acc[c][dt]);
     if (more) load_v();
   }
 
-  l += wave_xor(l, 16);
-  l += wave_xor(l, 32);
-  if (!valid) return;
-  const float inv = l > 0.f ? 1.f / l : 0.f;
-  const float lse_v = l > 0.f ? kLn2 * (mc + __log2f(l)) : kNegInf;
-  if (part < 0) {
-    __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D + 4 * g4;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      __bf16 o4[4];
+  for (int c = 0; c < NC; ++c) {
+    l[c] += wave_xor(l[c], 16);
+    l[c] += wave_xor(l[c], 32);
+  }
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o4[e] = (__bf16)(acc[dt][e] * inv);
-      *reinterpret_cast<u32x2*>(op + 16 * dt) = __builtin_bit_cast(u32x2, o4);
+  for (int c = 0; c < NC; ++c) {
+    if (!valid[c]) continue;
+    const float inv = l[c] > 0.f ? 1.f / l[c] : 0.f;
+    const float lse_v = l[c] > 0.f ? kLn2 * (mc[c] + __log2f(l[c])) : kNegInf;
+    if (part < 0) {
+      __bf16* op = a.out + ((int64_t)(qs + qi[c]) * a.hq + hq[c]) * D + 4 * g4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        __bf16 o4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o4[e] = (__bf16)(acc[c][dt][e] * inv);
+        *reinterpret_cast<u32x2*>(op + 16 * dt) = __builtin_bit_cast(u32x2, o4);
+      }
+      if (a.lse && g4 == 0) a.lse[(int64_t)(qs + qi[c]) * a.hq + hq[c]] = lse_v;
+    } else {
+      const int prow = part + 16 * c + j;
+      float* op = a.ws_o + (int64_t)prow * D + 4 * g4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4*>(op + 16 * dt) = acc[c][dt] * inv;
+      if (g4 == 0) a.ws_lse[prow] = lse_v;
     }
-    if (a.lse && g4 == 0) a.lse[(int64_t)(qs + qi) * a.hq + hq] = lse_v;
-  } else {
-    float* op = a.ws_o + (int64_t)(part + j) * D + 4 * g4;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4*>(op + 16 * dt) = acc[dt] * inv;
-    if (g4 == 0) a.ws_lse[part + j] = lse_v;
   }
 }
 
-// MIX: 1 = tile and shared items only, 2 = row items only, 3 = both.
-// Separate instantiations keep a pure prefill or pure decode launch from
-// paying the other path's registers and LDS.
+// MIX bits: 1 = tile and shared items, 2 = row items of at most 16 rows,
+// 4 = row items of up to 32 rows.  Separate instantiations keep a pure
+// prefill or pure decode launch from paying the other paths' registers and
+// LDS; a launch with only 16-row row items runs at three waves per SIMD.
+template <int MIX>
+constexpr int waves_per_eu() { return MIX == 2 ? 3 : kTileWavesPerEu; }
+
 template <int D, int MIX>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kTileWavesPerEu))) void attn_bf16_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_eu<MIX>()))) void attn_bf16_kernel(AttnArgs a) {
   const int32_t* plan = a.plan;
   const int n_tile = plan[H_N_SHARED] + plan[H_N_TILE];  // workgroups before the row quads
   const int b = blockIdx.x;
@@ -608,86 +659,91 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kTileWavesP
       return;
     }
   }
-  if constexpr (MIX & 2) {
+  if constexpr ((MIX & 6) != 0) {
     const int idx = 4 * (b - n_tile) + (threadIdx.x >> 6);
-    if (b >= n_tile && idx < plan[H_N_ROW])
-      row_item<D>(plan + plan[H_ROW_OFF] + idx * kItemWords, a);
+    if (b >= n_tile && idx < plan[H_N_ROW]) {
+      const int32_t* it = plan + plan[H_ROW_OFF] + idx * kItemWords;
+      if constexpr ((MIX & 4) != 0) {
+        if (it[I_NROWS] > 16) {
+          row_item<D, 2>(it, a);
+          return;
+        }
+      }
+      row_item<D, 1>(it, a);
+    }
   }
 }
 
 // Combine split partial results by log-sum-exp: one workgroup per merge
-// group, one wavefront per row.  Lane s reads part s's LSE, the wavefront
-// reduces them, and each lane then accumulates D/64 output dims over the
-// parts with the weights broadcast from their lanes; the part loads are
-// independent, so they are issued back to back.
+// group of at most four rows, one wavefront per row, lanes over the output
+// dims.  The partial outputs of the first 16 parts are requested
+// before the part LSEs are reduced, so a row costs about one memory round
+// trip; parts are combined in split order (deterministic).
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(AttnArgs a) {
-  const int32_t* plan = a.plan;
-  const int32_t* gr = plan + plan[H_GROUP_OFF] + blockIdx.x * kGroupWords;
-  const int r = gr[G_SEQ], g = gr[G_KVH], row0 = gr[G_ROW0], nrows = gr[G_NROWS];
-  const int nsplit = gr[G_NSPLIT], part = gr[G_PART], stride = gr[G_STRIDE];
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int qs = a.cu_q[r];
-  for (int lr = w; lr < nrows; lr += 4) {
-    // pass 1: max and sum of exp over the parts' LSEs (64 parts per round)
-    float mx = kNegInf;
-    for (int s0 = 0; s0 < nsplit; s0 += 64) {
-      const int s = s0 + lane;
-      const float v = s < nsplit ? a.ws_lse[part + s * stride + lr] : kNegInf;
-      mx = fmaxf(mx, v);
-    }
+  constexpr int V = D / 64;  // output dims per lane
+  constexpr int C = 16;      // parts whose loads are in flight together
+  const int32_t* gr = a.plan + a.plan[H_GROUP_OFF] + blockIdx.x * kGroupWords;
+  const int lr = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lr >= gr[G_NROWS]) return;
+  const int r = gr[G_SEQ], g = gr[G_KVH], row0 = gr[G_ROW0];
+  const int nsplit = gr[G_NSPLIT], stride = gr[G_STRIDE];
+  const int64_t prow = (int64_t)gr[G_PART] + lr;  // partial row of split 0
+  auto part_o = [&](int s) { return a.ws_o + (prow + (int64_t)s * stride) * D + lane; };
+  auto part_lse = [&](int s) { return a.ws_lse[prow + (int64_t)s * stride]; };
+  float x[C][V];
+  auto load_batch = [&](int s0) {
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-    float sum = 0.f;
-    if (mx != kNegInf) {
-      for (int s0 = 0; s0 < nsplit; s0 += 64) {
-        const int s = s0 + lane;
-        if (s < nsplit) sum += exp2f((a.ws_lse[part + s * stride + lr] - mx) * kLog2e);
-      }
+    for (int u = 0; u < C; ++u) {
+      const float* src = part_o(min(s0 + u, nsplit - 1));  // in bounds; weight 0 past the end
+#pragma unroll
+      for (int k = 0; k < V; ++k) x[u][k] = src[64 * k];
     }
+  };
+  load_batch(0);
+  // max and sum of exp over the part LSEs, 64 parts per round
+  const float lse0 = lane < nsplit ? part_lse(lane) : kNegInf;
+  float mx = lse0;
+  for (int s = 64 + lane; s - lane < nsplit; s += 64) mx = fmaxf(mx, s < nsplit ? part_lse(s) : kNegInf);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  float o_acc[V];
+#pragma unroll
+  for (int k = 0; k < V; ++k) o_acc[k] = 0.f;
+  float lse_v = kNegInf;
+  if (mx != kNegInf) {
+    float sum = lse0 == kNegInf ? 0.f : exp2f((lse0 - mx) * kLog2e);
+    for (int s = 64 + lane; s - lane < nsplit; s += 64)
+      if (s < nsplit) sum += exp2f((part_lse(s) - mx) * kLog2e);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
-    const float lse_v = mx == kNegInf ? kNegInf : mx + kLn2 * __log2f(sum);
-    // pass 2: weighted sum of the normalised partial outputs
-    float o[D / 64];
-#pragma unroll
-    for (int k = 0; k < D / 64; ++k) o[k] = 0.f;
-    if (mx != kNegInf) {
-      for (int s0 = 0; s0 < nsplit; s0 += 64) {
-        const int sl = s0 + lane;
-        const float wl = sl < nsplit ? exp2f((a.ws_lse[part + sl * stride + lr] - lse_v) * kLog2e) : 0.f;
-        const int cnt = min(64, nsplit - s0);
-        int s = 0;
-        for (; s + 4 <= cnt; s += 4) {
-          float x[4][D / 64], wt[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            wt[u] = __shfl(wl, s + u, 64);
-            const float* src = a.ws_o + (int64_t)(part + (s0 + s + u) * stride + lr) * D + lane;
-#pragma unroll
-            for (int k = 0; k < D / 64; ++k) x[u][k] = src[64 * k];
-          }
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int k = 0; k < D / 64; ++k) o[k] = fmaf(wt[u], x[u][k], o[k]);
-        }
-        for (; s < cnt; ++s) {
-          const float wt = __shfl(wl, s, 64);
-          const float* src = a.ws_o + (int64_t)(part + (s0 + s) * stride + lr) * D + lane;
-#pragma unroll
-          for (int k = 0; k < D / 64; ++k) o[k] = fmaf(wt, src[64 * k], o[k]);
+    lse_v = mx + kLn2 * __log2f(sum);
+    // weight of part s0 + lane of the current round of 64, held by that lane
+    float wl = exp2f((lse0 - lse_v) * kLog2e);
+    for (int s0 = 0; s0 < nsplit; s0 += C) {
+      if (s0 > 0) {
+        load_batch(s0);
+        if (s0 % 64 == 0) {
+          const int s = s0 + lane;
+          wl = s < nsplit ? exp2f((part_lse(s) - lse_v) * kLog2e) : 0.f;
         }
       }
-    }
-    const int rho = row0 + lr;
-    const int qi = rho / a.group;
-    const int hq = g * a.group + (rho - qi * a.group);
-    __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D;
 #pragma unroll
-    for (int k = 0; k < D / 64; ++k) op[lane + 64 * k] = (__bf16)o[k];
-    if (a.lse && lane == 0) a.lse[(int64_t)(qs + qi) * a.hq + hq] = lse_v;
+      for (int u = 0; u < C; ++u) {
+        const float wt = s0 + u < nsplit ? __shfl(wl, (s0 + u) & 63, 64) : 0.f;
+#pragma unroll
+        for (int k = 0; k < V; ++k) o_acc[k] = fmaf(wt, x[u][k], o_acc[k]);
+      }
+    }
   }
+  const int qs = a.cu_q[r];
+  const int rho = row0 + lr;
+  const int qi = rho / a.group;
+  const int hq = g * a.group + (rho - qi * a.group);
+  __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D;
+#pragma unroll
+  for (int k = 0; k < V; ++k) op[lane + 64 * k] = (__bf16)o_acc[k];
+  if (a.lse && lane == 0) a.lse[(int64_t)(qs + qi) * a.hq + hq] = lse_v;
 }
 
 }  // namespace
@@ -696,7 +752,7 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
                      const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
                      const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
                      const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
-                     int64_t partial_rows, void* ws, void* out, float* lse,
+                     bool wide_rows, int64_t partial_rows, void* ws, void* out, float* lse,
                      hipStream_t stream) {
   AttnArgs a;
   a.q = static_cast<const __bf16*>(q);
@@ -717,14 +773,25 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
   a.group = hq / hkv;
   a.scale_log2 = scale * kLog2e;
   if (grid > 0) {
-    const int mix = (n_tile > 0 ? 1 : 0) | (grid > n_tile ? 2 : 0);
+    // tiles and rows together: the tile path's register budget holds the
+    // wide row path too
+    const bool rows = grid > n_tile;
+    const int mix = n_tile == 0 ? (wide_rows ? 6 : 2) : (rows ? 7 : 1);
 #define PA_LAUNCH(DD, MM) \
   hipLaunchKernelGGL((attn_bf16_kernel<DD, MM>), dim3(grid), dim3(256), 0, stream, a)
+#define PA_LAUNCH_D(DD)                      \
+  switch (mix) {                             \
+    case 1: PA_LAUNCH(DD, 1); break;         \
+    case 2: PA_LAUNCH(DD, 2); break;         \
+    case 6: PA_LAUNCH(DD, 6); break;         \
+    default: PA_LAUNCH(DD, 7); break;        \
+  }
     if (d == 128) {
-      if (mix == 1) PA_LAUNCH(128, 1); else if (mix == 2) PA_LAUNCH(128, 2); else PA_LAUNCH(128, 3);
+      PA_LAUNCH_D(128);
     } else {
-      if (mix == 1) PA_LAUNCH(64, 1); else if (mix == 2) PA_LAUNCH(64, 2); else PA_LAUNCH(64, 3);
+      PA_LAUNCH_D(64);
     }
+#undef PA_LAUNCH_D
 #undef PA_LAUNCH
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return static_cast<int>(e);

@@ -4,14 +4,14 @@
 // every row of an item reads the same keys and values (grouped-query
 // attention).  Sequences with many rows (suffix prefill, prefill chunks) are
 // cut into 128-row tile items, each a workgroup of four wavefronts sharing
-// key/value tiles through LDS.  Sequences with at most 64 rows (decode: G rows;
-// verification: n_q * G rows) become single-wavefront row items of up to 16
-// rows whose key range is split so the launch has enough wavefronts in flight
-// to stream the cache at HBM bandwidth; the row groups of one key range sit
-// next to each other so their loads meet in cache, and split partial results
-// are combined by log-sum-exp in a merge pass.
+// key/value tiles through LDS.  Sequences with at most 32 rows (decode: G
+// rows; short verification: n_q * G rows) become single-wavefront row items
+// whose key range is split so the launch has enough wavefronts in flight to
+// stream the cache at HBM bandwidth; sequences with 33..64 rows run their
+// split key ranges as tile items.  Split partial results are combined by
+// log-sum-exp in a merge pass.
 //
-// Shared prefixes (cascade): single-wave sequences whose block tables start
+// Shared prefixes (cascade): few-row sequences whose block tables start
 // with the same blocks read the same prefix keys (Section 2, Automatic Prefix
 // Caching; Section 5.3, the same policy prefix across thousands of requests).
 // Their attention over the shared keys is computed once, as 128-row MFMA tiles
@@ -41,6 +41,8 @@
 namespace {
 
 constexpr int kXcds = 8;
+constexpr int64_t kRowWavesPerCu = 16;      // row-item split target
+constexpr int64_t kPrivateTileKeys = 2048;  // most private keys a few-row tile item covers
 
 using Rec = std::array<int32_t, pa::kItemWords>;
 
@@ -163,13 +165,13 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   if (dtype == PA_BF16) {
     auto qlen = [&](int32_t r) { return cu_seqlens_q[r + 1] - cu_seqlens_q[r]; };
     // Sequences with few rows (decode, verification) get split key ranges and
-    // may join a cascade group; their private keys run on single-wave row
-    // items when a 16-row MFMA tile holds all their rows, else on tile items
-    // (the keys are then streamed once for all rows instead of once per 16).
+    // may join a cascade group.  Their private keys run on one single-wave
+    // row item per key range when it holds all their rows (at most 32), else
+    // on tile items, whose four wavefronts share each key tile through LDS.
     auto is_row = [&](int32_t r) { return qlen(r) > 0 && qlen(r) * G <= pa::kRowSeqRows; };
     auto on_tiles = [&](int32_t r) { return qlen(r) * G > pa::kRowItemRows; };
 
-    // Cascade groups: single-wave sequences with the same first block and
+    // Cascade groups: few-row sequences with the same first block and
     // q_len whose leading blocks coincide share those keys; attention over
     // them runs once for all the group's rows.
     std::vector<int32_t> kstart(n_seqs, 0);       // first private key
@@ -217,14 +219,13 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     }
 
     // Key-range split of row items (private keys only for cascade members):
-    // aim for enough single-wave items to keep ~16 wavefronts per CU busy,
-    // never below 256 keys per item.
+    // aim for enough single-wave items to keep kRowWavesPerCu wavefronts per
+    // CU busy, never below 256 keys per item.
     int64_t row_keys = 0;
     for (int32_t r = 0; r < n_seqs; ++r)
       if (is_row(r) && !on_tiles(r))
-        row_keys += int64_t(seq_lens[r] - kstart[r]) * num_kv_heads *
-                    cdiv(qlen(r) * G, pa::kRowItemRows);
-    const int64_t target_waves = int64_t(num_cus) * 16;
+        row_keys += int64_t(seq_lens[r] - kstart[r]) * num_kv_heads;
+    const int64_t target_waves = int64_t(num_cus) * kRowWavesPerCu;
     int64_t chunk = std::max<int64_t>(256, cdiv(row_keys, std::max<int64_t>(1, target_waves)));
     chunk = cdiv(chunk, pa::kKeyStep) * pa::kKeyStep;
 
@@ -239,10 +240,9 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       for (int32_t r = 0; r < n_seqs; ++r) {
         if (qlen(r) == 0) continue;
         if (is_row(r) && on_tiles(r))
-          nt += cdiv(seq_lens[r] - kstart[r], pa::kPrivateTileKeys);
+          nt += cdiv(seq_lens[r] - kstart[r], kPrivateTileKeys);
         else if (is_row(r))
-          nr += cdiv(qlen(r) * G, pa::kRowItemRows) *
-                std::max<int64_t>(1, cdiv(seq_lens[r] - kstart[r], chunk));
+          nr += std::max<int64_t>(1, cdiv(seq_lens[r] - kstart[r], chunk));
         else
           nt += cdiv(int64_t(qlen(r)) * G, pa::kTileRows);
       }
@@ -252,9 +252,9 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         head_rows[g].reserve(nr);
         row_cost[g].reserve(nr);
       }
-      int64_t ng = 0;  // merge groups, at most one per 16 rows of a few-row sequence
+      int64_t ng = 0;  // merge groups, one per kMergeRows rows of a few-row sequence
       for (int32_t r = 0; r < n_seqs; ++r)
-        if (is_row(r)) ng += cdiv(qlen(r) * G, pa::kRowItemRows);
+        if (is_row(r)) ng += cdiv(qlen(r) * G, pa::kMergeRows);
       groups.reserve(size_t(ng) * num_kv_heads);
     }
     for (int32_t r = 0; r < n_seqs; ++r) {
@@ -265,30 +265,30 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       if (is_row(r)) {
         const int32_t k0s = kstart[r];
         const bool tiled = on_tiles(r);
-        const int64_t split = tiled ? pa::kPrivateTileKeys : chunk;
-        const int64_t step = tiled ? pa::kTileStep : pa::kKeyStep;
+        const int64_t split = tiled ? kPrivateTileKeys : chunk;
+        const int64_t kstep = tiled ? pa::kTileStep : pa::kKeyStep;
         const int32_t nsplit = static_cast<int32_t>(std::max<int64_t>(1, cdiv(L - k0s, split)));
         // equal private key ranges, multiples of the key step, covering [k0s, L)
-        const int64_t per = cdiv(cdiv(L - k0s, nsplit), step) * step;
+        const int64_t per = cdiv(cdiv(L - k0s, nsplit), kstep) * kstep;
         int32_t used = 0;
         while (used < nsplit && k0s + int64_t(used) * per < L) ++used;
         // parts 0 .. first-1 are the shared prefix's key chunks
         const int32_t first = cgroup[r] >= 0 ? cg_chunks[cgroup[r]] : 0;
         const int32_t parts = used + first;
-        const int32_t ngroups = static_cast<int32_t>(cdiv(rows, pa::kRowItemRows));
+        const int32_t nmerge = static_cast<int32_t>(cdiv(rows, pa::kMergeRows));
         for (int32_t g = 0; g < num_kv_heads; ++g) {
           int64_t base = -1;
           if (parts > 1) {
             base = partial_rows;
             partial_rows += int64_t(parts) * rows;
-            for (int32_t gi = 0; gi < ngroups; ++gi) {
-              const int32_t row0 = gi * pa::kRowItemRows;
-              const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
+            for (int32_t gi = 0; gi < nmerge; ++gi) {
+              const int32_t row0 = gi * pa::kMergeRows;
+              const int32_t nr = std::min(pa::kMergeRows, rows - row0);
               groups.push_back({r, g, row0, nr, parts, int32_t(base + row0), rows, 0});
             }
             if (first) member_base[size_t(r) * num_kv_heads + g] = int32_t(base);
           }
-          // per split, the row groups back to back (or one tile item with all rows)
+          // per split, the row pieces back to back
           for (int32_t sp = 0; sp < used; ++sp) {
             const int64_t k0 = k0s + sp * per, k1 = std::min<int64_t>(L, k0s + (sp + 1) * per);
             if (tiled) {
@@ -297,14 +297,9 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
               tile_cost[g].push_back((k1 - k0) * rows);
               continue;
             }
-            for (int32_t gi = 0; gi < ngroups; ++gi) {
-              const int32_t row0 = gi * pa::kRowItemRows;
-              const int32_t nr = std::min(pa::kRowItemRows, rows - row0);
-              const int32_t part =
-                  base < 0 ? -1 : int32_t(base + int64_t(sp + first) * rows + row0);
-              head_rows[g].push_back({r, g, row0, nr, int32_t(k0), int32_t(k1), part, 0});
-              row_cost[g].push_back(k1 - k0);
-            }
+            const int32_t part = base < 0 ? -1 : int32_t(base + int64_t(sp + first) * rows);
+            head_rows[g].push_back({r, g, 0, rows, int32_t(k0), int32_t(k1), part, 0});
+            row_cost[g].push_back(k1 - k0);
           }
         }
       } else {
@@ -363,10 +358,10 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         const auto ord = order_longest_first(costs[g]);
         for (size_t i = 0; i < ord.size(); ++i) q[xs[i % xs.size()]].push_back(lists[g][ord[i]]);
       }
-      return interleave(q);
+      return q;
     };
-    shared = deal(head_shared, shared_cost);
-    tiles = deal(head_tiles, tile_cost);
+    const auto shared_q = deal(head_shared, shared_cost);
+    const auto tile_q = deal(head_tiles, tile_cost);
     // Row items: per head, longest first, four to a workgroup (padded with
     // empty items) so a workgroup's waves share one kv-head.
     std::vector<std::vector<std::pair<int32_t, int32_t>>> quad_q(kXcds);
@@ -378,6 +373,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       for (auto x : xs) quad_q[x].reserve(quad_q[x].size() + size_t(nq) / xs.size() + 1);
       for (int32_t q = 0; q < nq; ++q) quad_q[xs[q % xs.size()]].push_back({g, 4 * q});
     }
+    shared = interleave(shared_q);
+    tiles = interleave(tile_q);
     quads = interleave(quad_q);
   }
 
@@ -403,7 +400,10 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   info->n_merge_rows = 0;
   for (auto& g : groups) info->n_merge_rows += g[pa::G_NROWS];
   info->grid = int32_t(grid);
-  info->variant = dtype == PA_F32 ? 0 : 1;
+  bool wide = false;
+  for (const auto& rows : head_rows)
+    for (const auto& it : rows) wide = wide || it[pa::I_NROWS] > 16;
+  info->variant = dtype == PA_F32 ? 0 : (pa::kVariantBf16 | (wide ? pa::kVariantWideRows : 0));
   info->plan_words = words;
   info->workspace_bytes = partial_rows * int64_t(head_dim + 1) * int64_t(sizeof(float));
   if (!plan) return PA_OK;

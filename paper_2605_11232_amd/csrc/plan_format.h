@@ -60,13 +60,18 @@ enum : int32_t {
   kGroupWords = 8
 };
 
+// pa_plan_info.variant: 0 float32 kernel; bf16 plans 1, plus 2 when some
+// row item holds more than 16 rows (selects the wide row-item kernel).
+constexpr int32_t kVariantBf16 = 1;
+constexpr int32_t kVariantWideRows = 2;
+
 constexpr int32_t kTileRows = 128;    // rows per tile item (4 waves x 32)
-constexpr int32_t kRowItemRows = 16;  // rows per single-wave item (one 16-column MFMA tile)
+constexpr int32_t kRowItemRows = 32;  // rows per single-wave item (two 16-column MFMA tiles)
+constexpr int32_t kMergeRows = 4;     // rows per merge group (one wavefront each)
 constexpr int32_t kRowSeqRows = 64;   // sequences with at most this many rows use row items
 constexpr int32_t kKeyStep = 32;      // keys per row-item inner iteration
 constexpr int32_t kTileStep = 64;     // keys per tile-item inner iteration
 constexpr int32_t kSharedChunk = 2048;  // most shared keys one cascade item covers
-constexpr int32_t kPrivateTileKeys = 2048;  // most private keys a few-row tile item covers
 constexpr int32_t kSharedMinKeys = 256; // shorter shared prefixes are not split off
 
 }  // namespace pa

@@ -200,7 +200,8 @@ H_N_SHARED, H_N_TILE, H_N_ROW, H_N_GROUPS, H_GRID = 2, 3, 4, 5, 6
 H_SHARED_OFF, H_TILE_OFF, H_ROW_OFF, H_GROUP_OFF, H_MEMBER_OFF, H_PARTIAL_ROWS = 12, 13, 14, 15, 16, 17
 WAVES = 4                 # wavefronts per workgroup: row items come WAVES to a workgroup
 TILE_ROWS = 32 * WAVES    # rows of a tile or shared item (32 per wavefront)
-ROW_ITEM_ROWS = 16
+ROW_ITEM_ROWS = 32        # rows of a row item (two 16-column MFMA tiles)
+VARIANT_WIDE_ROWS = 2     # plan info variant bit: some row item has more than 16 rows
 
 
 def parse_plan(plan):
@@ -226,6 +227,7 @@ def check_plan(plan, info, L, cu, G, hkv, D=128):
         if pr >= 0:
             writes[pr] = writes.get(pr, 0) + 1
     assert h[H_N_ROW] % WAVES == 0
+    assert bool(info.variant & VARIANT_WIDE_ROWS) == any(t[3] > 16 for t in rows if t[0] >= 0)
     assert all(0 < t[3] <= TILE_ROWS for t in tiles) and all(0 < t[3] <= TILE_ROWS for t in shared)
     assert all(t[3] <= ROW_ITEM_ROWS for t in rows if t[0] >= 0)
     for seq, kvh, row0, nrows, kv0, kv1, part, _ in tiles + rows:

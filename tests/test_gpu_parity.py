@@ -189,7 +189,8 @@ def test_needle_through_block_table():
 
 def test_edge_cases():
     """Empty launch, zero-query sequences mixed in, a one-token sequence,
-    head_dim 64 in bf16, G = 1, verify with 64 rows (tile path)."""
+    head_dim 64 in bf16, G = 1, verify with 16 to 128 rows per sequence (narrow
+    and wide row items, tile items)."""
     _gpu()
     from oracle.run import OracleReplay
     from paper_2605_11232_amd.runtime import DeviceReplay
@@ -231,10 +232,12 @@ def test_edge_cases():
         torch.cuda.synchronize()
         if sum(ql):
             close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"edge{ci}")
-    # verify with n_q = 8: G = 2 gives 16 rows per sequence (single-wave row
-    # items); G = 8 gives 64 rows (tile items with split private key ranges,
+    # verify with n_q = 8: G = 2 gives 16 rows per sequence (one 16-row row
+    # item per key range); G = 3 gives 24 rows (a row item of two 16-column
+    # tiles); G = 8 gives 64 rows (tile items over split private key ranges,
     # two of the four wavefronts idle); G = 16 gives 128 rows (one tile item)
-    for G, want_tiles in ((2, False), (8, True), (16, True)):
+    for G, want_tiles, want_wide in ((2, False, False), (3, False, True), (8, True, False),
+                                     (16, True, False)):
         cfg8 = synth.AttnConfig(f"edge-g{G}", "bf16", 2 * G, 2, 128, 16, 78)
         setup, launch = mk([8, 8], [40, 517], 9, cfg=cfg8)
         wl = synth.Workload(cfg8, 128, np.arange(128, dtype=np.int32), setup, [launch], None, 40)
@@ -245,6 +248,7 @@ def test_edge_cases():
         torch.cuda.synchronize()
         assert (p.info.n_tile_items > 0) == want_tiles
         assert (p.info.n_row_items > 0) == (not want_tiles)
+        assert bool(p.info.variant & 2) == want_wide
         close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"verify-G{G}")
 
 
