@@ -242,8 +242,22 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
                     &sm.v[buf][512 * (4 * i + w)]);
   };
 
+  // LDS operand addresses: per lane, the byte offset of its K unit for each
+  // k-step (row j of a 32-key tile; the swizzle depends on the k-step) and
+  // of its V^T unit; buffers, 32-key tiles and 32-dim tiles add constants, so
+  // with the buffer known at compile time every operand read is one
+  // register plus an immediate offset.
+  uint32_t kofs[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) kofs[ks] = 16u * (j * CU + ((2 * ks + hh) ^ (j % CU)));
+  const uint32_t vofs = 16u * (2 * j + (hh ^ vswz(j)));  // vswz(32 dt + j) == vswz(j)
+  auto lds_at = [](const __bf16* base, uint32_t byte_off) {
+    return reinterpret_cast<const __bf16*>(reinterpret_cast<const char*>(base) + byte_off);
+  };
+
   // S^T[key][row] of a step for the wave's 32 rows: NSUB independent 32-key chains.
-  auto scores = [&](int buf, f32x16 (&s)[NSUB]) {
+  auto scores = [&](auto buf_c, f32x16 (&s)[NSUB]) {
+    constexpr int buf = decltype(buf_c)::value;
 #pragma unroll
     for (int u = 0; u < NSUB; ++u)
 #pragma unroll
@@ -251,10 +265,8 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks)
 #pragma unroll
-      for (int u = 0; u < NSUB; ++u) {
-        const int r = 32 * u + j, col = 2 * ks + hh;
-        s[u] = mfma32(as_bf16x8(ld16(&sm.k[buf][8 * (r * CU + (col ^ (r % CU)))])), qf[ks], s[u]);
-      }
+      for (int u = 0; u < NSUB; ++u)
+        s[u] = mfma32(as_bf16x8(ld16(lds_at(&sm.k[buf][32 * u * D], kofs[ks]))), qf[ks], s[u]);
   };
   auto mask = [&](int t0, f32x16 (&s)[NSUB]) {
 #pragma unroll
@@ -307,17 +319,16 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     }
     l = l0 + l1;
   };
-  auto pv = [&](int buf, const bf16x8 (&p)[NSUB][2]) {
+  auto pv = [&](auto buf_c, const bf16x8 (&p)[NSUB][2]) {
+    constexpr int buf = decltype(buf_c)::value;
 #pragma unroll
     for (int u = 0; u < NSUB; ++u)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) {
-          const int d = 32 * dt + j;
-          const __bf16* vb = &sm.v[buf][(2 * u + kk) * BLK + 8 * (2 * d + (hh ^ vswz(d)))];
-          acc[dt] = mfma32(as_bf16x8(ld16(vb)), p[u][kk], acc[dt]);
-        }
+        for (int dt = 0; dt < D / 32; ++dt)
+          acc[dt] = mfma32(as_bf16x8(ld16(lds_at(&sm.v[buf][(2 * u + kk) * BLK + 512 * dt], vofs))),
+                           p[u][kk], acc[dt]);
   };
   // Values of keys at or past kend in the last step: zero (never-written cache
   // slots may hold anything, and 0 * NaN would reach the output).
@@ -348,31 +359,35 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     // with the copies and pass the barriers.
     const bool active = FULL || w * 32 < nrows;
     f32x16 s[NSUB];
+    using B0 = std::integral_constant<int, 0>;
+    using B1 = std::integral_constant<int, 1>;
     if (active) {
-      scores(0, s);
+      scores(B0{}, s);
       if (n_plain == 0) mask(kv0, s);
       rebase(rowmax(s));
     }
     __syncthreads();  // K buffer 0 is refilled next
 
     // One pipelined step: softmax + PV of step t, scores + max of step t + 1.
-    auto step = [&](int t, auto mask_next) {
+    // buf_c = t % 2, the LDS buffer pair of step t (a compile-time constant).
+    auto step = [&](int t, auto mask_next, auto buf_c) {
+      constexpr int buf = decltype(buf_c)::value;
       const int t0 = kv0 + KT * t;
       if (t + 2 < ntiles) {
         step_blocks(t0 + 2 * KT, bk);
-        issue_k(bk, t & 1);
+        issue_k(bk, buf);
       }
-      issue_v(bv, (t + 1) & 1);  // blocks of step t + 1, found one step earlier
+      issue_v(bv, 1 - buf);  // blocks of step t + 1, found one step earlier
 #pragma unroll
       for (int b = 0; b < NB; ++b) bv[b] = bk[b];
       bf16x8 p[NSUB][2];
       f32x16 sn[NSUB];
       probs(s, p);
-      scores((t + 1) & 1, sn);
+      scores(std::integral_constant<int, 1 - buf>{}, sn);
       // keep the row-sum additions in this region, where they overlap the
       // score MFMAs, instead of letting them sink past the barrier
       asm volatile("" : "+v"(l));
-      pv(t & 1, p);
+      pv(buf_c, p);
       if constexpr (decltype(mask_next)::value) mask(t0 + KT, sn);
       const float mx = rowmax(sn);
       wait_vmem();
@@ -393,10 +408,21 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
       wait_vmem();
       __syncthreads();
     };
+    // steps [t, lim) with the given masking, two at a time so that each
+    // step's buffer pair is a compile-time constant
+    auto run = [&](int& t, int lim, auto mask_next) {
+      if (t < lim && (t & 1)) step(t++, mask_next, B1{});
+      for (; t + 1 < lim; t += 2) {
+        step(t, mask_next, B0{});
+        step(t + 1, mask_next, B1{});
+      }
+      if (t < lim) step(t++, mask_next, B0{});
+    };
     int t = 0;
     if (active) {
-      for (; t + 1 < min(n_plain, ntiles); ++t) step(t, std::false_type{});
-      for (; t + 1 < ntiles; ++t) step(t, std::true_type{});
+      // step t masks the scores of step t + 1: unmasked while t + 1 < n_plain
+      run(t, min(n_plain, ntiles) - 1, std::false_type{});
+      run(t, ntiles - 1, std::true_type{});
     } else {
       for (; t + 1 < ntiles; ++t) idle_step(t);
     }
@@ -408,7 +434,10 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
       zero_tail(t0, t & 1);
       __syncthreads();
     }
-    if (active) pv(t & 1, p);
+    if (active) {
+      if (t & 1) pv(B1{}, p);
+      else pv(B0{}, p);
+    }
   }
 
   l += wave_xor(l, 32);
