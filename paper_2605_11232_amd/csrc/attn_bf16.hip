@@ -489,7 +489,9 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   const int lane = threadIdx.x & 63, j = lane & 15, g4 = lane >> 4;
   const int L = a.seq_lens[r];
   const int qs = a.cu_q[r], n = a.cu_q[r + 1] - qs;
-  const int kv1 = min(it[I_KV1], L);
+  // at most kRowItemBlocks blocks per item (the planner's limit; the clamp
+  // keeps every table read inside the item's span)
+  const int kv1 = min(min(it[I_KV1], L), kv0 + kRowItemBlocks * kBlock);
   const int G = a.group;
 
   // column j of tile c is the item's row 16 c + j
@@ -531,11 +533,12 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   // One register set for K and one for V^T: the next step's K loads are
   // issued as soon as the score MFMAs have consumed K, and its V^T loads as
   // soon as the PV MFMAs have consumed V^T, so HBM reads overlap the softmax
-  // and the MFMAs of the current step.  All loads are in bounds (a missing
-  // second block aliases the first).
+  // and the MFMAs of the current step.  The loads are non-temporal (private
+  // keys are read once).  All loads are in bounds (a missing second block
+  // aliases the first).
   u32x4 kreg[2][KS], vreg[DT];
   int b0 = 0, b1 = 0;
-  BlockWindow win;
+  BlockSpan win;
   win.init(bt, a.max_blocks, kv0 / kBlock);
   auto blocks_of = [&](int t0) {
     const int jb = t0 / kBlock;
@@ -549,13 +552,13 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
       const int blk = kk < 16 ? b0 : b1;
       const __bf16* p = a.kc + blk * blk_k + head_k + (kk & 15) * D + 8 * g4;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kreg[tt][ks] = ld16(p + 32 * ks);
+      for (int ks = 0; ks < KS; ++ks) kreg[tt][ks] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p + 32 * ks));
     }
   };
   auto load_v = [&]() {
     const __bf16* p = a.vc + (g4 < 2 ? b0 : b1) * blk_v + head_v + j * kBlock + 8 * (g4 & 1);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vreg[dt] = ld16(p + 16 * kBlock * dt);
+    for (int dt = 0; dt < DT; ++dt) vreg[dt] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p + 16 * kBlock * dt));
   };
 
   if (kv0 < kv1) {

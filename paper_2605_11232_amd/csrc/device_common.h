@@ -85,6 +85,24 @@ struct BlockWindow {
   }
 };
 
+// A wavefront's view of at most 64 consecutive entries of a block-table row,
+// one per lane, loaded once (items that never span more than 64 blocks): no
+// table load inside the key loop, so the loop's memory waits only concern
+// its key and value loads.
+struct BlockSpan {
+  int base;  // first block index held
+  int ids;
+  __device__ __forceinline__ void init(const int32_t* row, int max_blocks, int first_block) {
+    base = first_block;
+    const int j = first_block + (threadIdx.x & 63);
+    ids = row[j < max_blocks ? j : max_blocks - 1];
+  }
+  // Block id of logical block jb, base <= jb < base + 64 (wave-uniform).
+  __device__ __forceinline__ int get(int jb) const {
+    return __builtin_amdgcn_readlane(ids, (jb - base) & 63);
+  }
+};
+
 __device__ __forceinline__ int clamp_block(int b, int num_blocks) {
   return b < 0 ? 0 : (b >= num_blocks ? num_blocks - 1 : b);
 }

@@ -220,7 +220,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
 
     // Key-range split of row items (private keys only for cascade members):
     // aim for enough single-wave items to keep kRowWavesPerCu wavefronts per
-    // CU busy, never below 256 keys per item.
+    // CU busy, never below 256 keys and never above 1024 keys per item.
     int64_t row_keys = 0;
     for (int32_t r = 0; r < n_seqs; ++r)
       if (is_row(r) && !on_tiles(r))
@@ -228,6 +228,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     const int64_t target_waves = int64_t(num_cus) * kRowWavesPerCu;
     int64_t chunk = std::max<int64_t>(256, cdiv(row_keys, std::max<int64_t>(1, target_waves)));
     chunk = cdiv(chunk, pa::kKeyStep) * pa::kKeyStep;
+    // a row item's block ids fit one wavefront (64 lanes): at most 1024 keys
+    chunk = std::min<int64_t>(chunk, int64_t(pa::kRowItemBlocks) * block_size);
 
     std::vector<std::vector<Rec>> head_tiles(num_kv_heads);
     head_rows.assign(num_kv_heads, {});

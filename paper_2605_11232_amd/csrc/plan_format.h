@@ -70,6 +70,7 @@ constexpr int32_t kRowItemRows = 32;  // rows per single-wave item (two 16-colum
 constexpr int32_t kMergeRows = 4;     // rows per merge group (one wavefront each)
 constexpr int32_t kRowSeqRows = 64;   // sequences with at most this many rows use row items
 constexpr int32_t kKeyStep = 32;      // keys per row-item inner iteration
+constexpr int32_t kRowItemBlocks = 64;  // most blocks (of 16 keys) one row item spans
 constexpr int32_t kTileStep = 64;     // keys per tile-item inner iteration
 constexpr int32_t kSharedChunk = 2048;  // most shared keys one cascade item covers
 constexpr int32_t kSharedMinKeys = 256; // shorter shared prefixes are not split off

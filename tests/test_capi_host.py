@@ -230,6 +230,8 @@ def check_plan(plan, info, L, cu, G, hkv, D=128):
     assert bool(info.variant & VARIANT_WIDE_ROWS) == any(t[3] > 16 for t in rows if t[0] >= 0)
     assert all(0 < t[3] <= TILE_ROWS for t in tiles) and all(0 < t[3] <= TILE_ROWS for t in shared)
     assert all(t[3] <= ROW_ITEM_ROWS for t in rows if t[0] >= 0)
+    # a row item's block ids are one 64-lane load: at most 64 blocks of 16 keys
+    assert all(t[5] - t[4] <= 64 * 16 for t in rows if t[0] >= 0)
     for seq, kvh, row0, nrows, kv0, kv1, part, _ in tiles + rows:
         if seq < 0:
             continue
