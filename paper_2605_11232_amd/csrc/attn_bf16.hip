@@ -111,6 +111,32 @@ __device__ __forceinline__ float add_bf16x8(bf16x8 v, float acc) {
   return acc;
 }
 
+#ifndef PA_LDS_PREFETCH
+#define PA_LDS_PREFETCH 8
+#endif
+// N MFMAs whose A operands are 16-byte LDS reads (addr(i) gives the address
+// of MFMA i), with PF reads in flight ahead of the MFMA that uses them: LDS
+// latency is hidden behind the MFMAs instead of being paid before each one.
+// The scheduling-group barriers keep the read-ahead order in the code.
+template <int N, int PF, class AddrF, class MfmaF>
+__device__ __forceinline__ void lds_mfma_pipeline(AddrF addr, MfmaF mfma) {
+  static_assert(PF >= 1 && PF <= N, "read-ahead depth");
+  u32x4 x[PF];
+#pragma unroll
+  for (int i = 0; i < PF; ++i) x[i] = ld16(addr(i));
+  __builtin_amdgcn_sched_group_barrier(0x100, PF, 0);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const u32x4 a = x[i % PF];
+    if (i + PF < N) {
+      x[i % PF] = ld16(addr(i + PF));
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    mfma(i, a);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+}
+
 // max of a value over the two lane halves (lane l and l ^ 32)
 __device__ __forceinline__ float max_halves(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -262,11 +288,10 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
     for (int u = 0; u < NSUB; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[u][e] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks)
-#pragma unroll
-      for (int u = 0; u < NSUB; ++u)
-        s[u] = mfma32(as_bf16x8(ld16(lds_at(&sm.k[buf][32 * u * D], kofs[ks]))), qf[ks], s[u]);
+    // MFMA i: k-step i / NSUB of 32-key chain i % NSUB
+    lds_mfma_pipeline<D / 16 * NSUB, PA_LDS_PREFETCH>(
+        [&](int i) { return lds_at(&sm.k[buf][32 * (i % NSUB) * D], kofs[i / NSUB]); },
+        [&](int i, u32x4 k) { s[i % NSUB] = mfma32(as_bf16x8(k), qf[i / NSUB], s[i % NSUB]); });
   };
   auto mask = [&](int t0, f32x16 (&s)[NSUB]) {
 #pragma unroll
@@ -321,14 +346,13 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
   };
   auto pv = [&](auto buf_c, const bf16x8 (&p)[NSUB][2]) {
     constexpr int buf = decltype(buf_c)::value;
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt)
-          acc[dt] = mfma32(as_bf16x8(ld16(lds_at(&sm.v[buf][(2 * u + kk) * BLK + 512 * dt], vofs))),
-                           p[u][kk], acc[dt]);
+    // MFMA i: dims 32 (i % DT) .. of keys 16 (i / DT) .. (16-key half i / DT)
+    constexpr int DT = D / 32;
+    lds_mfma_pipeline<2 * NSUB * DT, PA_LDS_PREFETCH>(
+        [&](int i) { return lds_at(&sm.v[buf][(i / DT) * BLK + 512 * (i % DT)], vofs); },
+        [&](int i, u32x4 v) {
+          acc[i % DT] = mfma32(as_bf16x8(v), p[(i / DT) / 2][(i / DT) % 2], acc[i % DT]);
+        });
   };
   // Values of keys at or past kend in the last step: zero (never-written cache
   // slots may hold anything, and 0 * NaN would reach the output).
@@ -383,11 +407,16 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
       bf16x8 p[NSUB][2];
       f32x16 sn[NSUB];
       probs(s, p);
+      // The matrix section runs at raised issue priority: of the two
+      // wavefronts sharing a SIMD, the one issuing MFMAs goes first and the
+      // other's softmax VALU work fills the remaining issue slots.
+      __builtin_amdgcn_s_setprio(1);
       scores(std::integral_constant<int, 1 - buf>{}, sn);
       // keep the row-sum additions in this region, where they overlap the
       // score MFMAs, instead of letting them sink past the barrier
       asm volatile("" : "+v"(l));
       pv(buf_c, p);
+      __builtin_amdgcn_s_setprio(0);
       if constexpr (decltype(mask_next)::value) mask(t0 + KT, sn);
       const float mx = rowmax(sn);
       wait_vmem();
