@@ -82,6 +82,19 @@ std::vector<int32_t> order_longest_first(const std::vector<int64_t>& cost) {
   return out;
 }
 
+// Length of the common prefix of a[0, n) and b[0, n), compared sixteen
+// entries at a time (the or-reduction vectorises).
+int64_t common_prefix(const int32_t* a, const int32_t* b, int64_t n) {
+  int64_t k = 0;
+  for (; k + 16 <= n; k += 16) {
+    int32_t d = 0;
+    for (int i = 0; i < 16; ++i) d |= a[k + i] ^ b[k + i];
+    if (d) break;
+  }
+  while (k < n && a[k] == b[k]) ++k;
+  return k;
+}
+
 // Interleave per-XCD queues of units into dispatch order: unit slot b goes to
 // queue b % kXcds while it has units, else to the longest remaining queue.
 template <class U>
@@ -91,8 +104,8 @@ std::vector<U> interleave(const std::vector<std::vector<U>>& queues) {
   size_t total = 0;
   for (auto& q : queues) total += q.size();
   out.reserve(total);
-  for (size_t b = 0; b < total; ++b) {
-    size_t q = b % queues.size();
+  for (size_t b = 0, slot = 0; b < total; ++b, slot = slot + 1 == queues.size() ? 0 : slot + 1) {
+    size_t q = slot;
     if (pos[q] >= queues[q].size()) {
       size_t best = q;
       size_t left = 0;
@@ -151,16 +164,19 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   }
   const int32_t total_q = n_seqs > 0 ? cu_seqlens_q[n_seqs] : 0;
 
-  std::vector<std::array<int32_t, pa::kGroupWords>> groups;
-  std::vector<int32_t> members;  // cascade member tables, (sequence, partial base) pairs
-  int64_t partial_rows = 0;
-  std::vector<Rec> shared, tiles;
-  // Row-item workgroups in dispatch order, as (kv-head, index of the group's
-  // first item in that head's longest-first order); records are written once,
-  // straight into the plan.
-  std::vector<std::pair<int32_t, int32_t>> quads;
-  std::vector<std::vector<Rec>> head_rows;
-  std::vector<std::vector<int32_t>> head_order;
+  // Items are generated once, as templates for kv-head 0: every kv-head has
+  // the same items, with its own kvh and its own block of partial rows (head
+  // g's partial rows are g * head_partial plus the template's).  Dispatch
+  // lists hold (kv-head, template index) pairs; records are stamped when the
+  // plan is written.
+  using Grp = std::array<int32_t, pa::kGroupWords>;
+  using Ref = std::pair<int32_t, int32_t>;
+  std::vector<Rec> t_shared, t_tiles, t_rows;
+  std::vector<Grp> t_groups;
+  std::vector<int32_t> t_members;  // head 0's member tables: (sequence, partial base) pairs
+  std::vector<Rec> sorted_rows;    // row templates, longest first, padded to whole quads
+  int64_t head_partial = 0;
+  std::vector<Ref> shared, tiles, quads;  // quads: (kv-head, first index into sorted_rows)
 
   if (dtype == PA_BF16) {
     auto qlen = [&](int32_t r) { return cu_seqlens_q[r + 1] - cu_seqlens_q[r]; };
@@ -173,46 +189,44 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
 
     // Cascade groups: few-row sequences with the same first block and
     // q_len whose leading blocks coincide share those keys; attention over
-    // them runs once for all the group's rows.
-    std::vector<int32_t> kstart(n_seqs, 0);       // first private key
-    std::vector<int32_t> cgroup(n_seqs, -1);      // cascade group of a sequence
-    std::vector<std::vector<int32_t>> cg_members;
+    // them runs once for all the group's rows.  Candidates are found by
+    // sorting (first block, q_len, sequence) keys.
+    std::vector<int32_t> kstart(n_seqs, 0);   // first private key
+    std::vector<int32_t> cgroup(n_seqs, -1);  // cascade group of a sequence
+    std::vector<int32_t> cg_seqs;             // members of all groups, group by group
+    std::vector<int32_t> cg_begin{0};         // group c's members start at cg_seqs[cg_begin[c]]
     std::vector<int32_t> cg_keys, cg_chunks;  // shared keys, key chunks (one merge part each)
     if (block_table) {
-      std::unordered_map<int64_t, int32_t> by_key;
-      std::vector<std::vector<int32_t>> cand;
-      for (int32_t r = 0; r < n_seqs; ++r) {
-        if (!is_row(r)) continue;
-        const int64_t key = (int64_t(block_table[int64_t(r) * max_blocks_per_seq]) << 8) | qlen(r);
-        auto it = by_key.find(key);
-        if (it == by_key.end()) {
-          by_key.emplace(key, int32_t(cand.size()));
-          cand.push_back({r});
-        } else {
-          cand[it->second].push_back(r);
-        }
-      }
-      for (auto& mem : cand) {
-        if (mem.size() < 2) continue;
-        const int32_t* b0 = block_table + int64_t(mem[0]) * max_blocks_per_seq;
+      std::vector<std::pair<int64_t, int32_t>> cand;
+      cand.reserve(n_seqs);
+      for (int32_t r = 0; r < n_seqs; ++r)
+        if (is_row(r))
+          cand.push_back({(int64_t(block_table[int64_t(r) * max_blocks_per_seq]) << 8) | qlen(r), r});
+      std::sort(cand.begin(), cand.end());
+      cg_seqs.reserve(cand.size());
+      for (size_t i = 0, j = 0; i < cand.size(); i = j) {
+        for (j = i + 1; j < cand.size() && cand[j].first == cand[i].first;) ++j;
+        if (j - i < 2) continue;
+        const int32_t* b0 = block_table + int64_t(cand[i].second) * max_blocks_per_seq;
         int64_t lcp = max_blocks_per_seq;
         int64_t limit = INT64_MAX;
-        for (int32_t r : mem) {
+        for (size_t m = i; m < j; ++m) {
+          const int32_t r = cand[m].second;
           const int32_t* br = block_table + int64_t(r) * max_blocks_per_seq;
           const int64_t nb = std::min<int64_t>(lcp, cdiv(seq_lens[r], block_size));
-          int64_t k = 0;
-          while (k < nb && br[k] == b0[k]) ++k;
-          lcp = k;
+          lcp = common_prefix(br, b0, nb);
           limit = std::min<int64_t>(limit, seq_lens[r] - qlen(r));
         }
         int64_t S = std::min<int64_t>(lcp * block_size, limit);
         S = S / pa::kTileStep * pa::kTileStep;
         if (S < pa::kSharedMinKeys) continue;
-        for (int32_t r : mem) {
+        for (size_t m = i; m < j; ++m) {
+          const int32_t r = cand[m].second;
           kstart[r] = int32_t(S);
-          cgroup[r] = int32_t(cg_members.size());
+          cgroup[r] = int32_t(cg_keys.size());
+          cg_seqs.push_back(r);
         }
-        cg_members.push_back(mem);
+        cg_begin.push_back(int32_t(cg_seqs.size()));
         cg_keys.push_back(int32_t(S));
         cg_chunks.push_back(int32_t(cdiv(S, pa::kSharedChunk)));
       }
@@ -231,16 +245,15 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     // a row item's block ids fit one wavefront (64 lanes): at most 1024 keys
     chunk = std::min<int64_t>(chunk, int64_t(pa::kRowItemBlocks) * block_size);
 
-    std::vector<std::vector<Rec>> head_tiles(num_kv_heads);
-    head_rows.assign(num_kv_heads, {});
-    std::vector<std::vector<int64_t>> tile_cost(num_kv_heads), row_cost(num_kv_heads);
-    // partial base of (cascade group member, kv-head): member_base[r * Hkv + g]
-    std::vector<int32_t> member_base(cg_members.empty() ? 0 : size_t(n_seqs) * num_kv_heads, -1);
+    std::vector<int64_t> tile_cost, row_cost, shared_cost;
+    // head-0 partial base of a cascade member's merge group
+    std::vector<int32_t> member_base(cg_keys.empty() ? 0 : size_t(n_seqs), -1);
     {
-      // exact per-head item counts, so the lists are allocated once
-      int64_t nt = 0, nr = 0;
+      // exact item counts, so the lists are allocated once
+      int64_t nt = 0, nr = 0, ng = 0;
       for (int32_t r = 0; r < n_seqs; ++r) {
         if (qlen(r) == 0) continue;
+        if (is_row(r)) ng += cdiv(qlen(r) * G, pa::kMergeRows);
         if (is_row(r) && on_tiles(r))
           nt += cdiv(seq_lens[r] - kstart[r], kPrivateTileKeys);
         else if (is_row(r))
@@ -248,16 +261,11 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         else
           nt += cdiv(int64_t(qlen(r)) * G, pa::kTileRows);
       }
-      for (int32_t g = 0; g < num_kv_heads; ++g) {
-        head_tiles[g].reserve(nt);
-        tile_cost[g].reserve(nt);
-        head_rows[g].reserve(nr);
-        row_cost[g].reserve(nr);
-      }
-      int64_t ng = 0;  // merge groups, one per kMergeRows rows of a few-row sequence
-      for (int32_t r = 0; r < n_seqs; ++r)
-        if (is_row(r)) ng += cdiv(qlen(r) * G, pa::kMergeRows);
-      groups.reserve(size_t(ng) * num_kv_heads);
+      t_tiles.reserve(nt);
+      tile_cost.reserve(nt);
+      t_rows.reserve(nr);
+      row_cost.reserve(nr);
+      t_groups.reserve(ng);
     }
     for (int32_t r = 0; r < n_seqs; ++r) {
       const int32_t n = qlen(r);
@@ -277,117 +285,113 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         // parts 0 .. first-1 are the shared prefix's key chunks
         const int32_t first = cgroup[r] >= 0 ? cg_chunks[cgroup[r]] : 0;
         const int32_t parts = used + first;
-        const int32_t nmerge = static_cast<int32_t>(cdiv(rows, pa::kMergeRows));
-        for (int32_t g = 0; g < num_kv_heads; ++g) {
-          int64_t base = -1;
-          if (parts > 1) {
-            base = partial_rows;
-            partial_rows += int64_t(parts) * rows;
-            for (int32_t gi = 0; gi < nmerge; ++gi) {
-              const int32_t row0 = gi * pa::kMergeRows;
-              const int32_t nr = std::min(pa::kMergeRows, rows - row0);
-              groups.push_back({r, g, row0, nr, parts, int32_t(base + row0), rows, 0});
-            }
-            if (first) member_base[size_t(r) * num_kv_heads + g] = int32_t(base);
+        int64_t base = -1;
+        if (parts > 1) {
+          base = head_partial;
+          head_partial += int64_t(parts) * rows;
+          for (int32_t row0 = 0; row0 < rows; row0 += pa::kMergeRows) {
+            const int32_t nr = std::min(pa::kMergeRows, rows - row0);
+            t_groups.push_back({r, 0, row0, nr, parts, int32_t(base + row0), rows, 0});
           }
-          // per split, the row pieces back to back
-          for (int32_t sp = 0; sp < used; ++sp) {
-            const int64_t k0 = k0s + sp * per, k1 = std::min<int64_t>(L, k0s + (sp + 1) * per);
-            if (tiled) {
-              const int32_t part = base < 0 ? -1 : int32_t(base + int64_t(sp + first) * rows);
-              head_tiles[g].push_back({r, g, 0, rows, int32_t(k0), int32_t(k1), part, 0});
-              tile_cost[g].push_back((k1 - k0) * rows);
-              continue;
-            }
-            const int32_t part = base < 0 ? -1 : int32_t(base + int64_t(sp + first) * rows);
-            head_rows[g].push_back({r, g, 0, rows, int32_t(k0), int32_t(k1), part, 0});
-            row_cost[g].push_back(k1 - k0);
+          if (first) member_base[r] = int32_t(base);
+        }
+        // per split, the row pieces back to back
+        for (int32_t sp = 0; sp < used; ++sp) {
+          const int64_t k0 = k0s + sp * per, k1 = std::min<int64_t>(L, k0s + (sp + 1) * per);
+          const int32_t part = base < 0 ? -1 : int32_t(base + int64_t(sp + first) * rows);
+          if (tiled) {
+            t_tiles.push_back({r, 0, 0, rows, int32_t(k0), int32_t(k1), part, 0});
+            tile_cost.push_back((k1 - k0) * rows);
+          } else {
+            t_rows.push_back({r, 0, 0, rows, int32_t(k0), int32_t(k1), part, 0});
+            row_cost.push_back(k1 - k0);
           }
         }
       } else {
-        const int32_t ntiles = static_cast<int32_t>(cdiv(rows, pa::kTileRows));
-        for (int32_t g = 0; g < num_kv_heads; ++g) {
-          for (int32_t t = 0; t < ntiles; ++t) {
-            const int32_t row0 = t * pa::kTileRows;
-            const int32_t nrows = std::min(pa::kTileRows, rows - row0);
-            const int32_t last_q = (row0 + nrows - 1) / G;
-            const int32_t kv1 = L - n + last_q + 1;
-            head_tiles[g].push_back({r, g, row0, nrows, 0, kv1, -1, 0});
-            tile_cost[g].push_back(int64_t(kv1) * nrows);
-          }
+        for (int32_t row0 = 0; row0 < rows; row0 += pa::kTileRows) {
+          const int32_t nrows = std::min(pa::kTileRows, rows - row0);
+          const int32_t last_q = (row0 + nrows - 1) / G;
+          const int32_t kv1 = L - n + last_q + 1;
+          t_tiles.push_back({r, 0, row0, nrows, 0, kv1, -1, 0});
+          tile_cost.push_back(int64_t(kv1) * nrows);
         }
       }
     }
-    // Shared-prefix items: per cascade group and kv-head, a member table and
-    // 128-row tiles of the gathered rows over key chunks of the shared keys.
-    std::vector<std::vector<Rec>> head_shared(num_kv_heads);
-    std::vector<std::vector<int64_t>> shared_cost(num_kv_heads);
-    for (size_t cg = 0; cg < cg_members.size(); ++cg) {
-      const auto& mem = cg_members[cg];
+    // Shared-prefix items: per cascade group, a member table and 128-row
+    // tiles of the gathered rows over key chunks of the shared keys.
+    for (size_t cg = 0; cg < cg_keys.size(); ++cg) {
+      const int32_t* mem = cg_seqs.data() + cg_begin[cg];
+      const int32_t nmem = cg_begin[cg + 1] - cg_begin[cg];
       const int32_t S = cg_keys[cg];
       const int32_t rpm = qlen(mem[0]) * G;
-      const int64_t total_rows = int64_t(rpm) * mem.size();
+      const int64_t total_rows = int64_t(rpm) * nmem;
       const int32_t nch = cg_chunks[cg];
       // chunk boundaries on the tile step; every chunk is non-empty because
       // S / nch >= kSharedChunk / 2 > kTileStep
       auto bound = [&](int64_t c) {
         return c >= nch ? int64_t(S) : (c * S / nch) / pa::kTileStep * pa::kTileStep;
       };
-      for (int32_t g = 0; g < num_kv_heads; ++g) {
-        for (int32_t ch = 0; ch < nch; ++ch) {
-          const int64_t k0 = bound(ch), k1 = bound(ch + 1);
-          // member table of this chunk: (sequence, partial row of its row 0)
-          const int32_t off = int32_t(members.size());
-          for (int32_t r : mem) {
-            members.push_back(r);
-            members.push_back(member_base[size_t(r) * num_kv_heads + g] + ch * rpm);
-          }
-          for (int64_t row0 = 0; row0 < total_rows; row0 += pa::kTileRows) {
-            const int32_t nrows = int32_t(std::min<int64_t>(pa::kTileRows, total_rows - row0));
-            head_shared[g].push_back({off, g, int32_t(row0), nrows, int32_t(k0), int32_t(k1), rpm,
-                                      mem[0]});
-            shared_cost[g].push_back((k1 - k0) * nrows);
-          }
+      for (int32_t ch = 0; ch < nch; ++ch) {
+        const int64_t k0 = bound(ch), k1 = bound(ch + 1);
+        // member table of this chunk: (sequence, partial row of its row 0)
+        const int32_t off = int32_t(t_members.size());
+        for (int32_t m = 0; m < nmem; ++m) {
+          t_members.push_back(mem[m]);
+          t_members.push_back(member_base[mem[m]] + ch * rpm);
+        }
+        for (int64_t row0 = 0; row0 < total_rows; row0 += pa::kTileRows) {
+          const int32_t nrows = int32_t(std::min<int64_t>(pa::kTileRows, total_rows - row0));
+          t_shared.push_back({off, 0, int32_t(row0), nrows, int32_t(k0), int32_t(k1), rpm, mem[0]});
+          shared_cost.push_back((k1 - k0) * nrows);
         }
       }
     }
     // Shared and tile items: per head, longest first, dealt round robin to the
     // head's XCD queues (which stay longest first).
-    auto deal = [&](std::vector<std::vector<Rec>>& lists, std::vector<std::vector<int64_t>>& costs) {
-      std::vector<std::vector<Rec>> q(kXcds);
+    std::vector<std::vector<int>> xs_of(num_kv_heads);
+    for (int32_t g = 0; g < num_kv_heads; ++g) xs_of[g] = xcds_of_head(g, num_kv_heads);
+    auto deal = [&](const std::vector<int64_t>& costs) {
+      const auto ord = order_longest_first(costs);
+      std::vector<std::vector<Ref>> q(kXcds);
+      for (auto& x : q) x.reserve(ord.size() * num_kv_heads / kXcds + ord.size());
       for (int32_t g = 0; g < num_kv_heads; ++g) {
-        const auto xs = xcds_of_head(g, num_kv_heads);
-        const auto ord = order_longest_first(costs[g]);
-        for (size_t i = 0; i < ord.size(); ++i) q[xs[i % xs.size()]].push_back(lists[g][ord[i]]);
+        const auto& xs = xs_of[g];
+        for (size_t i = 0, x = 0; i < ord.size(); ++i, x = x + 1 == xs.size() ? 0 : x + 1)
+          q[xs[x]].push_back({g, ord[i]});
       }
-      return q;
+      return interleave(q);
     };
-    const auto shared_q = deal(head_shared, shared_cost);
-    const auto tile_q = deal(head_tiles, tile_cost);
+    shared = deal(shared_cost);
+    tiles = deal(tile_cost);
     // Row items: per head, longest first, four to a workgroup (padded with
     // empty items) so a workgroup's waves share one kv-head.
-    std::vector<std::vector<std::pair<int32_t, int32_t>>> quad_q(kXcds);
-    head_order.resize(num_kv_heads);
-    for (int32_t g = 0; g < num_kv_heads; ++g) {
-      const auto xs = xcds_of_head(g, num_kv_heads);
-      head_order[g] = order_longest_first(row_cost[g]);
-      const int32_t nq = int32_t(cdiv(int64_t(head_order[g].size()), 4));
-      for (auto x : xs) quad_q[x].reserve(quad_q[x].size() + size_t(nq) / xs.size() + 1);
-      for (int32_t q = 0; q < nq; ++q) quad_q[xs[q % xs.size()]].push_back({g, 4 * q});
+    {
+      const auto ord = order_longest_first(row_cost);
+      sorted_rows.reserve(cdiv(int64_t(ord.size()), 4) * 4);
+      for (int32_t i : ord) sorted_rows.push_back(t_rows[i]);
+      while (sorted_rows.size() % 4) sorted_rows.push_back({-1, 0, 0, 0, 0, 0, -1, 0});
     }
-    shared = interleave(shared_q);
-    tiles = interleave(tile_q);
+    const int32_t nq = int32_t(sorted_rows.size() / 4);
+    std::vector<std::vector<Ref>> quad_q(kXcds);
+    for (auto& x : quad_q) x.reserve(size_t(nq) * num_kv_heads / kXcds + nq);
+    for (int32_t g = 0; g < num_kv_heads; ++g) {
+      const auto& xs = xs_of[g];
+      for (size_t q = 0, x = 0; q < size_t(nq); ++q, x = x + 1 == xs.size() ? 0 : x + 1)
+        quad_q[xs[x]].push_back({g, int32_t(4 * q)});
+    }
     quads = interleave(quad_q);
   }
 
+  const int64_t partial_rows = head_partial * num_kv_heads;
   const int64_t n_row = int64_t(quads.size()) * 4;
-  const int64_t n_groups = int64_t(groups.size());
+  const int64_t n_groups = int64_t(t_groups.size()) * num_kv_heads;
+  const int64_t head_members = int64_t(t_members.size());
   const int64_t shared_off = pa::kHeaderWords;
   const int64_t tile_off = shared_off + int64_t(shared.size()) * pa::kSharedWords;
   const int64_t row_off = tile_off + int64_t(tiles.size()) * pa::kItemWords;
   const int64_t group_off = row_off + n_row * pa::kItemWords;
   const int64_t member_off = group_off + n_groups * pa::kGroupWords;
-  const int64_t words = member_off + int64_t(members.size());
+  const int64_t words = member_off + head_members * num_kv_heads;
   const int64_t grid = dtype == PA_F32 ? int64_t(total_q) * num_q_heads
                                        : int64_t(shared.size() + tiles.size() + quads.size());
   if (words >= (int64_t{1} << 31) || grid >= (int64_t{1} << 31) || partial_rows >= (int64_t{1} << 31))
@@ -400,11 +404,10 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   info->n_row_items = int32_t(n_row);
   info->n_groups = int32_t(n_groups);
   info->n_merge_rows = 0;
-  for (auto& g : groups) info->n_merge_rows += g[pa::G_NROWS];
+  for (const auto& g : t_groups) info->n_merge_rows += int64_t(g[pa::G_NROWS]) * num_kv_heads;
   info->grid = int32_t(grid);
   bool wide = false;
-  for (const auto& rows : head_rows)
-    for (const auto& it : rows) wide = wide || it[pa::I_NROWS] > 16;
+  for (const auto& it : t_rows) wide = wide || it[pa::I_NROWS] > 16;
   info->variant = dtype == PA_F32 ? 0 : (pa::kVariantBf16 | (wide ? pa::kVariantWideRows : 0));
   info->plan_words = words;
   info->workspace_bytes = partial_rows * int64_t(head_dim + 1) * int64_t(sizeof(float));
@@ -432,23 +435,43 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   h[pa::H_GROUP_OFF] = int32_t(group_off);
   h[pa::H_MEMBER_OFF] = int32_t(member_off);
   h[pa::H_PARTIAL_ROWS] = int32_t(partial_rows);
+  // an item template stamped for kv-head g (empty slots stay as they are);
+  // partial rows fit int32 (checked above)
+  auto put_item = [&](int32_t* q, const Rec& t, int32_t g) {
+    const bool live = t[pa::I_SEQ] >= 0;
+    const int32_t part = t[pa::I_PART];
+    std::copy(t.begin(), t.end(), q);
+    q[pa::I_KVH] = live ? g : t[pa::I_KVH];
+    q[pa::I_PART] = live && part >= 0 ? part + int32_t(g * head_partial) : part;
+  };
   int32_t* p = plan + shared_off;
-  for (auto& it : shared) {
-    Rec w = it;
-    w[pa::S_MEMBERS] += int32_t(member_off);  // absolute word offset of the member table
-    p = std::copy(w.begin(), w.end(), p);
+  for (const auto& [g, i] : shared) {
+    const Rec& t = t_shared[i];
+    std::copy(t.begin(), t.end(), p);
+    p[pa::S_KVH] = g;
+    // absolute word offset of head g's copy of the member table
+    p[pa::S_MEMBERS] = int32_t(member_off + g * head_members + t[pa::S_MEMBERS]);
+    p += pa::kSharedWords;
   }
-  for (auto& it : tiles) p = std::copy(it.begin(), it.end(), p);
-  const Rec empty = {-1, 0, 0, 0, 0, 0, -1, 0};
-  for (const auto& q : quads) {
-    const auto& ord = head_order[q.first];
-    for (int32_t k = 0; k < 4; ++k) {
-      const size_t i = size_t(q.second) + k;
-      const Rec& it = i < ord.size() ? head_rows[q.first][ord[i]] : empty;
-      p = std::copy(it.begin(), it.end(), p);
-    }
+  for (const auto& [g, i] : tiles) {
+    put_item(p, t_tiles[i], g);
+    p += pa::kItemWords;
   }
-  for (auto& g : groups) p = std::copy(g.begin(), g.end(), p);
-  std::copy(members.begin(), members.end(), p);
+  for (const auto& [g, q0] : quads)
+    for (int32_t k = 0; k < 4; ++k, p += pa::kItemWords) put_item(p, sorted_rows[q0 + k], g);
+  if (dtype == PA_BF16) {
+    for (int32_t g = 0; g < num_kv_heads; ++g)
+      for (const auto& t : t_groups) {
+        std::copy(t.begin(), t.end(), p);
+        p[pa::G_KVH] = g;
+        p[pa::G_PART] = int32_t(t[pa::G_PART] + g * head_partial);
+        p += pa::kGroupWords;
+      }
+    for (int32_t g = 0; g < num_kv_heads; ++g)
+      for (int64_t m = 0; m < head_members; m += 2) {
+        *p++ = t_members[m];
+        *p++ = int32_t(t_members[m + 1] + g * head_partial);
+      }
+  }
   return PA_OK;
 }

@@ -49,24 +49,32 @@ def batch_ops(ops):
 
 
 class Staging:
-    """Pinned host buffers and device buffers for one launch's metadata and
-    plan.  The host fills the pinned buffers while the GPU still works on an
-    earlier launch; ``ready`` (recorded after the copies) guards reuse."""
+    """One pinned host buffer and one device buffer holding a launch's
+    metadata and plan ([seq_lens | cu_seqlens_q | block_table | slot_mapping |
+    plan], int32), uploaded with a single asynchronous copy on the compute
+    stream, so stream order puts it after the kernels of the launch that used
+    the device buffer before.  The host fills the pinned buffer while the GPU
+    still works on an earlier launch; ``ready`` (recorded after the copy)
+    guards reuse of the host buffer."""
 
     def __init__(self, device, n_seqs, max_blocks, max_tokens, plan_words):
-        def pair(n):
-            h = torch.empty(max(1, n), dtype=torch.int32, pin_memory=True)
-            return h, torch.empty(max(1, n), dtype=torch.int32, device=device)
         self.n_seqs, self.max_blocks = n_seqs, max_blocks
-        self.bt = pair(n_seqs * max_blocks)
-        self.sl = pair(n_seqs)
-        self.cu = pair(n_seqs + 1)
-        self.slots = pair(max_tokens)
-        self.plan = pair(plan_words)
-        self.ready = None
+        sizes = [("sl", n_seqs), ("cu", n_seqs + 1), ("bt", n_seqs * max_blocks),
+                 ("slots", max_tokens), ("plan", plan_words)]
+        total = sum(max(1, n) for _, n in sizes)
+        self.host = torch.empty(total, dtype=torch.int32, pin_memory=True)
+        self.dev = torch.empty(total, dtype=torch.int32, device=device)
+        off = 0
+        for name, n in sizes:
+            m = max(1, n)
+            setattr(self, name, (self.host[off:off + m], self.dev[off:off + m]))
+            setattr(self, name + "_off", off)
+            off += m
+        self.ready = torch.cuda.Event()
+        self.used = False
 
     def wait(self):
-        if self.ready is not None:
+        if self.used:
             self.ready.synchronize()
 
 
@@ -87,6 +95,7 @@ class DeviceReplay:
         self.num_cus = num_cus
         self.cascade = cascade
         self.n_cached = {}
+        self._ws = None  # split-K workspace of staged launches (all on the current stream)
 
     # -- host ops ------------------------------------------------------------
     def _write_kv(self, seq_id, k: np.ndarray, v: np.ndarray):
@@ -176,9 +185,9 @@ class DeviceReplay:
             n_cached=dict(self.n_cached))
 
     def prepare_staged(self, launch, st: Staging, q, k_new, v_new, out, lse) -> Prepared:
-        """Like ``prepare`` but through preallocated pinned/device buffers with
-        asynchronous copies and batched pool calls, so host bookkeeping
-        overlaps earlier GPU work."""
+        """Like ``prepare`` but through a preallocated pinned/device staging
+        pair, one asynchronous upload and batched pool calls, so host
+        bookkeeping overlaps earlier GPU work."""
         self.n_cached = {}
         self.apply_batched(launch, "pre")
         cfg = self.cfg
@@ -197,15 +206,17 @@ class DeviceReplay:
                             block_table=md["block_table"] if self.cascade else None)
         if info.plan_words > st.plan[0].numel():
             raise RuntimeError("staging plan buffer too small")
-        for (h, d), cnt in ((st.bt, n * st.max_blocks), (st.sl, n), (st.cu, n + 1),
-                            (st.slots, T), (st.plan, int(info.plan_words))):
-            if cnt:
-                d[:cnt].copy_(h[:cnt], non_blocking=True)
-        st.ready = torch.cuda.Event()
+        # one copy: everything up to the end of the plan
+        used = st.plan_off + int(info.plan_words)
+        st.dev[:used].copy_(st.host[:used], non_blocking=True)
         st.ready.record()
+        st.used = True
         ws = None
         if info.workspace_bytes:
-            ws = torch.empty(int(info.workspace_bytes), dtype=torch.uint8, device=self.device)
+            if self._ws is None or self._ws.numel() < int(info.workspace_bytes):
+                self._ws = torch.empty(int(info.workspace_bytes), dtype=torch.uint8,
+                                       device=self.device)
+            ws = self._ws
         return Prepared(
             kind=kind, meta=md, info=info, plan_host=plan,
             block_table=st.bt[1][:n * st.max_blocks].view(n, st.max_blocks),
