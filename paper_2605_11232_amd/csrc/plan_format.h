@@ -72,7 +72,7 @@ constexpr int32_t kRowSeqRows = 64;   // sequences with at most this many rows u
 constexpr int32_t kKeyStep = 32;      // keys per row-item inner iteration
 constexpr int32_t kRowItemBlocks = 64;  // most blocks (of 16 keys) one row item spans
 constexpr int32_t kTileStep = 64;     // keys per tile-item inner iteration
-constexpr int32_t kSharedChunk = 4096;  // most shared keys one cascade item covers
+constexpr int32_t kSharedChunk = 6144;  // most shared keys one cascade item covers
 constexpr int32_t kSharedMinKeys = 256; // shorter shared prefixes are not split off
 
 }  // namespace pa
