@@ -48,6 +48,24 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const T* __restrict__ k_
     st16(&tile[tt][part * E], vx);
   }
   __syncthreads();
+  // The tile's tokens fill one cache block in order (a sequence's run of
+  // new tokens starting on a block boundary): each thread writes eight
+  // tokens of one dimension of V^T as one 16-byte store.
+  const int s0 = slot_sh[0];
+  bool in_order = s0 >= 0 && s0 % kBlock == 0;
+#pragma unroll
+  for (int tt = 1; tt < kBlock; ++tt) in_order = in_order && slot_sh[tt] == s0 + tt;
+  if (in_order) {
+    T* vb = vc + ((int64_t)(s0 / kBlock) * hkv + h) * D * kBlock;
+    for (int c = tid; c < D * (kBlock / E); c += 256) {
+      const int d = c / (kBlock / E), t8 = (c % (kBlock / E)) * E;
+      T w[E];
+#pragma unroll
+      for (int i = 0; i < E; ++i) w[i] = tile[t8 + i][d];
+      st16(vb + d * kBlock + t8, __builtin_bit_cast(u32x4, w));
+    }
+    return;
+  }
   for (int e = tid; e < kBlock * D; e += 256) {
     const int tt = e % kBlock, d = e / kBlock;
     const int s = slot_sh[tt];
