@@ -736,74 +736,76 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_e
 }
 
 // Combine split partial results by log-sum-exp: one workgroup per merge
-// group of at most four rows, one wavefront per row, lanes over the output
-// dims.  The partial outputs of the first 16 parts are requested
-// before the part LSEs are reduced, so a row costs about one memory round
-// trip; parts are combined in split order (deterministic).
+// group of at most four rows, half a wavefront per row (32 lanes over the
+// output dims, 16-byte partial loads).  The partial outputs of up to 16 parts
+// are requested before the part LSEs are reduced, so a row costs about one
+// memory round trip; parts are combined in split order (deterministic).
 template <int D>
-__global__ __launch_bounds__(256) void merge_kernel(AttnArgs a) {
-  constexpr int V = D / 64;  // output dims per lane
-  constexpr int C = 16;      // parts whose loads are in flight together
+__global__ __launch_bounds__(kMergeRows * 32) void merge_kernel(AttnArgs a) {
+  constexpr int VD = D / 32;  // output dims per lane
+  constexpr int C = 16;       // parts whose loads are in flight together
+  typedef float vecf __attribute__((ext_vector_type(VD)));
   const int32_t* gr = a.plan + a.plan[H_GROUP_OFF] + blockIdx.x * kGroupWords;
-  const int lr = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (lr >= gr[G_NROWS]) return;
+  const int lr = threadIdx.x >> 5, lane = threadIdx.x & 31;
+  const int half = threadIdx.x & 32;  // first lane of this row's half wavefront
+  const int nrows = gr[G_NROWS];
+  const bool valid = lr < nrows;
   const int r = gr[G_SEQ], g = gr[G_KVH], row0 = gr[G_ROW0];
   const int nsplit = gr[G_NSPLIT], stride = gr[G_STRIDE];
-  const int64_t prow = (int64_t)gr[G_PART] + lr;  // partial row of split 0
-  auto part_o = [&](int s) { return a.ws_o + (prow + (int64_t)s * stride) * D + lane; };
+  // rows past nrows repeat the group's last row (in bounds) and store nothing
+  const int64_t prow = (int64_t)gr[G_PART] + min(lr, nrows - 1);  // partial row of split 0
+  auto part_o = [&](int s) {
+    return reinterpret_cast<const vecf*>(a.ws_o + (prow + (int64_t)s * stride) * D) + lane;
+  };
   auto part_lse = [&](int s) { return a.ws_lse[prow + (int64_t)s * stride]; };
-  float x[C][V];
+  vecf x[C];
   auto load_batch = [&](int s0) {
 #pragma unroll
-    for (int u = 0; u < C; ++u) {
-      const float* src = part_o(min(s0 + u, nsplit - 1));  // in bounds; weight 0 past the end
-#pragma unroll
-      for (int k = 0; k < V; ++k) x[u][k] = src[64 * k];
-    }
+    for (int u = 0; u < C; ++u)
+      if (s0 + u < nsplit) x[u] = *part_o(s0 + u);
   };
   load_batch(0);
-  // max and sum of exp over the part LSEs, 64 parts per round
+  // max and sum of exp over the part LSEs, 32 parts per round
   const float lse0 = lane < nsplit ? part_lse(lane) : kNegInf;
   float mx = lse0;
-  for (int s = 64 + lane; s - lane < nsplit; s += 64) mx = fmaxf(mx, s < nsplit ? part_lse(s) : kNegInf);
+  for (int s = 32 + lane; s - lane < nsplit; s += 32) mx = fmaxf(mx, s < nsplit ? part_lse(s) : kNegInf);
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-  float o_acc[V];
-#pragma unroll
-  for (int k = 0; k < V; ++k) o_acc[k] = 0.f;
+  for (int o = 16; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  vecf o_acc = {};
   float lse_v = kNegInf;
   if (mx != kNegInf) {
     float sum = lse0 == kNegInf ? 0.f : exp2f((lse0 - mx) * kLog2e);
-    for (int s = 64 + lane; s - lane < nsplit; s += 64)
+    for (int s = 32 + lane; s - lane < nsplit; s += 32)
       if (s < nsplit) sum += exp2f((part_lse(s) - mx) * kLog2e);
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
+    for (int o = 16; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
     lse_v = mx + kLn2 * __log2f(sum);
-    // weight of part s0 + lane of the current round of 64, held by that lane
+    // weight of part s0 + lane of the current round of 32, held by that lane
     float wl = exp2f((lse0 - lse_v) * kLog2e);
     for (int s0 = 0; s0 < nsplit; s0 += C) {
       if (s0 > 0) {
         load_batch(s0);
-        if (s0 % 64 == 0) {
+        if (s0 % 32 == 0) {
           const int s = s0 + lane;
           wl = s < nsplit ? exp2f((part_lse(s) - lse_v) * kLog2e) : 0.f;
         }
       }
 #pragma unroll
-      for (int u = 0; u < C; ++u) {
-        const float wt = s0 + u < nsplit ? __shfl(wl, (s0 + u) & 63, 64) : 0.f;
-#pragma unroll
-        for (int k = 0; k < V; ++k) o_acc[k] = fmaf(wt, x[u][k], o_acc[k]);
-      }
+      for (int u = 0; u < C; ++u)
+        if (s0 + u < nsplit) o_acc += __shfl(wl, half | ((s0 + u) & 31), 64) * x[u];
     }
   }
+  if (!valid) return;
   const int qs = a.cu_q[r];
   const int rho = row0 + lr;
   const int qi = rho / a.group;
   const int hq = g * a.group + (rho - qi * a.group);
-  __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D;
+  __bf16 ob[VD];
 #pragma unroll
-  for (int k = 0; k < V; ++k) op[lane + 64 * k] = (__bf16)o_acc[k];
+  for (int k = 0; k < VD; ++k) ob[k] = (__bf16)o_acc[k];
+  __bf16* op = a.out + ((int64_t)(qs + qi) * a.hq + hq) * D + VD * lane;
+  if constexpr (VD == 4) *reinterpret_cast<u32x2*>(op) = __builtin_bit_cast(u32x2, ob);
+  else *reinterpret_cast<uint32_t*>(op) = __builtin_bit_cast(uint32_t, ob);
   if (a.lse && lane == 0) a.lse[(int64_t)(qs + qi) * a.hq + hq] = lse_v;
 }
 
@@ -859,9 +861,9 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
   }
   if (n_groups > 0) {
     if (d == 128)
-      hipLaunchKernelGGL(merge_kernel<128>, dim3(n_groups), dim3(256), 0, stream, a);
+      hipLaunchKernelGGL(merge_kernel<128>, dim3(n_groups), dim3(kMergeRows * 32), 0, stream, a);
     else
-      hipLaunchKernelGGL(merge_kernel<64>, dim3(n_groups), dim3(256), 0, stream, a);
+      hipLaunchKernelGGL(merge_kernel<64>, dim3(n_groups), dim3(kMergeRows * 32), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return static_cast<int>(e);
   }
