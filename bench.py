@@ -17,6 +17,7 @@ of the same launch, on this host's cores.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -119,8 +120,8 @@ def cpu_baseline(wl, launch, budget_s: float = 12.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="prefill", choices=list(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=0,
@@ -212,12 +213,19 @@ def main():
     meta = p.meta if W else None
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(K)]
+    # no garbage-collector pass inside the timed steps: a full collection of
+    # the interpreter's objects takes milliseconds, several steps' worth
+    gc.collect()
+    gc.freeze()
+    gc.disable()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
         p = step(W + i, events[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    gc.enable()
+    gc.unfreeze()
     meta = {k: np.array(v, copy=True) for k, v in p.meta.items()}
     per_ms = [a.elapsed_time(b) for a, b in events]
     attn_ms = float(np.mean(per_ms))
