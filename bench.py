@@ -150,7 +150,7 @@ def main():
         print(json.dumps({"copy_bytes": n, "launches": 5}), flush=True)
         return
     from paper_2605_11232_amd import perf, synth
-    from paper_2605_11232_amd.runtime import DeviceReplay, Staging
+    from paper_2605_11232_amd.runtime import DeviceReplay, Staging, plan_words_bound
 
     torch.cuda.set_device(0)
     name = args.workload
@@ -163,9 +163,9 @@ def main():
     dev = DeviceReplay(wl).setup()
     launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K + C)]
     # pack each step's token batches (input marshalling) before timing
-    from paper_2605_11232_amd.runtime import batch_ops
+    from paper_2605_11232_amd.runtime import marshal_launch
     for ln in launches:
-        ln.__dict__["_batched"] = {"pre": batch_ops(ln.pre), "post": batch_ops(ln.post)}
+        marshal_launch(ln)
     L0 = launches[0]
     T = L0.total_q
     tdt = dev.tdtype
@@ -175,11 +175,7 @@ def main():
     out = torch.empty((T, cfg.num_q_heads, cfg.head_dim), dtype=tdt, device="cuda")
     lse = torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device="cuda")
     n = len(L0.seq_ids)
-    # plan size bound: tile items + single-wave items (key splits of >= 256) +
-    # split groups, plus per-XCD padding
-    max_keys = wl.max_blocks_per_seq * cfg.block_size
-    plan_words = 32 + 8 * (cfg.num_kv_heads * (T * cfg.group // 128 + n)
-                           + 2 * cfg.num_kv_heads * n * (max_keys // 256 + 2) + 64)
+    plan_words = plan_words_bound(cfg, n, T, wl.max_blocks_per_seq)
     stagings = [Staging("cuda", n, wl.max_blocks_per_seq, T, plan_words) for _ in range(2)]
     stream = torch.cuda.current_stream()
 

@@ -281,6 +281,32 @@ int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int32_t* seq_l
                  int32_t head_dim, int32_t block_size, int32_t dtype, int32_t num_cus,
                  int32_t* plan, int64_t plan_capacity, pa_plan_info* info);
 
+/* The host side of one serving step's launch in one call (paper: Section 2,
+ * block tables and Automatic Prefix Caching; Section 5.2, one batched launch
+ * per step): exactly
+ *   pa_pool_apply(pool, n_ops, ops, op_seq_ids, op_token_offsets, op_tokens,
+ *                 op_new_lens, op_n_cached, NULL)          (skipped if n_ops == 0)
+ *   pa_build_metadata(pool, n_seqs, seq_ids, q_lens, max_blocks_per_seq,
+ *                     block_table, seq_lens, cu_seqlens_q, slot_mapping,
+ *                     slot_capacity)
+ *   pa_attn_plan(kind, n_q, n_seqs, seq_lens, cu_seqlens_q,
+ *                shared_prefix ? block_table : NULL, max_blocks_per_seq,
+ *                num_q_heads, num_kv_heads, head_dim, <the pool's block size>,
+ *                dtype, num_cus, plan, plan_capacity, info)
+ * with the arguments, layouts, ownership (all host, caller-owned) and error
+ * behaviour of those three functions.  It stops at the first failing step
+ * and returns its code: pool operations already applied stay applied (as
+ * pa_pool_apply documents); outputs of later steps are not written. */
+int pa_prepare_launch(pa_pool* pool, int32_t n_ops, const int32_t* ops,
+                      const int64_t* op_seq_ids, const int32_t* op_token_offsets,
+                      const int32_t* op_tokens, const int32_t* op_new_lens, int32_t* op_n_cached,
+                      int32_t n_seqs, const int64_t* seq_ids, const int32_t* q_lens,
+                      int32_t max_blocks_per_seq, int32_t* block_table, int32_t* seq_lens,
+                      int32_t* cu_seqlens_q, int32_t* slot_mapping, int64_t slot_capacity,
+                      int32_t kind, int32_t n_q, int32_t num_q_heads, int32_t num_kv_heads,
+                      int32_t head_dim, int32_t dtype, int32_t num_cus, int32_t shared_prefix,
+                      int32_t* plan, int64_t plan_capacity, pa_plan_info* info);
+
 /* ------------------------------------------------------------------------ *
  * Device operations.                                                         *
  * ------------------------------------------------------------------------ */

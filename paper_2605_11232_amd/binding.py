@@ -28,7 +28,7 @@ EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy
            "pa_seqs_truncate", "pa_seqs_free", "pa_pool_apply", "pa_seq_len", "pa_seq_blocks",
            "pa_pool_free_list", "pa_build_metadata", "pa_attn_plan", "pa_kv_append",
            "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify", "pa_pool_set_eviction",
-           "pa_pool_get_stats", "pa_pool_kv_waste", "pa_form_batches"]
+           "pa_pool_get_stats", "pa_pool_kv_waste", "pa_form_batches", "pa_prepare_launch"]
 
 
 class PaError(RuntimeError):
@@ -86,7 +86,7 @@ def lib():
         "pa_seqs_extend": (C.c_int, [_P, i32, _I64P, _I32P, _I32P, _I32P]),
         "pa_seqs_truncate": (C.c_int, [_P, i32, _I64P, _I32P, _I32P]),
         "pa_seqs_free": (C.c_int, [_P, i32, _I64P, _I32P]),
-        "pa_pool_apply": (C.c_int, [_P, i32, _I32P, _I64P, _I32P, _I32P, _I32P, _I32P, _I32P]),
+        "pa_pool_apply": (C.c_int, [_P, i32, _P, _P, _P, _P, _P, _P, _P]),
         "pa_seq_len": (C.c_int, [_P, i64, _I32P]),
         "pa_seq_blocks": (C.c_int, [_P, i64, _I32P, i32, _I32P]),
         "pa_pool_free_list": (C.c_int, [_P, _I32P, i32, _I32P]),
@@ -99,6 +99,9 @@ def lib():
         "pa_pool_kv_waste": (C.c_int, [_P, i32, C.POINTER(KvWaste)]),
         "pa_form_batches": (C.c_int, [i32, _I32P, _I32P, i32, _I32P, _I32P, _I32P, _I32P, _I32P,
                                       _I32P, _I32P]),
+        "pa_prepare_launch": (C.c_int, [_P, i32, _P, _P, _P, _P, _P, _P, i32, _P, _P, i32, _P, _P,
+                                        _P, _P, i64, i32, i32, i32, i32, i32, i32, i32, i32, _P,
+                                        i64, C.POINTER(PlanInfo)]),
     }
     attn = (C.c_int, [_P, _P, _P, i32, _P, i32, _P, _P, i32, i32, i32, i32, i32, i32, f32, i32, _P,
                       C.POINTER(PlanInfo), _P, C.c_size_t, _P, _P, _P])
@@ -123,6 +126,77 @@ def _i32(a) -> np.ndarray:
 
 def _ptr(a: np.ndarray, ctype=C.c_int32):
     return a.ctypes.data_as(C.POINTER(ctype))
+
+
+def _addr(a) -> int:
+    """Address of a numpy array's data (0 for None or an empty array)."""
+    return 0 if a is None or a.size == 0 else a.ctypes.data
+
+
+class PackedOps:
+    """A step's pool operations as pa_pool_apply takes them (ops, seq_ids,
+    token_offsets, tokens, new_lens), plus the n_cached output array, with
+    their addresses taken once so that repeated calls marshal nothing."""
+
+    def __init__(self, ops, seq_ids, offsets, tokens, new_lens):
+        self.ops = _i32(ops)
+        self.seq_ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
+        self.offsets = _i32(offsets)
+        self.tokens = _i32(tokens)
+        self.new_lens = _i32(new_lens)
+        self.n = int(self.ops.size)
+        if not (self.seq_ids.size == self.n and self.offsets.size == self.n + 1
+                and self.new_lens.size == self.n):
+            raise ValueError("PackedOps: arrays of inconsistent length")
+        self.n_cached = np.zeros(max(1, self.n), np.int32)
+        self.addrs = (_addr(self.ops), _addr(self.seq_ids), _addr(self.offsets),
+                      _addr(self.tokens), _addr(self.new_lens), _addr(self.n_cached))
+        self.add_rows = np.flatnonzero(self.ops == OP_ADD)
+        self.add_ids = self.seq_ids[self.add_rows].tolist()
+
+    def admitted(self) -> dict:
+        """{seq_id: reused tokens} of the admissions of the last application."""
+        return dict(zip(self.add_ids, self.n_cached[self.add_rows].tolist())) if self.add_ids else {}
+
+
+class LaunchInputs:
+    """One launch's sequence ids (int64) and query lengths (int32), with
+    their addresses taken once."""
+
+    def __init__(self, seq_ids, q_lens):
+        self.seq_ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
+        self.q_lens = _i32(q_lens)
+        if self.seq_ids.size != self.q_lens.size:
+            raise ValueError("LaunchInputs: seq_ids and q_lens differ in length")
+        self.n = int(self.seq_ids.size)
+        self.total_q = int(self.q_lens.sum()) if self.n else 0
+        self.addrs = (_addr(self.seq_ids), _addr(self.q_lens))
+
+
+class LaunchBuffers:
+    """Caller-owned host int32 arrays that launch metadata and plan are
+    written to (e.g. views of one pinned staging buffer): block_table
+    [rows, max_blocks], seq_lens [rows], cu_seqlens_q [rows + 1],
+    slot_mapping [tokens], plan [words]; addresses taken once."""
+
+    def __init__(self, block_table, seq_lens, cu_seqlens_q, slot_mapping, plan):
+        arrs = (block_table, seq_lens, cu_seqlens_q, slot_mapping, plan)
+        for a in arrs:
+            if a.dtype != np.int32 or not a.flags["C_CONTIGUOUS"]:
+                raise ValueError("LaunchBuffers: arrays must be contiguous int32")
+        if block_table.ndim != 2 or seq_lens.size != block_table.shape[0] or \
+                cu_seqlens_q.size < seq_lens.size + 1:
+            raise ValueError("LaunchBuffers: inconsistent shapes")
+        self.block_table, self.seq_lens, self.cu_seqlens_q, self.slot_mapping, self.plan = arrs
+        self.rows, self.max_blocks = (int(x) for x in block_table.shape)
+        # slot_mapping may be empty; a non-null address is passed regardless
+        self.addrs = tuple(a.ctypes.data for a in arrs)
+
+    def meta(self, n: int, total_q: int) -> dict:
+        """Views of the first launch's metadata (as Pool.metadata returns)."""
+        return {"block_table": self.block_table[:n], "seq_lens": self.seq_lens[:n],
+                "cu_seqlens_q": self.cu_seqlens_q[:n + 1],
+                "slot_mapping": self.slot_mapping[:total_q]}
 
 
 class Pool:
@@ -209,11 +283,36 @@ class Pool:
     def apply(self, ops, seq_ids, offsets, tokens, new_lens):
         """Mixed pool operations in one call (arrays as pa_pool_apply takes
         them); returns reused-token counts (int32, 0 for non-admissions)."""
-        out = np.zeros(len(ops), np.int32)
-        _check(self._lib.pa_pool_apply(self._h, len(ops), _ptr(ops), seq_ids.ctypes.data_as(_I64P),
-                                       _ptr(offsets), _ptr(tokens) if tokens.size else None,
-                                       _ptr(new_lens), _ptr(out), None))
-        return out
+        p = PackedOps(ops, seq_ids, offsets, tokens, new_lens)
+        return self.apply_packed(p).copy()
+
+    def apply_packed(self, p: PackedOps):
+        """pa_pool_apply on pre-packed operations; returns p's n_cached view."""
+        if p.n:
+            _check(self._lib.pa_pool_apply(self._h, p.n, *p.addrs, None))
+        return p.n_cached[:p.n]
+
+    def prepare_launch(self, ops, inp: LaunchInputs, buf: LaunchBuffers, kind: int, n_q: int,
+                       num_q_heads: int, num_kv_heads: int, head_dim: int, dtype: int,
+                       num_cus: int = 0, shared_prefix: bool = True, info=None):
+        """pa_prepare_launch: ``ops`` (PackedOps or None) applied, then the
+        metadata of ``inp`` and its plan written into ``buf``; returns the
+        PlanInfo (``info`` is reused when given)."""
+        if inp.n > buf.rows or inp.total_q > buf.slot_mapping.size:
+            raise ValueError("prepare_launch: launch larger than its buffers")
+        if info is None:
+            info = PlanInfo()
+        if ops is not None and ops.n:
+            n_ops, oa = ops.n, ops.addrs
+        else:
+            n_ops, oa = 0, (0, 0, 0, 0, 0, 0)
+        bt, sl, cu, sm, pl = buf.addrs
+        _check(self._lib.pa_prepare_launch(
+            self._h, n_ops, *oa, inp.n, *inp.addrs, buf.max_blocks, bt, sl, cu, sm,
+            buf.slot_mapping.size, int(kind), int(n_q), int(num_q_heads), int(num_kv_heads),
+            int(head_dim), int(dtype), int(num_cus), 1 if shared_prefix else 0, pl,
+            buf.plan.size, C.byref(info)))
+        return info
 
     def seq_len(self, seq_id: int) -> int:
         n = C.c_int32(0)

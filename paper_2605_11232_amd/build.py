@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libpa.so")
 
 HIP_SOURCES = ["attn_bf16.hip", "attn_f32.hip", "kv_append.hip", "api.hip"]
-HOST_SOURCES = ["pool.cpp", "plan.cpp", "batch.cpp", "errors.cpp"]
+HOST_SOURCES = ["pool.cpp", "plan.cpp", "batch.cpp", "step.cpp", "errors.cpp"]
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -13,4 +13,7 @@ namespace pa {
 int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 void clear_error();
 
+// Tokens per block of a pool (the pool must not be NULL).
+int32_t pool_block_size(const pa_pool* pool);
+
 }  // namespace pa

@@ -178,6 +178,10 @@ struct pa_pool {
   }
 };
 
+namespace pa {
+int32_t pool_block_size(const pa_pool* pool) { return pool->bs; }
+}  // namespace pa
+
 extern "C" {
 
 int pa_pool_create(int32_t num_blocks, int32_t block_size, const int32_t* free_order,

@@ -29,7 +29,7 @@ class Prepared:
 _OPCODE = {"add": B.OP_ADD, "extend": B.OP_EXTEND, "truncate": B.OP_TRUNCATE, "free": B.OP_FREE}
 
 
-def batch_ops(ops):
+def batch_ops(ops) -> B.PackedOps:
     """Pack a list of pool ops into the arrays of one pa_pool_apply call
     (write_kv ops, which only occur in setup, are kept apart)."""
     pool_ops = [op for op in ops if op.kind != "write_kv"]
@@ -45,7 +45,27 @@ def batch_ops(ops):
     toks = [op.tokens for op in pool_ops if op.tokens is not None and len(op.tokens)]
     toks = np.concatenate(toks).astype(np.int32) if toks else np.zeros(0, np.int32)
     new_lens = np.array([op.n if op.kind == "truncate" else 0 for op in pool_ops], dtype=np.int32)
-    return codes, ids, off, toks, new_lens
+    return B.PackedOps(codes, ids, off, toks, new_lens)
+
+
+def marshal_launch(launch):
+    """Pack a launch's pool operations and its (seq_ids, q_lens) once, as
+    the staged path passes them to the library (cached on the launch)."""
+    d = launch.__dict__
+    if "_batched" not in d:
+        d["_batched"] = {"pre": batch_ops(launch.pre), "post": batch_ops(launch.post)}
+    if "_inputs" not in d:
+        d["_inputs"] = B.LaunchInputs(launch.seq_ids, launch.q_lens)
+    return d["_batched"], d["_inputs"]
+
+
+def plan_words_bound(cfg, n_seqs: int, total_q: int, max_blocks_per_seq: int) -> int:
+    """Upper bound on the plan size of a launch of n_seqs sequences and
+    total_q query tokens (tile items, key-split items of at least 256 keys,
+    merge groups, cascade member tables, per-XCD padding)."""
+    max_keys = max_blocks_per_seq * cfg.block_size
+    return 32 + 8 * (cfg.num_kv_heads * (total_q * cfg.group // 128 + n_seqs)
+                     + 2 * cfg.num_kv_heads * n_seqs * (max_keys // 256 + 2) + 64)
 
 
 class Staging:
@@ -72,6 +92,22 @@ class Staging:
             off += m
         self.ready = torch.cuda.Event()
         self.used = False
+        # host views the library writes into, and device views by launch shape
+        self.buffers = B.LaunchBuffers(self.bt[0].numpy().reshape(n_seqs, max_blocks),
+                                       self.sl[0].numpy(), self.cu[0].numpy(),
+                                       self.slots[0].numpy(), self.plan[0].numpy())
+        self.info = B.PlanInfo()
+        self._views = {}
+
+    def device_views(self, n, total_q):
+        """(block_table [n, max_blocks], seq_lens, cu_seqlens_q, slot_mapping)
+        views of the device buffer for a launch of n sequences."""
+        key = (n, total_q)
+        v = self._views.get(key)
+        if v is None:
+            v = self._views[key] = (self.bt[1][:n * self.max_blocks].view(n, self.max_blocks),
+                                    self.sl[1][:n], self.cu[1][:n + 1], self.slots[1][:total_q])
+        return v
 
     def wait(self):
         if self.used:
@@ -123,16 +159,11 @@ class DeviceReplay:
 
     def apply_batched(self, launch, which: str):
         """Apply the launch's pre or post pool ops in one library call."""
-        cache = launch.__dict__.setdefault("_batched", {})
-        if which not in cache:
-            cache[which] = batch_ops(getattr(launch, which))
-        codes, ids, off, toks, new_lens = cache[which]
-        if len(codes) == 0:
+        packed = marshal_launch(launch)[0][which]
+        if packed.n == 0:
             return
-        hits = self.pool.apply(codes, ids, off, toks, new_lens)
-        added = codes == B.OP_ADD
-        if added.any():
-            self.n_cached.update(zip(ids[added].tolist(), hits[added].tolist()))
+        self.pool.apply_packed(packed)
+        self.n_cached.update(packed.admitted())
 
     def setup(self):
         for op in self.wl.setup:
@@ -186,26 +217,20 @@ class DeviceReplay:
 
     def prepare_staged(self, launch, st: Staging, q, k_new, v_new, out, lse) -> Prepared:
         """Like ``prepare`` but through a preallocated pinned/device staging
-        pair, one asynchronous upload and batched pool calls, so host
-        bookkeeping overlaps earlier GPU work."""
-        self.n_cached = {}
-        self.apply_batched(launch, "pre")
+        pair: one library call applies the launch's pool operations and
+        writes its metadata and plan into the pinned buffer, one
+        asynchronous copy uploads them, so host bookkeeping overlaps earlier
+        GPU work."""
+        batched, inp = marshal_launch(launch)
         cfg = self.cfg
-        n = len(launch.seq_ids)
-        T = launch.total_q
-        st.wait()
-        hv = {"block_table": st.bt[0][:n * st.max_blocks].numpy().reshape(n, st.max_blocks),
-              "seq_lens": st.sl[0][:n].numpy(), "cu_seqlens_q": st.cu[0][:n + 1].numpy(),
-              "slot_mapping": st.slots[0][:T].numpy()}
-        md = self.pool.metadata(launch.seq_ids, launch.q_lens, st.max_blocks, out=hv)
+        n, T = inp.n, inp.total_q
         kind = self.launch_kind(launch)
         n_q = launch.q_lens[0] if kind == "verify" else 1
-        plan, info = B.plan(KIND[kind], n_q, md["seq_lens"], md["cu_seqlens_q"], cfg.num_q_heads,
-                            cfg.num_kv_heads, cfg.head_dim, cfg.block_size, self.dcode,
-                            self.num_cus, out=st.plan[0].numpy(),
-                            block_table=md["block_table"] if self.cascade else None)
-        if info.plan_words > st.plan[0].numel():
-            raise RuntimeError("staging plan buffer too small")
+        st.wait()
+        info = self.pool.prepare_launch(batched["pre"], inp, st.buffers, KIND[kind], n_q,
+                                        cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
+                                        self.dcode, self.num_cus, self.cascade, info=st.info)
+        self.n_cached = batched["pre"].admitted()
         # one copy: everything up to the end of the plan
         used = st.plan_off + int(info.plan_words)
         st.dev[:used].copy_(st.host[:used], non_blocking=True)
@@ -217,12 +242,12 @@ class DeviceReplay:
                 self._ws = torch.empty(int(info.workspace_bytes), dtype=torch.uint8,
                                        device=self.device)
             ws = self._ws
+        bt, sl, cu, slots = st.device_views(n, T)
         return Prepared(
-            kind=kind, meta=md, info=info, plan_host=plan,
-            block_table=st.bt[1][:n * st.max_blocks].view(n, st.max_blocks),
-            seq_lens=st.sl[1][:n], cu=st.cu[1][:n + 1], slots=st.slots[1][:T],
-            plan=st.plan[1][:int(info.plan_words)], q=q, k_new=k_new, v_new=v_new, ws=ws,
-            out=out, lse=lse, n_cached=dict(self.n_cached))
+            kind=kind, meta=st.buffers.meta(n, T), info=info,
+            plan_host=st.buffers.plan[:int(info.plan_words)], block_table=bt, seq_lens=sl,
+            cu=cu, slots=slots, plan=st.plan[1], q=q, k_new=k_new, v_new=v_new, ws=ws, out=out,
+            lse=lse, n_cached=self.n_cached)
 
     def append(self, p: Prepared, stream=None):
         B.kv_append(p.k_new, p.v_new, p.slots, self.k_cache, self.v_cache, stream)

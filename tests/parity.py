@@ -9,7 +9,7 @@ import numpy as np
 import torch
 
 from oracle.run import OracleReplay
-from paper_2605_11232_amd.runtime import DeviceReplay
+from paper_2605_11232_amd.runtime import DeviceReplay, Staging, plan_words_bound
 
 # Elementwise |o - r| <= atol + rtol * |r|: bf16 inputs with float32
 # accumulation 1e-2 / 2e-2; the float32 path 1e-5 / 1e-5.
@@ -54,8 +54,12 @@ def compare_cache(dev: DeviceReplay, prep, k_new, v_new):
     np.testing.assert_array_equal(vd, v_new)
 
 
-def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, label=""):
-    """Replay ``wl`` through both; returns per-launch normalized errors."""
+def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, label="",
+               staged=False):
+    """Replay ``wl`` through both; returns per-launch normalized errors.
+    ``staged``: the device side runs the benchmark's path (one library call
+    for pool operations, metadata and plan into alternating pinned staging
+    buffers, one upload each, a reused workspace)."""
     cfg = wl.cfg
     atol, rtol = TOL[cfg.dtype]
     latol, lrtol = LSE_TOL[cfg.dtype]
@@ -66,10 +70,29 @@ def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, lab
     if steps:
         launches += [wl.step(s) for s in steps]
     errs = []
+    stagings = None
+    if staged:
+        n = max(len(ln.seq_ids) for ln in launches)
+        T = max(ln.total_q for ln in launches)
+        words = plan_words_bound(cfg, n, T, wl.max_blocks_per_seq)
+        stagings = [Staging(dev.device, n, wl.max_blocks_per_seq, T, words) for _ in range(2)]
     for li, launch in enumerate(launches):
-        say(f"[parity] {label or cfg.name}: launch {li} ({launch.total_q} query tokens)")
+        say(f"[parity] {label or cfg.name}: launch {li} ({launch.total_q} query tokens)"
+            + (" staged" if staged else ""))
         ro = orc.launch(launch, rows=rows)
-        p = dev.run(launch)
+        if staged:
+            T = launch.total_q
+            q = torch.from_numpy(launch.q.get()).to(dev.device, dev.tdtype)
+            k_new = torch.from_numpy(launch.k_new.get()).to(dev.device, dev.tdtype)
+            v_new = torch.from_numpy(launch.v_new.get()).to(dev.device, dev.tdtype)
+            out = torch.empty((T, cfg.num_q_heads, cfg.head_dim), dtype=dev.tdtype,
+                              device=dev.device)
+            lse = torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device=dev.device)
+            p = dev.prepare_staged(launch, stagings[li % 2], q, k_new, v_new, out, lse)
+            dev.append(p)
+            dev.attend(p)
+        else:
+            p = dev.run(launch)
         torch.cuda.synchronize()
         for k in ("block_table", "seq_lens", "cu_seqlens_q", "slot_mapping"):
             np.testing.assert_array_equal(p.meta[k], ro["meta"][k], err_msg=k)
@@ -81,7 +104,7 @@ def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, lab
         errs.append(close(out, ro["out"], atol, rtol, f"out[{li}]"))
         close(lse, ro["lse"], latol, lrtol, f"lse[{li}]")
         orc.finish(launch)
-        dev.finish(launch)
+        dev.finish(launch, batched=staged)
     return errs, dev, orc
 
 

@@ -421,7 +421,7 @@ def test_pool_apply_matches_oracle_on_steps(name):
             lp.free(op.seq_id)
     for st in range(3):
         launch = wl.step(st)
-        hits = lp.apply(*batch_ops(launch.pre))
+        hits = lp.apply_packed(batch_ops(launch.pre)).copy()
         want = [o.add(op.seq_id, op.tokens) if op.kind == "add" else
                 (o.extend(op.seq_id, op.tokens) or 0) for op in launch.pre]
         assert hits.tolist() == want
@@ -429,7 +429,7 @@ def test_pool_apply_matches_oracle_on_steps(name):
         ml = lp.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
         for k in mo:
             np.testing.assert_array_equal(mo[k], ml[k])
-        lp.apply(*batch_ops(launch.post))
+        lp.apply_packed(batch_ops(launch.post))
         for op in launch.post:
             if op.kind == "free":
                 o.free_seq(op.seq_id)
@@ -494,3 +494,64 @@ def test_batch_former_rejects_bad_arguments():
         with pytest.raises(B.PaError) as e:
             B.form_batches(ad, ln, bb)
         assert e.value.code == "arg"
+
+
+@pytest.mark.parametrize("name", ["decode", "verify", "mixed"])
+def test_prepare_launch_matches_separate_calls(name):
+    """pa_prepare_launch (pool operations, metadata and plan in one call, into
+    caller buffers) against pa_pool_apply + pa_build_metadata + pa_attn_plan
+    on a second pool, over several steps: identical tables, plans, infos,
+    reuse counts and free lists."""
+    from paper_2605_11232_amd.runtime import batch_ops
+    wl = synth.workload(name, scale=0.25, steps=4)
+    cfg = wl.cfg
+    pools = [B.Pool(wl.num_blocks, cfg.block_size, wl.free_order) for _ in range(2)]
+    for lp in pools:
+        for op in wl.setup:
+            if op.kind == "add":
+                lp.add(op.seq_id, op.tokens)
+            elif op.kind == "free":
+                lp.free(op.seq_id)
+    mb = wl.max_blocks_per_seq
+    for st in range(3):
+        launch = wl.step(st)
+        n, T = len(launch.seq_ids), int(sum(launch.q_lens))
+        kind = {"decode": B.KIND_DECODE, "verify": B.KIND_VERIFY}.get(name, B.KIND_PREFILL)
+        n_q = launch.q_lens[0] if name == "verify" else 1
+        # fused, into caller buffers
+        buf = B.LaunchBuffers(np.full((n, mb), 7, np.int32), np.zeros(n, np.int32),
+                              np.zeros(n + 1, np.int32), np.zeros(T, np.int32),
+                              np.zeros(1 << 20, np.int32))
+        pre = batch_ops(launch.pre)
+        info = pools[0].prepare_launch(pre, B.LaunchInputs(launch.seq_ids, launch.q_lens), buf,
+                                       kind, n_q, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
+                                       B.PA_BF16, 256, True)
+        # separate calls
+        hits = pools[1].apply_packed(batch_ops(launch.pre)).copy()
+        md = pools[1].metadata(launch.seq_ids, launch.q_lens, mb)
+        plan, info2 = B.plan(kind, n_q, md["seq_lens"], md["cu_seqlens_q"], cfg.num_q_heads,
+                             cfg.num_kv_heads, cfg.head_dim, cfg.block_size, B.PA_BF16, 256,
+                             block_table=md["block_table"])
+        assert pre.n_cached[:pre.n].tolist() == hits.tolist()
+        for k, v in buf.meta(n, T).items():
+            np.testing.assert_array_equal(v, md[k], err_msg=k)
+        np.testing.assert_array_equal(buf.plan[:info.plan_words], plan)
+        for f, _ in B.PlanInfo._fields_:
+            assert getattr(info, f) == getattr(info2, f), f
+        for lp in pools:
+            lp.apply_packed(batch_ops(launch.post))
+        assert pools[0].free_list() == pools[1].free_list()
+    # a plan buffer that is too small: argument error, pool operations applied
+    launch = wl.step(3)
+    n, T = len(launch.seq_ids), int(sum(launch.q_lens))
+    small = B.LaunchBuffers(np.zeros((n, mb), np.int32), np.zeros(n, np.int32),
+                            np.zeros(n + 1, np.int32), np.zeros(T, np.int32),
+                            np.zeros(8, np.int32))
+    before = pools[0].stats()["live_tokens"]
+    with pytest.raises(B.PaError) as e:
+        pools[0].prepare_launch(batch_ops(launch.pre), B.LaunchInputs(launch.seq_ids, launch.q_lens),
+                                small, B.KIND_PREFILL if name == "mixed" else kind, n_q,
+                                cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, B.PA_BF16)
+    assert e.value.rc == B.PA_ERR_ARG and b"capacity" in B.lib().pa_last_error()
+    added = sum(len(op.tokens) for op in launch.pre if op.tokens is not None)
+    assert pools[0].stats()["live_tokens"] == before + added

@@ -53,6 +53,23 @@ def test_reduced(name, scale):
     say(name, "normalized errors", errs)
 
 
+@pytest.mark.parametrize("name,scale", [("tiny", None), ("prefill", 0.125), ("decode", 0.0625),
+                                        ("mixed", 0.0625), ("verify", 0.125)])
+def test_staged_path(name, scale):
+    """The benchmark's path: one library call per step for pool operations,
+    metadata and plan into pinned staging buffers used alternately, one
+    upload, the reused split workspace, batched release; four consecutive
+    steps so each staging buffer is reused."""
+    _gpu()
+    if scale is None:  # the tiny float32 workload: its own nine launches
+        wl, steps = synth.workload(name), None
+    else:
+        wl, steps = synth.workload(name, scale=scale, steps=5), [1, 2, 3]
+    errs, _, _ = run_parity(wl, steps=steps, staged=True, label=f"staged {name}")
+    say(name, "staged normalized errors", errs)
+    assert len(errs) == len(wl.launches) + len(steps or [])
+
+
 @pytest.mark.parametrize("name", ["prefill", "decode", "mixed", "verify"])
 def test_full_size_sampled(name):
     """The benchmark's exact launch (full size) on sampled rows."""
