@@ -66,6 +66,18 @@ def kernel_fingerprint() -> str:
     return h.hexdigest()
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (as /proc/cpuinfo gives it)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
 def measured_traffic(name: str):
     """Counter-measured HBM bytes per call for this workload, or None when no
     record exists or the kernels changed since it was taken."""
@@ -132,6 +144,9 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, 5 times "
                          "(calibrates the HBM byte counters against a known transfer)")
+    ap.add_argument("--matmul-n", type=int, default=0,
+                    help="only run a bf16 [n, n] x [n, n] torch.matmul 5 times (calibrates the "
+                         "MFMA operation counters against a known FLOP count)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the hot path here is a single-GPU kernel "
@@ -148,6 +163,17 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "launches": 5}), flush=True)
+        return
+    if args.matmul_n:
+        n = args.matmul_n
+        g = torch.Generator(device="cuda").manual_seed(0)
+        x = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16).contiguous()
+        y = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16).contiguous()
+        for _ in range(5):
+            z = torch.matmul(x, y)
+        torch.cuda.synchronize()
+        print(json.dumps({"matmul_n": n, "flop_per_launch": 2 * n ** 3, "launches": 5,
+                          "checksum": float(z.float().abs().mean())}), flush=True)
         return
     from paper_2605_11232_amd import perf, synth
     from paper_2605_11232_amd.runtime import DeviceReplay, Staging, plan_words_bound
@@ -304,7 +330,7 @@ def main():
         rec["cpu_baseline"] = {"value": cval, "unit": cunit, "cores": threads, "kind": "oracle",
                                "sample": f"float64 oracle attention of the first {done} of "
                                          f"{len(L0.seq_ids)} requests of the same launch "
-                                         f"(all heads), {dt:.1f} s"}
+                                         f"(all heads), {dt:.1f} s on {cpu_model()}"}
     print(json.dumps(rec), flush=True)
 
 
