@@ -19,9 +19,9 @@
 // merged with each sequence's private-key part by log-sum-exp: the prefix is
 // read from memory once per launch instead of once per sequence.
 //
-// Paper: Section 5.2 (split
-// prefills under a batched-token budget, mixed prefill and decode), Section 6,
-// Table "playbook" (long prefills blocking short decodes).
+// Paper: Section 5.2 (split prefills under a batched-token budget, mixed
+// prefill and decode), Section 6, Table "playbook" (long prefills blocking
+// short decodes).
 //
 // Dispatch order: workgroup ids are handed to the eight XCDs round robin, and
 // each XCD has its own L2.  Items are queued per XCD by kv-head so that all
@@ -32,7 +32,6 @@
 #include <array>
 #include <climits>
 #include <cstdint>
-#include <unordered_map>
 #include <vector>
 
 #include "internal.h"
