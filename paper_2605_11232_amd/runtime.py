@@ -220,7 +220,8 @@ class DeviceReplay:
         pair: one library call applies the launch's pool operations and
         writes its metadata and plan into the pinned buffer, one
         asynchronous copy uploads them, so host bookkeeping overlaps earlier
-        GPU work."""
+        GPU work.  The returned host views (meta, plan_host, info) live in the
+        staging buffer: valid until the buffer is used for another launch."""
         batched, inp = marshal_launch(launch)
         cfg = self.cfg
         n, T = inp.n, inp.total_q
