@@ -70,13 +70,16 @@ def test_staged_path(name, scale):
     assert len(errs) == len(wl.launches) + len(steps or [])
 
 
+@pytest.mark.parametrize("staged", [False, True])
 @pytest.mark.parametrize("name", ["prefill", "decode", "mixed", "verify"])
-def test_full_size_sampled(name):
-    """The benchmark's exact launch (full size) on sampled rows."""
+def test_full_size_sampled(name, staged):
+    """The benchmark's exact launch (full size) on sampled rows, through the
+    plain path and through the staged path bench.py times."""
     _gpu()
     wl = synth.workload(name, steps=2)
     rows = sample_rows(wl.launches[0], 48, wl.cfg.num_q_heads, seed=7)
-    errs, _, _ = run_parity(wl, n_launches=1, rows=rows, label=f"{name}-full")
+    errs, _, _ = run_parity(wl, n_launches=1, rows=rows, staged=staged,
+                            label=f"{name}-full" + (" staged" if staged else ""))
     say(name, "full-size normalized error", errs)
 
 
