@@ -322,6 +322,18 @@ int pa_kv_append(const void* k_new, const void* v_new, const int32_t* slot_mappi
                  int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t dtype,
                  void* stream);
 
+/* Upload of a launch's host-built metadata and plan (paper: Section 5.2, one
+ * batched launch per serving step): copies bytes (a multiple of 4) from src,
+ * page-locked host memory the device can read (e.g. from hipHostMalloc), to
+ * dst, device memory, by a kernel on the stream, which reads the host buffer
+ * over the bus (no copy-engine start-up).  The caller must not modify src
+ * until the copy has completed on the stream (e.g. an event recorded after
+ * this call).  Errors (checked before anything is launched): PA_ERR_ARG (size
+ * not a multiple of 4, misaligned or NULL pointers, either end of the source
+ * range not pinned host memory the device can address, or of the destination
+ * range not device memory); PA_ERR_LAUNCH. */
+int pa_stage_upload(void* dst, const void* src, int64_t bytes, void* stream);
+
 /* Paged attention over a prefix-shared KV cache.  For sequence r, q-head h
  * and its query i at logical position a = seq_lens[r] - q_len_r + i:
  *   out = sum_{t<=a} softmax_t(scale * q . k_t) v_t,   k_t, v_t from kv-head

@@ -28,7 +28,8 @@ EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy
            "pa_seqs_truncate", "pa_seqs_free", "pa_pool_apply", "pa_seq_len", "pa_seq_blocks",
            "pa_pool_free_list", "pa_build_metadata", "pa_attn_plan", "pa_kv_append",
            "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify", "pa_pool_set_eviction",
-           "pa_pool_get_stats", "pa_pool_kv_waste", "pa_form_batches", "pa_prepare_launch"]
+           "pa_pool_get_stats", "pa_pool_kv_waste", "pa_form_batches", "pa_prepare_launch",
+           "pa_stage_upload"]
 
 
 class PaError(RuntimeError):
@@ -94,6 +95,7 @@ def lib():
         "pa_attn_plan": (C.c_int, [i32, i32, i32, _I32P, _I32P, _I32P, i32, i32, i32, i32, i32, i32,
                                    i32, _I32P, i64, C.POINTER(PlanInfo)]),
         "pa_kv_append": (C.c_int, [_P, _P, _P, i32, _P, _P, i32, i32, i32, i32, i32, _P]),
+        "pa_stage_upload": (C.c_int, [_P, _P, i64, _P]),
         "pa_pool_set_eviction": (C.c_int, [_P, i32]),
         "pa_pool_get_stats": (C.c_int, [_P, C.POINTER(PoolStats)]),
         "pa_pool_kv_waste": (C.c_int, [_P, i32, C.POINTER(KvWaste)]),
@@ -423,6 +425,12 @@ def _dtype_code(t) -> int:
     if t.dtype == torch.float32:
         return PA_F32
     raise PaError(PA_ERR_UNSUPPORTED, f"dtype {t.dtype}")
+
+
+def stage_upload(dst, src, nbytes: int, stream=None):
+    """Copy the first nbytes of pinned host tensor src into device tensor dst
+    with the library's upload kernel (pa_stage_upload)."""
+    _check(lib().pa_stage_upload(_dptr(dst), _dptr(src), int(nbytes), _stream(stream)))
 
 
 def kv_append(k_new, v_new, slot_mapping, k_cache, v_cache, stream=None):

@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libpa.so")
 
-HIP_SOURCES = ["attn_bf16.hip", "attn_f32.hip", "kv_append.hip", "api.hip"]
+HIP_SOURCES = ["attn_bf16.hip", "attn_f32.hip", "kv_append.hip", "stage.hip", "api.hip"]
 HOST_SOURCES = ["pool.cpp", "plan.cpp", "batch.cpp", "step.cpp", "errors.cpp"]
 
 ARCH = "gfx950"

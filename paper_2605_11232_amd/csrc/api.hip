@@ -20,6 +20,7 @@ int launch_attn_f32(const void* q, const void* kc, const void* vc, int32_t num_b
 int launch_kv_append(const void* kn, const void* vn, const int32_t* slots, int32_t n, void* kc,
                      void* vc, int32_t nb, int32_t hkv, int32_t d, int32_t dtype,
                      hipStream_t stream);
+int launch_stage_upload(const void* src, void* dst, int64_t n_dwords, hipStream_t stream);
 }  // namespace dev
 
 namespace {
@@ -112,6 +113,46 @@ int pa_kv_append(const void* k_new, const void* v_new, const int32_t* slot_mappi
                                  static_cast<hipStream_t>(stream));
   if (rc)
     return pa::fail(PA_ERR_LAUNCH, "pa_kv_append: %s",
+                    hipGetErrorString(static_cast<hipError_t>(rc)));
+  return PA_OK;
+}
+
+// Both ends of [p, p + bytes) must be memory of the given kind that the device
+// can address; *dev receives the device address of p.  A failed query leaves
+// no HIP error behind.
+static bool device_visible(const void* p, int64_t bytes, hipMemoryType want, void** dev) {
+  const char* c = static_cast<const char*>(p);
+  for (const char* q : {c, c + bytes - 1}) {
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, q) != hipSuccess) {
+      (void)hipGetLastError();
+      return false;
+    }
+    if (at.type != want || at.devicePointer == nullptr) return false;
+    if (q == c) *dev = at.devicePointer;
+  }
+  return true;
+}
+
+int pa_stage_upload(void* dst, const void* src, int64_t bytes, void* stream) {
+  pa::clear_error();
+  if (bytes < 0 || bytes % 4 ||
+      (bytes > 0 && (!dst || !src ||
+                     ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src)) & 3))))
+    return pa::fail(PA_ERR_ARG, "pa_stage_upload: bytes %lld must be a multiple of 4 with "
+                    "4-byte aligned, non-NULL pointers", (long long)bytes);
+  if (bytes == 0) return PA_OK;
+  void* src_dev = nullptr;
+  void* dst_dev = nullptr;
+  if (!device_visible(src, bytes, hipMemoryTypeHost, &src_dev))
+    return pa::fail(PA_ERR_ARG, "pa_stage_upload: source is not pinned host memory the device "
+                    "can read");
+  if (!device_visible(dst, bytes, hipMemoryTypeDevice, &dst_dev))
+    return pa::fail(PA_ERR_ARG, "pa_stage_upload: destination is not device memory");
+  const int rc =
+      pa::dev::launch_stage_upload(src_dev, dst_dev, bytes / 4, static_cast<hipStream_t>(stream));
+  if (rc)
+    return pa::fail(PA_ERR_LAUNCH, "pa_stage_upload: %s",
                     hipGetErrorString(static_cast<hipError_t>(rc)));
   return PA_OK;
 }

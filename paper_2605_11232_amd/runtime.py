@@ -71,9 +71,9 @@ def plan_words_bound(cfg, n_seqs: int, total_q: int, max_blocks_per_seq: int) ->
 class Staging:
     """One pinned host buffer and one device buffer holding a launch's
     metadata and plan ([seq_lens | cu_seqlens_q | block_table | slot_mapping |
-    plan], int32), uploaded with a single asynchronous copy on the compute
-    stream, so stream order puts it after the kernels of the launch that used
-    the device buffer before.  The host fills the pinned buffer while the GPU
+    plan], int32), uploaded in one piece on the compute stream (by the
+    library's upload kernel, or a copy-engine copy), so stream order puts it
+    after the kernels of the launch that used the device buffer before.  The host fills the pinned buffer while the GPU
     still works on an earlier launch; ``ready`` (recorded after the copy)
     guards reuse of the host buffer."""
 
@@ -116,7 +116,7 @@ class Staging:
 
 class DeviceReplay:
     def __init__(self, wl, device: str = "cuda", kind: str | None = None, num_cus: int = 0,
-                 cascade: bool = True):
+                 cascade: bool = True, stage_kernel: bool = True):
         cfg = wl.cfg
         self.wl, self.cfg, self.device = wl, cfg, torch.device(device)
         self.tdtype = torch_dtype(cfg.dtype)
@@ -130,6 +130,8 @@ class DeviceReplay:
         self.kind = kind
         self.num_cus = num_cus
         self.cascade = cascade
+        # staged uploads by the library's kernel (else by a copy-engine copy)
+        self.stage_kernel = stage_kernel
         self.n_cached = {}
         self._ws = None  # split-K workspace of staged launches (all on the current stream)
 
@@ -234,7 +236,10 @@ class DeviceReplay:
         self.n_cached = batched["pre"].admitted()
         # one copy: everything up to the end of the plan
         used = st.plan_off + int(info.plan_words)
-        st.dev[:used].copy_(st.host[:used], non_blocking=True)
+        if self.stage_kernel:
+            B.stage_upload(st.dev, st.host, 4 * used)
+        else:
+            st.dev[:used].copy_(st.host[:used], non_blocking=True)
         st.ready.record()
         st.used = True
         ws = None

@@ -349,6 +349,12 @@ def test_device_calls_reject_bad_arguments_without_launching():
     assert lib.pa_attn_decode(*args) == B.PA_ERR_ARG
     assert lib.pa_kv_append(None, None, None, 3, None, None, 16, 2, 128, 16, B.PA_BF16, None) == B.PA_ERR_ARG
     assert lib.pa_kv_append(None, None, None, 0, None, None, 16, 2, 100, 16, B.PA_BF16, None) == B.PA_ERR_UNSUPPORTED
+    # staged upload: size and alignment are checked before any runtime call
+    assert lib.pa_stage_upload(None, None, 0, None) == B.PA_OK
+    assert lib.pa_stage_upload(None, None, 8, None) == B.PA_ERR_ARG
+    assert lib.pa_stage_upload(4096, 8192, 6, None) == B.PA_ERR_ARG
+    assert lib.pa_stage_upload(4098, 8192, 8, None) == B.PA_ERR_ARG
+    assert lib.pa_stage_upload(4096, 8192, -4, None) == B.PA_ERR_ARG
 
 
 def test_plan_rejects_inconsistent_lengths():

@@ -83,6 +83,38 @@ def test_full_size_sampled(name, staged):
     say(name, "full-size normalized error", errs)
 
 
+def test_stage_upload():
+    """The upload kernel copies pinned host memory to device memory exactly,
+    twice in a row (the second time fewer bytes of rewritten data: the new
+    values arrive, nothing past the range changes, nothing stale is read), and
+    refuses sources that are not pinned host memory before launching."""
+    _gpu()
+    from paper_2605_11232_amd import binding as B
+    n = 1_000_003
+    r = np.random.default_rng(3)
+    host = torch.empty(n, dtype=torch.int32, pin_memory=True)
+    dev = torch.zeros(n, dtype=torch.int32, device="cuda")
+    first = r.integers(-2**31, 2**31 - 1, size=n, dtype=np.int64).astype(np.int32)
+    host.numpy()[:] = first
+    B.stage_upload(dev, host, 4 * n)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(dev.cpu().numpy(), first)
+    m = 12_345
+    second = r.integers(-2**31, 2**31 - 1, size=n, dtype=np.int64).astype(np.int32)
+    host.numpy()[:] = second
+    B.stage_upload(dev, host, 4 * m)
+    torch.cuda.synchronize()
+    got = dev.cpu().numpy()
+    np.testing.assert_array_equal(got[:m], second[:m])
+    np.testing.assert_array_equal(got[m:], first[m:])
+    pageable = torch.ones(16, dtype=torch.int32)
+    with pytest.raises(B.PaError):
+        B.stage_upload(dev, pageable, 64)
+    with pytest.raises(B.PaError):
+        B.stage_upload(dev, dev, 64)
+    torch.cuda.synchronize()
+
+
 def test_bitwise_invariants():
     """Outputs are identical bit for bit when physical placement changes and
     when the shared prefix is duplicated instead of shared, and from run to run
