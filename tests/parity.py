@@ -55,17 +55,18 @@ def compare_cache(dev: DeviceReplay, prep, k_new, v_new):
 
 
 def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, label="",
-               staged=False):
+               staged=False, stage_kernel=True):
     """Replay ``wl`` through both; returns per-launch normalized errors.
     ``staged``: the device side runs the benchmark's path (one library call
     for pool operations, metadata and plan into alternating pinned staging
-    buffers, one upload each, a reused workspace)."""
+    buffers, one upload each, a reused workspace; ``stage_kernel``: the
+    upload by the library's kernel, else by a copy-engine copy)."""
     cfg = wl.cfg
     atol, rtol = TOL[cfg.dtype]
     latol, lrtol = LSE_TOL[cfg.dtype]
     say(f"[parity] {label or cfg.name}: setup")
     orc = OracleReplay(wl).setup()
-    dev = DeviceReplay(wl).setup()
+    dev = DeviceReplay(wl, stage_kernel=stage_kernel).setup()
     launches = list(wl.launches[:n_launches] if n_launches else wl.launches)
     if steps:
         launches += [wl.step(s) for s in steps]

@@ -70,6 +70,15 @@ def test_staged_path(name, scale):
     assert len(errs) == len(wl.launches) + len(steps or [])
 
 
+def test_staged_path_copy_engine_upload():
+    """The staged path with a copy-engine copy instead of the upload kernel,
+    reduced decode over consecutive steps."""
+    _gpu()
+    errs, _, _ = run_parity(synth.workload("decode", scale=0.0625, steps=5), steps=[1, 2, 3],
+                            staged=True, stage_kernel=False, label="staged decode copy")
+    say("staged copy-engine normalized errors", errs)
+
+
 @pytest.mark.parametrize("staged", [False, True])
 @pytest.mark.parametrize("name", ["prefill", "decode", "mixed", "verify"])
 def test_full_size_sampled(name, staged):
