@@ -418,6 +418,69 @@ def _stream(stream) -> int:
     return int(getattr(stream, "cuda_stream", stream))
 
 
+_hip = None
+HIP_EVENT_DISABLE_TIMING, HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x2, 0x20000000
+
+
+def _hip_runtime():
+    """The HIP runtime libpa links against (the process's only copy: torch
+    loads the same soname)."""
+    global _hip
+    if _hip is None:
+        lib()
+        h = C.CDLL("libamdhip64.so.7")
+        h.hipEventCreateWithFlags.argtypes = [C.POINTER(_P), C.c_uint]
+        h.hipEventRecord.argtypes = [_P, _P]
+        h.hipEventSynchronize.argtypes = [_P]
+        h.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), _P, _P]
+        h.hipEventDestroy.argtypes = [_P]
+        for f in ("hipEventCreateWithFlags", "hipEventRecord", "hipEventSynchronize",
+                  "hipEventElapsedTime", "hipEventDestroy"):
+            getattr(h, f).restype = C.c_int
+        _hip = h
+    return _hip
+
+
+class StreamEvent:
+    """A HIP event recorded without a system-scope fence.
+
+    A default event record writes back and invalidates the GPU caches at
+    system scope so the host can read device results once the event
+    completes; in a stream of back-to-back kernels each such record costs
+    several microseconds of idle device.  Nothing waiting on these events
+    reads device memory: the staging buffers use them to learn that an
+    upload has finished reading pinned host memory (its loads bypass the
+    caches), and the benchmark uses them for timing only."""
+
+    def __init__(self, timing: bool = False):
+        self._h = _hip_runtime()
+        self._ev = _P()
+        flags = HIP_EVENT_DISABLE_SYSTEM_FENCE | (0 if timing else HIP_EVENT_DISABLE_TIMING)
+        self._rc("hipEventCreateWithFlags", self._h.hipEventCreateWithFlags(C.byref(self._ev), flags))
+
+    @staticmethod
+    def _rc(what: str, rc: int):
+        if rc != 0:
+            raise PaError(PA_ERR_LAUNCH, f"{what} returned HIP error {rc}")
+
+    def record(self, stream=None):
+        self._rc("hipEventRecord", self._h.hipEventRecord(self._ev, _stream(stream)))
+
+    def synchronize(self):
+        self._rc("hipEventSynchronize", self._h.hipEventSynchronize(self._ev))
+
+    def elapsed_time(self, end: "StreamEvent") -> float:
+        """Milliseconds from this event to end (both recorded and complete)."""
+        ms = C.c_float()
+        self._rc("hipEventElapsedTime", self._h.hipEventElapsedTime(C.byref(ms), self._ev, end._ev))
+        return float(ms.value)
+
+    def __del__(self):
+        if getattr(self, "_ev", None) and _hip is not None:
+            _hip.hipEventDestroy(self._ev)
+            self._ev = None
+
+
 def _dtype_code(t) -> int:
     import torch
     if t.dtype == torch.bfloat16:

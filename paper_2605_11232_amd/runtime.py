@@ -74,8 +74,9 @@ class Staging:
     plan], int32), uploaded in one piece on the compute stream (by the
     library's upload kernel, or a copy-engine copy), so stream order puts it
     after the kernels of the launch that used the device buffer before.  The host fills the pinned buffer while the GPU
-    still works on an earlier launch; ``ready`` (recorded after the copy)
-    guards reuse of the host buffer."""
+    still works on an earlier launch; ``guard``, an event recorded after the
+    upload (``ready``, or one the caller hands to ``prepare_staged``), guards
+    reuse of the host buffer."""
 
     def __init__(self, device, n_seqs, max_blocks, max_tokens, plan_words):
         self.n_seqs, self.max_blocks = n_seqs, max_blocks
@@ -90,7 +91,8 @@ class Staging:
             setattr(self, name, (self.host[off:off + m], self.dev[off:off + m]))
             setattr(self, name + "_off", off)
             off += m
-        self.ready = torch.cuda.Event()
+        self.ready = B.StreamEvent()
+        self.guard = self.ready
         self.used = False
         # host views the library writes into, and device views by launch shape
         self.buffers = B.LaunchBuffers(self.bt[0].numpy().reshape(n_seqs, max_blocks),
@@ -111,7 +113,7 @@ class Staging:
 
     def wait(self):
         if self.used:
-            self.ready.synchronize()
+            self.guard.synchronize()
 
 
 class DeviceReplay:
@@ -217,13 +219,21 @@ class DeviceReplay:
             lse=torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device=dev),
             n_cached=dict(self.n_cached))
 
-    def prepare_staged(self, launch, st: Staging, q, k_new, v_new, out, lse) -> Prepared:
+    def prepare_staged(self, launch, st: Staging, q, k_new, v_new, out, lse,
+                       guard=None) -> Prepared:
         """Like ``prepare`` but through a preallocated pinned/device staging
         pair: one library call applies the launch's pool operations and
         writes its metadata and plan into the pinned buffer, one
         asynchronous copy uploads them, so host bookkeeping overlaps earlier
         GPU work.  The returned host views (meta, plan_host, info) live in the
-        staging buffer: valid until the buffer is used for another launch."""
+        staging buffer: valid until the buffer is used for another launch.
+
+        The staging buffer is released for reuse by an event recorded after
+        the upload: its own ``ready`` event right after it, or, when the
+        caller passes ``guard`` (an event it wants on the stream anyway, such
+        as the start of a timed attention call), that event, recorded by
+        ``append`` after the KV append.  Each event record is a marker in the
+        stream that idles the device for a few microseconds."""
         batched, inp = marshal_launch(launch)
         cfg = self.cfg
         n, T = inp.n, inp.total_q
@@ -240,7 +250,11 @@ class DeviceReplay:
             B.stage_upload(st.dev, st.host, 4 * used)
         else:
             st.dev[:used].copy_(st.host[:used], non_blocking=True)
-        st.ready.record()
+        if guard is None:
+            st.ready.record()
+            st.guard = st.ready
+        else:
+            st.guard = guard
         st.used = True
         ws = None
         if info.workspace_bytes:
@@ -253,10 +267,13 @@ class DeviceReplay:
             kind=kind, meta=st.buffers.meta(n, T), info=info,
             plan_host=st.buffers.plan[:int(info.plan_words)], block_table=bt, seq_lens=sl,
             cu=cu, slots=slots, plan=st.plan[1], q=q, k_new=k_new, v_new=v_new, ws=ws, out=out,
-            lse=lse, n_cached=self.n_cached)
+            lse=lse, n_cached=self.n_cached, guard=guard)
 
     def append(self, p: Prepared, stream=None):
         B.kv_append(p.k_new, p.v_new, p.slots, self.k_cache, self.v_cache, stream)
+        guard = getattr(p, "guard", None)
+        if guard is not None:
+            guard.record(stream)
 
     def attend(self, p: Prepared, stream=None):
         B.attention(KIND[p.kind], p.q, self.k_cache, self.v_cache, p.block_table, p.seq_lens, p.cu,

@@ -9,6 +9,7 @@ import numpy as np
 import torch
 
 from oracle.run import OracleReplay
+from paper_2605_11232_amd import binding as B
 from paper_2605_11232_amd.runtime import DeviceReplay, Staging, plan_words_bound
 
 # Elementwise |o - r| <= atol + rtol * |r|: bf16 inputs with float32
@@ -59,8 +60,9 @@ def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, lab
     """Replay ``wl`` through both; returns per-launch normalized errors.
     ``staged``: the device side runs the benchmark's path (one library call
     for pool operations, metadata and plan into alternating pinned staging
-    buffers, one upload each, a reused workspace; ``stage_kernel``: the
-    upload by the library's kernel, else by a copy-engine copy)."""
+    buffers, one upload each, a reused workspace, odd launches released by a
+    caller's event; ``stage_kernel``: the upload by the library's kernel, else
+    by a copy-engine copy)."""
     cfg = wl.cfg
     atol, rtol = TOL[cfg.dtype]
     latol, lrtol = LSE_TOL[cfg.dtype]
@@ -89,7 +91,11 @@ def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, lab
             out = torch.empty((T, cfg.num_q_heads, cfg.head_dim), dtype=dev.tdtype,
                               device=dev.device)
             lse = torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device=dev.device)
-            p = dev.prepare_staged(launch, stagings[li % 2], q, k_new, v_new, out, lse)
+            # odd launches release their staging buffer through a caller's
+            # event recorded after the KV append (the benchmark's timed steps)
+            guard = B.StreamEvent() if li % 2 else None
+            p = dev.prepare_staged(launch, stagings[li % 2], q, k_new, v_new, out, lse,
+                                   guard=guard)
             dev.append(p)
             dev.attend(p)
         else:

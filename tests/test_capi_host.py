@@ -357,6 +357,20 @@ def test_device_calls_reject_bad_arguments_without_launching():
     assert lib.pa_stage_upload(4096, 8192, -4, None) == B.PA_ERR_ARG
 
 
+def test_stream_event_binds_the_runtime():
+    """The fence-free stream events resolve in the HIP runtime libpa links;
+    without a device, creating one raises instead of returning a null event."""
+    h = B._hip_runtime()
+    for f in ("hipEventCreateWithFlags", "hipEventRecord", "hipEventSynchronize",
+              "hipEventElapsedTime", "hipEventDestroy"):
+        assert getattr(h, f) is not None
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a device is present; the GPU tests record these events")
+    with pytest.raises(B.PaError, match="hipEventCreateWithFlags"):
+        B.StreamEvent(timing=True)
+
+
 def test_plan_rejects_inconsistent_lengths():
     with pytest.raises(B.PaError) as e:
         B.plan(B.KIND_DECODE, 1, [10, 10], [0, 1, 3], 8, 2, 128, 16, B.PA_BF16)
