@@ -124,6 +124,34 @@ def test_stage_upload():
     torch.cuda.synchronize()
 
 
+def test_stream_events():
+    """Fence-free events: a timed interval around an upload is positive and
+    ordered on the stream; a staging buffer released by a caller's event
+    waits on that event, not its own."""
+    _gpu()
+    from paper_2605_11232_amd import binding as B
+    from paper_2605_11232_amd.runtime import Staging
+    n = 1 << 22
+    host = torch.arange(n, dtype=torch.int32).pin_memory()
+    dev = torch.zeros(n, dtype=torch.int32, device="cuda")
+    a, b = B.StreamEvent(timing=True), B.StreamEvent(timing=True)
+    a.record()
+    B.stage_upload(dev, host, 4 * n)
+    b.record()
+    b.synchronize()
+    ms = a.elapsed_time(b)
+    assert 0.0 < ms < 1000.0, ms
+    # the upload before b is complete once b is
+    assert int(dev[n - 1].item()) == n - 1
+    st = Staging("cuda", 2, 4, 8, 64)
+    assert st.guard is st.ready
+    g = B.StreamEvent()
+    st.guard, st.used = g, True
+    g.record()
+    st.wait()
+    torch.cuda.synchronize()
+
+
 def test_bitwise_invariants():
     """Outputs are identical bit for bit when physical placement changes and
     when the shared prefix is duplicated instead of shared, and from run to run
