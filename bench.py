@@ -133,7 +133,8 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=30,
+                    help="untimed steps first; the device clock settles over ~20 calls")
     ap.add_argument("--workload", default="prefill", choices=list(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=0,
@@ -234,16 +235,18 @@ def main():
         dev.finish(launches[s], batched=True)
         return p
 
-    for s in range(W):
-        p = step(s)
-    torch.cuda.synchronize()
-    meta = p.meta if W else None
     events = [(B.StreamEvent(timing=True), B.StreamEvent(timing=True)) for _ in range(K)]
     # no garbage-collector pass inside the timed steps: a full collection of
-    # the interpreter's objects takes milliseconds, several steps' worth
+    # the interpreter's objects takes milliseconds, several steps' worth.
+    # Collect before the warm-up, not between it and the timed steps: after
+    # an idle pause of that length the device's power management repeats its
+    # start-up transient (a fast call, then 10-20 calls 5-30 % slower), so
+    # the timed steps would not start from the state the warm-up reached.
     gc.collect()
     gc.freeze()
     gc.disable()
+    for s in range(W):
+        p = step(s)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
