@@ -12,7 +12,11 @@ Prints one JSON line.  ``value`` is the step throughput (prefill and mixed:
 attention TFLOP/s; decode and verify: algorithmic HBM GB/s of the step);
 ``roofline`` is the attention launch alone, timed with HIP events on the
 stream it runs on; ``cpu_baseline`` is the float64 oracle on a bounded sample
-of the same launch, on this host's cores.
+of the same launch, on this host's cores.  A default (prefill) run then
+measures the other configurations the same way, each with its own warm-up,
+timed steps and short oracle sample, under ``workloads`` (decode and verify
+against HBM bandwidth, mixed against bf16 MFMA, tiny float32 against the
+vector ALU).
 """
 from __future__ import annotations
 
@@ -129,6 +133,177 @@ def cpu_baseline(wl, launch, budget_s: float = 12.0):
     return dt, done, flops, threads, sub
 
 
+def run_workload(name, W, K, C, cpu_budget, profile=False):
+    """Warm up W steps, time K steps (HIP events around every attention
+    call), then C cold-cache steps; returns the figures of one workload."""
+    import torch
+    from paper_2605_11232_amd import binding as B, perf, synth
+    from paper_2605_11232_amd.runtime import DeviceReplay, Staging, plan_words_bound, marshal_launch
+
+    wl = synth.workload(name, steps=W + K + C + 2)
+    cfg = wl.cfg
+    dev = DeviceReplay(wl).setup()
+    launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K + C)]
+    # pack each step's token batches (input marshalling) before timing
+    for ln in launches:
+        marshal_launch(ln)
+    L0 = launches[0]
+    T = L0.total_q
+    tdt = dev.tdtype
+    q = torch.from_numpy(L0.q.get()).to("cuda", tdt)
+    k_new = torch.from_numpy(L0.k_new.get()).to("cuda", tdt)
+    v_new = torch.from_numpy(L0.v_new.get()).to("cuda", tdt)
+    out = torch.empty((T, cfg.num_q_heads, cfg.head_dim), dtype=tdt, device="cuda")
+    lse = torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device="cuda")
+    n = len(L0.seq_ids)
+    plan_words = plan_words_bound(cfg, n, T, wl.max_blocks_per_seq)
+    stagings = [Staging("cuda", n, wl.max_blocks_per_seq, T, plan_words) for _ in range(2)]
+    stream = torch.cuda.current_stream()
+
+    kv_memory = {}
+    state = {"scrub": None}
+    scrub_sink = []
+
+    def step(s, record=None):
+        # a timed warm-cache step records the attention call's start event
+        # after the KV append, where it also releases the staging buffer: one
+        # event marker fewer per step than a separate release event
+        share = record is not None and state["scrub"] is None
+        p = dev.prepare_staged(launches[s], stagings[s % 2], q, k_new, v_new, out, lse,
+                               guard=record[0] if share else None)
+        if s == 0 and record is None:
+            # KV memory of the live batch: blocks versus contiguous reservations
+            # of the block-table capacity (outside the timed steps)
+            kv_memory.update(dev.pool.kv_waste(wl.max_blocks_per_seq * cfg.block_size))
+        dev.append(p)
+        if state["scrub"] is not None:
+            # read 1 GiB: L2 and MALL then hold none of the inputs (a read leaves
+            # no dirty lines whose write-back would compete with the call)
+            scrub_sink.append(state["scrub"].sum())
+        if record is not None and not share:
+            record[0].record(stream)
+        dev.attend(p)
+        if record is not None:
+            record[1].record(stream)
+        dev.finish(launches[s], batched=True)
+        return p
+
+    events = [(B.StreamEvent(timing=True), B.StreamEvent(timing=True)) for _ in range(K)]
+    # no garbage-collector pass inside the timed steps: a full collection of
+    # the interpreter's objects takes milliseconds, several steps' worth.
+    # Collect before the warm-up, not between it and the timed steps: after
+    # an idle pause of that length the device's power management repeats its
+    # start-up transient (a fast call, then 10-20 calls 5-30 % slower), so
+    # the timed steps would not start from the state the warm-up reached.
+    gc.collect()
+    gc.freeze()
+    gc.disable()
+    for s in range(W):
+        p = step(s)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        p = step(W + i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gc.enable()
+    gc.unfreeze()
+    meta = {k: np.array(v, copy=True) for k, v in p.meta.items()}
+    per_ms = [a.elapsed_time(b) for a, b in events]
+    attn_ms = float(np.mean(per_ms))
+    cold_ms = None
+    if C:
+        # cold caches: the same call after a 1 GiB read, outside the timed steps
+        state["scrub"] = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
+        cev = [(B.StreamEvent(timing=True), B.StreamEvent(timing=True)) for _ in range(C)]
+        for i in range(C):
+            step(W + K + i, cev[i])
+        torch.cuda.synchronize()
+        cold_ms = float(np.mean([a.elapsed_time(b) for a, b in cev]))
+        state["scrub"] = None
+
+    flops = perf.attention_flops(meta["seq_lens"], meta["cu_seqlens_q"], cfg.num_q_heads,
+                                 cfg.head_dim)
+    attn_bytes = perf.attention_bytes(meta, cfg, unique=True)
+    logical_bytes = perf.attention_bytes(meta, cfg, unique=False)
+    app_bytes = perf.append_bytes(T, cfg)
+    ms = wall / K * 1e3
+    compute_bound = name in ("prefill", "mixed")
+    if cfg.dtype == "f32":
+        peak, unit, bound = perf.MI355X_PEAKS["fp32_vector_tflops"], "TFLOP/s", "alu"
+        work, scale_u = flops, 1e12
+        value = flops / (ms * 1e-3) / 1e12
+    elif compute_bound:
+        peak, unit, bound = perf.MI355X_PEAKS["bf16_tflops"], "TFLOP/s", "mfma"
+        work, scale_u = flops, 1e12
+        value = flops / (ms * 1e-3) / 1e12
+    else:
+        peak, unit, bound = perf.MI355X_PEAKS["hbm_gbs"], "GB/s", "hbm"
+        work, scale_u = attn_bytes, 1e9
+        value = (attn_bytes + app_bytes) / (ms * 1e-3) / 1e9
+    achieved = work / (attn_ms * 1e-3) / scale_u
+    # the timed calls as three consecutive runs: each run's mean call time,
+    # and the median and range of the three (the paper's protocol reports
+    # the median and range of three runs)
+    runs = [float(np.mean(c)) for c in np.array_split(np.asarray(per_ms), 3) if len(c)]
+    res = {
+        "name": name, "cfg": cfg, "requests": len(L0.seq_ids), "query_tokens": T,
+        "flops": flops, "attn_bytes": attn_bytes, "logical_bytes": logical_bytes,
+        "app_bytes": app_bytes, "ms": ms, "value": value, "unit": unit, "bound": bound,
+        "peak": peak, "achieved": achieved, "attn_ms": attn_ms, "per_ms": per_ms, "runs": runs,
+        "run_achieved": [work / (r * 1e-3) / scale_u for r in runs], "kv_memory": kv_memory,
+        "W": W, "K": K,
+    }
+    if cold_ms is not None:
+        cold_ach = work / (cold_ms * 1e-3) / scale_u
+        res["cold"] = {"steps": C, "avg_launch_ms": round(cold_ms, 4),
+                       "achieved": round(cold_ach, 2), "unit": unit,
+                       "frac": round(cold_ach / peak, 4),
+                       "note": "attention call after a 1 GiB device read (L2 and MALL "
+                               "flushed); not part of value or roofline"}
+    del dev, stagings, q, k_new, v_new, out, lse
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    if cpu_budget > 0 and not profile:
+        dt, done, cflops, threads, sub = cpu_baseline(synth.workload(name, steps=2), L0,
+                                                      budget_s=cpu_budget)
+        if compute_bound or cfg.dtype == "f32":
+            cval, cunit = cflops / dt / 1e12, "TFLOP/s"
+        else:
+            cval = perf.attention_bytes(sub, cfg, unique=True) / dt / 1e9
+            cunit = "GB/s"
+        res["cpu_baseline"] = {"value": cval, "unit": cunit, "cores": threads, "kind": "oracle",
+                               "sample": f"float64 oracle attention of the first {done} of "
+                                         f"{len(L0.seq_ids)} requests of the same launch "
+                                         f"(all heads), {dt:.1f} s on {cpu_model()}"}
+    return res
+
+
+def call_summary(res):
+    """Attention-call figures of one workload (the roofline object's body)."""
+    per = np.asarray(res["per_ms"])
+    runs = res["runs"]
+    ra = res["run_achieved"]
+    return {"bound": res["bound"], "achieved": round(res["achieved"], 2), "peak": res["peak"],
+            "unit": res["unit"], "frac": round(res["achieved"] / res["peak"], 4),
+            "traffic": measured_traffic(res["name"]),
+            "traffic_unit": "HBM bytes per call (counters)",
+            "kernel": "pa_attn_" + ("prefill" if res["name"] in ("prefill", "mixed", "tiny")
+                                    else res["name"]),
+            "avg_launch_ms": round(res["attn_ms"], 4),
+            "launch_ms_median": round(float(np.median(per)), 4),
+            "launch_ms_min": round(float(np.min(per)), 4),
+            "launch_ms_max": round(float(np.max(per)), 4),
+            "runs_ms": [round(r, 4) for r in runs],
+            "runs_achieved_median": round(float(np.median(ra)), 2),
+            "runs_achieved_range": [round(float(min(ra)), 2), round(float(max(ra)), 2)],
+            "effective_logical_gbs": round(res["logical_bytes"] / (res["attn_ms"] * 1e-3) / 1e9, 1)}
+
+
+# The other configurations, measured in the same run after the headline.
+SECONDARY = ["decode", "verify", "mixed", "tiny"]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -137,6 +312,14 @@ def main():
                     help="untimed steps first; the device clock settles over ~20 calls")
     ap.add_argument("--workload", default="prefill", choices=list(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="measure only --workload (by default a prefill run also measures "
+                         "the decode, verify, mixed and tiny configurations)")
+    ap.add_argument("--secondary-steps", type=int, default=40,
+                    help="timed steps of each secondary configuration")
+    ap.add_argument("--secondary-warmup", type=int, default=25)
+    ap.add_argument("--secondary-cpu-budget", type=float, default=3.0,
+                    help="seconds of float64 oracle per secondary configuration")
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="run only this many steps without the CPU baseline (profiling)")
     ap.add_argument("--cold-steps", type=int, default=5,
@@ -176,8 +359,6 @@ def main():
         print(json.dumps({"matmul_n": n, "flop_per_launch": 2 * n ** 3, "launches": 5,
                           "checksum": float(z.float().abs().mean())}), flush=True)
         return
-    from paper_2605_11232_amd import binding as B, perf, synth
-    from paper_2605_11232_amd.runtime import DeviceReplay, Staging, plan_words_bound
 
     torch.cuda.set_device(0)
     name = args.workload
@@ -185,158 +366,54 @@ def main():
     C = 0 if args.profile_steps else max(0, args.cold_steps)
     if args.profile_steps:
         W, K = 1, args.profile_steps
-    wl = synth.workload(name, steps=W + K + C + 2)
-    cfg = wl.cfg
-    dev = DeviceReplay(wl).setup()
-    launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K + C)]
-    # pack each step's token batches (input marshalling) before timing
-    from paper_2605_11232_amd.runtime import marshal_launch
-    for ln in launches:
-        marshal_launch(ln)
-    L0 = launches[0]
-    T = L0.total_q
-    tdt = dev.tdtype
-    q = torch.from_numpy(L0.q.get()).to("cuda", tdt)
-    k_new = torch.from_numpy(L0.k_new.get()).to("cuda", tdt)
-    v_new = torch.from_numpy(L0.v_new.get()).to("cuda", tdt)
-    out = torch.empty((T, cfg.num_q_heads, cfg.head_dim), dtype=tdt, device="cuda")
-    lse = torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device="cuda")
-    n = len(L0.seq_ids)
-    plan_words = plan_words_bound(cfg, n, T, wl.max_blocks_per_seq)
-    stagings = [Staging("cuda", n, wl.max_blocks_per_seq, T, plan_words) for _ in range(2)]
-    stream = torch.cuda.current_stream()
-
-    kv_memory = {}
-
-    scrub = None
-    scrub_sink = []
-
-    def step(s, record=None):
-        # a timed warm-cache step records the attention call's start event
-        # after the KV append, where it also releases the staging buffer: one
-        # event marker fewer per step than a separate release event
-        share = record is not None and scrub is None
-        p = dev.prepare_staged(launches[s], stagings[s % 2], q, k_new, v_new, out, lse,
-                               guard=record[0] if share else None)
-        if s == 0 and record is None:
-            # KV memory of the live batch: blocks versus contiguous reservations
-            # of the block-table capacity (outside the timed steps)
-            kv_memory.update(dev.pool.kv_waste(wl.max_blocks_per_seq * cfg.block_size))
-        dev.append(p)
-        if scrub is not None:
-            # read 1 GiB: L2 and MALL then hold none of the inputs (a read leaves
-            # no dirty lines whose write-back would compete with the call)
-            scrub_sink.append(scrub.sum())
-        if record is not None and not share:
-            record[0].record(stream)
-        dev.attend(p)
-        if record is not None:
-            record[1].record(stream)
-        dev.finish(launches[s], batched=True)
-        return p
-
-    events = [(B.StreamEvent(timing=True), B.StreamEvent(timing=True)) for _ in range(K)]
-    # no garbage-collector pass inside the timed steps: a full collection of
-    # the interpreter's objects takes milliseconds, several steps' worth.
-    # Collect before the warm-up, not between it and the timed steps: after
-    # an idle pause of that length the device's power management repeats its
-    # start-up transient (a fast call, then 10-20 calls 5-30 % slower), so
-    # the timed steps would not start from the state the warm-up reached.
-    gc.collect()
-    gc.freeze()
-    gc.disable()
-    for s in range(W):
-        p = step(s)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(K):
-        p = step(W + i, events[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gc.enable()
-    gc.unfreeze()
-    meta = {k: np.array(v, copy=True) for k, v in p.meta.items()}
-    per_ms = [a.elapsed_time(b) for a, b in events]
-    attn_ms = float(np.mean(per_ms))
-    cold_ms = None
-    if C:
-        # cold caches: the same call after a 1 GiB read, outside the timed steps
-        scrub = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
-        cev = [(B.StreamEvent(timing=True), B.StreamEvent(timing=True)) for _ in range(C)]
-        for i in range(C):
-            step(W + K + i, cev[i])
-        torch.cuda.synchronize()
-        cold_ms = float(np.mean([a.elapsed_time(b) for a, b in cev]))
-        scrub = None
-
-    flops = perf.attention_flops(meta["seq_lens"], meta["cu_seqlens_q"], cfg.num_q_heads,
-                                 cfg.head_dim)
-    attn_bytes = perf.attention_bytes(meta, cfg, unique=True)
-    logical_bytes = perf.attention_bytes(meta, cfg, unique=False)
-    app_bytes = perf.append_bytes(T, cfg)
-    ms = wall / K * 1e3
-    compute_bound = name in ("prefill", "mixed")
-    if cfg.dtype == "f32":
-        peak, unit, bound = perf.MI355X_PEAKS["fp32_vector_tflops"], "TFLOP/s", "alu"
-        achieved = flops / (attn_ms * 1e-3) / 1e12
-        value, vunit = flops / (ms * 1e-3) / 1e12, "TFLOP/s"
-    elif compute_bound:
-        peak, unit, bound = perf.MI355X_PEAKS["bf16_tflops"], "TFLOP/s", "mfma"
-        achieved = flops / (attn_ms * 1e-3) / 1e12
-        value, vunit = flops / (ms * 1e-3) / 1e12, "TFLOP/s"
-    else:
-        peak, unit, bound = perf.MI355X_PEAKS["hbm_gbs"], "GB/s", "hbm"
-        achieved = attn_bytes / (attn_ms * 1e-3) / 1e9
-        value, vunit = (attn_bytes + app_bytes) / (ms * 1e-3) / 1e9, "GB/s"
-
+    profile = bool(args.profile_steps)
+    budget = 0.0 if args.no_cpu_baseline else 10.0
+    res = run_workload(name, W, K, C, budget, profile)
+    cfg = res["cfg"]
     rec = {
         "metric": METRIC,
-        "value": round(value, 3),
-        "unit": vunit,
+        "value": round(res["value"], 3),
+        "unit": res["unit"],
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
-        "ms_per_step": round(ms, 4),
+        "ms_per_step": round(res["ms"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
         "config": {"workload": DESCRIPTIONS[name], "name": name,
-                   "requests": len(L0.seq_ids), "query_tokens": T,
-                   "attn_flops": flops, "attn_unique_bytes": attn_bytes,
-                   "attn_logical_bytes": logical_bytes, "append_bytes": app_bytes,
+                   "requests": res["requests"], "query_tokens": res["query_tokens"],
+                   "attn_flops": res["flops"], "attn_unique_bytes": res["attn_bytes"],
+                   "attn_logical_bytes": res["logical_bytes"], "append_bytes": res["app_bytes"],
                    "parallelism": "single GPU"},
-        "kv_memory": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in kv_memory.items()},
-        "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-                     "frac": round(achieved / peak, 4), "traffic": measured_traffic(name),
-                     "traffic_unit": "HBM bytes per call (counters)",
-                     "kernel": "pa_attn_" + ("prefill" if name in ("prefill", "mixed", "tiny") else name),
-                     "avg_launch_ms": round(attn_ms, 4),
-                     "launch_ms_median": round(float(np.median(per_ms)), 4),
-                     "launch_ms_min": round(float(np.min(per_ms)), 4),
-                     "launch_ms_max": round(float(np.max(per_ms)), 4),
-                     "effective_logical_gbs": round(logical_bytes / (attn_ms * 1e-3) / 1e9, 1)},
+        "kv_memory": {k: (round(v, 4) if isinstance(v, float) else v)
+                      for k, v in res["kv_memory"].items()},
+        "roofline": call_summary(res),
     }
-    if cold_ms is not None:
-        cold_ach = (flops if unit == "TFLOP/s" else attn_bytes) / (cold_ms * 1e-3) / (
-            1e12 if unit == "TFLOP/s" else 1e9)
-        rec["cold_caches"] = {"steps": C, "avg_launch_ms": round(cold_ms, 4),
-                              "achieved": round(cold_ach, 2), "unit": unit,
-                              "frac": round(cold_ach / peak, 4),
-                              "note": "attention call after a 1 GiB device read (L2 and MALL "
-                                      "flushed); not part of value or roofline"}
-    if not args.no_cpu_baseline and not args.profile_steps:
-        dt, done, cflops, threads, sub = cpu_baseline(synth.workload(name, steps=2), L0)
-        if compute_bound or cfg.dtype == "f32":
-            cval, cunit = cflops / dt / 1e12, "TFLOP/s"
-        else:
-            cval = perf.attention_bytes(sub, cfg, unique=True) / dt / 1e9
-            cunit = "GB/s"
-        rec["cpu_baseline"] = {"value": cval, "unit": cunit, "cores": threads, "kind": "oracle",
-                               "sample": f"float64 oracle attention of the first {done} of "
-                                         f"{len(L0.seq_ids)} requests of the same launch "
-                                         f"(all heads), {dt:.1f} s on {cpu_model()}"}
+    if "cold" in res:
+        rec["cold_caches"] = res["cold"]
+    if "cpu_baseline" in res:
+        rec["cpu_baseline"] = res["cpu_baseline"]
+    if name == "prefill" and not args.no_secondary and not profile:
+        # every other configuration, each its own warm-up and timed steps;
+        # its figures are per attention call, like the roofline object
+        wls = {}
+        for other in SECONDARY:
+            print(f"[bench] {other}", file=sys.stderr, flush=True)
+            r2 = run_workload(other, args.secondary_warmup, args.secondary_steps, 0,
+                              0.0 if args.no_cpu_baseline else args.secondary_cpu_budget)
+            w = {"workload": DESCRIPTIONS[other], "dtype": r2["cfg"].dtype,
+                 "requests": r2["requests"], "query_tokens": r2["query_tokens"],
+                 "attn_flops": r2["flops"], "attn_unique_bytes": r2["attn_bytes"],
+                 "steps": r2["K"], "warmup": r2["W"], "ms_per_step": round(r2["ms"], 4),
+                 "step_value": round(r2["value"], 3), "step_unit": r2["unit"],
+                 "roofline": call_summary(r2)}
+            if "cpu_baseline" in r2:
+                w["cpu_baseline"] = r2["cpu_baseline"]
+            wls[other] = w
+        rec["workloads"] = wls
     print(json.dumps(rec), flush=True)
 
 

@@ -8,9 +8,9 @@
  * through a per-request block table (Section 2, PagedAttention), and blocks
  * holding a matching prefix are reused instead of recomputed (Section 2,
  * Automatic Prefix Caching; Section 3: shared policy prefixes should not be
- * recomputed; Section 5.3).  Attention runs for suffix prefill (per-case
+ * recomputed; Section 5.4).  Attention runs for suffix prefill (per-case
  * evidence against the cached prefix plus its own causal context), decode,
- * and speculative verification of draft tokens (Section 2 and Section 5.2,
+ * and speculative verification of draft tokens (Section 2 and Section 5.3,
  * EAGLE-style speculative decoding), including chunked-prefill chunks mixed
  * with decode tokens in one launch (Section 5.2: split prefills under a
  * batched-token budget; Section 6, Table "playbook": long prefills blocking
@@ -116,7 +116,7 @@ int pa_seq_truncate(pa_pool* pool, int64_t seq_id, int32_t new_len);
 int pa_seq_free(pa_pool* pool, int64_t seq_id);
 
 /* Least-recently-used eviction of idle cached blocks (paper: Section 2, APC
- * keeps reusable prefix blocks resident; Section 5.3, a prefix identical
+ * keeps reusable prefix blocks resident; Section 5.4, a prefix identical
  * across many requests stays hot).  Off by default: an admission or extension
  * needing more blocks than the free list holds then fails with
  * PA_ERR_NO_BLOCKS.  On: the free list is used first, then idle cached blocks
@@ -215,7 +215,7 @@ int pa_build_metadata(const pa_pool* pool, int32_t n_seqs, const int64_t* seq_id
                       int32_t* seq_lens, int32_t* cu_seqlens_q, int32_t* slot_mapping,
                       int64_t slot_capacity);
 
-/* Adapter-first, length-bucketed batch forming (paper: Section 6,
+/* Adapter-first, length-bucketed batch forming (paper: Section 5.6,
  * "Multi-Adapter and Length-Aware Batching", and Table "casec_adapter"): item
  * i is (adapter_ids[i], prompt_lens[i], i).  Items are grouped by adapter
  * (groups in the order of their first item) and each group is split into
@@ -250,7 +250,7 @@ typedef struct pa_plan_info {
   int32_t n_q;             /* query tokens per sequence (decode 1, verify n_q)    */
   int32_t n_shared_items;  /* shared-prefix (cascade) items, one workgroup each   */
   int32_t n_tile_items;    /* 128-row work items (one workgroup each)             */
-  int32_t n_row_items;     /* <=48-row work items (one wavefront each)            */
+  int32_t n_row_items;     /* <=32-row work items (one wavefront each)            */
   int32_t n_groups;        /* split groups the merge step combines                */
   int32_t n_merge_rows;    /* (token, head) rows produced by the merge step       */
   int32_t grid;            /* workgroups of the attention launch                  */
@@ -258,6 +258,15 @@ typedef struct pa_plan_info {
   int32_t reserved;
   int64_t plan_words;      /* int32 words of the plan array                       */
   int64_t workspace_bytes; /* device scratch the attention call needs             */
+  /* The launch shape the plan was built for; the attention calls reject a
+   * call whose arguments differ. */
+  int32_t n_seqs;
+  int32_t total_q;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t dtype;
+  int64_t partial_rows;    /* float32 partial rows in the workspace               */
 } pa_plan_info;
 
 /* Split one attention launch into work items from HOST copies of seq_lens,
@@ -280,6 +289,24 @@ int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int32_t* seq_l
                  int32_t max_blocks_per_seq, int32_t num_q_heads, int32_t num_kv_heads,
                  int32_t head_dim, int32_t block_size, int32_t dtype, int32_t num_cus,
                  int32_t* plan, int64_t plan_capacity, pa_plan_info* info);
+
+/* Upper bound on the split-K workspace (float32 partial outputs and their
+ * log-sum-exps, merged by the attention call) of any plan pa_attn_plan builds
+ * for a launch of total_q query tokens whose sequences are at most
+ * max_seq_len keys long, at num_q_heads query heads and head_dim (paper:
+ * Section 5.3, decode of short structured outputs, where long key ranges are
+ * split across wavefronts to stream the cache).  Lets a caller size one
+ * workspace before any plan exists; a plan's own need, info->workspace_bytes,
+ * is never larger.  Host only, allocates nothing.  *bytes receives the bound.
+ * Errors: PA_ERR_ARG (negative size, NULL bytes), PA_ERR_UNSUPPORTED
+ * (head_dim). */
+int pa_attn_workspace_size(int32_t total_q, int32_t num_q_heads, int32_t head_dim,
+                           int32_t max_seq_len, size_t* bytes);
+
+/* The same bound for a decode launch of n_seqs sequences (one query token
+ * each): pa_attn_workspace_size(n_seqs, ...). */
+int pa_attn_decode_workspace_size(int32_t n_seqs, int32_t num_q_heads, int32_t head_dim,
+                                  int32_t max_seq_len, size_t* bytes);
 
 /* The host side of one serving step's launch in one call (paper: Section 2,
  * block tables and Automatic Prefix Caching; Section 5.2, one batched launch
@@ -311,12 +338,18 @@ int pa_prepare_launch(pa_pool* pool, int32_t n_ops, const int32_t* ops,
  * Device operations.                                                         *
  * ------------------------------------------------------------------------ */
 
-/* Store the keys/values of n_tokens new tokens into their cache slots:
+/* Store the keys/values of n_tokens new tokens into their cache slots (paper:
+ * Section 2, PagedAttention keeps a request's KV in blocks addressed through
+ * its block table; a token's KV is written once and then reused by every
+ * later step and, for cached prefix blocks, by every request that hits them):
  * k_cache[s/bs][h][s%bs][:] = k_new[i][h][:] and
  * v_cache[s/bs][h][:][s%bs] = v_new[i][h][:] for s = slot_mapping[i].
  * k_new, v_new: [n_tokens][num_kv_heads][head_dim] (dtype).  A slot outside
- * [0, num_blocks*block_size) skips its token (use -1 for padding).
- * Bit-exact copy.  Errors: PA_ERR_ARG, PA_ERR_UNSUPPORTED, PA_ERR_LAUNCH. */
+ * [0, num_blocks*block_size) skips its token (use -1 for padding).  All
+ * pointers are caller-owned device memory; asynchronous on stream; allocates
+ * nothing.  Bit-exact copy.  Errors: PA_ERR_ARG (NULL pointer with tokens to
+ * store, negative n_tokens, bad sizes), PA_ERR_UNSUPPORTED (head_dim,
+ * block_size, dtype), PA_ERR_LAUNCH. */
 int pa_kv_append(const void* k_new, const void* v_new, const int32_t* slot_mapping,
                  int32_t n_tokens, void* k_cache, void* v_cache, int32_t num_blocks,
                  int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t dtype,
@@ -334,8 +367,17 @@ int pa_kv_append(const void* k_new, const void* v_new, const int32_t* slot_mappi
  * range not device memory); PA_ERR_LAUNCH. */
 int pa_stage_upload(void* dst, const void* src, int64_t bytes, void* stream);
 
-/* Paged attention over a prefix-shared KV cache.  For sequence r, q-head h
- * and its query i at logical position a = seq_lens[r] - q_len_r + i:
+/* Paged attention over a prefix-shared KV cache (paper: Section 2,
+ * PagedAttention's block tables and Automatic Prefix Caching; Section 3,
+ * cached shared policy prefixes give the result of recomputing them, so
+ * serving a suffix against cached prefix blocks is exact attention over the
+ * whole logical sequence).  pa_attn_prefill serves suffix prefill of per-case
+ * evidence against the cached prefix and, with a plan mixing prefill chunks
+ * and decode tokens, the mixed launch (Section 5.2, split prefills under a
+ * batched-token budget; Section 6, Table "playbook": long prefills blocking
+ * short decodes).
+ * For sequence r, q-head h and its query i at logical position
+ * a = seq_lens[r] - q_len_r + i:
  *   out = sum_{t<=a} softmax_t(scale * q . k_t) v_t,   k_t, v_t from kv-head
  *   h / G of the block table row r,
  *   lse = log sum_{t<=a} exp(scale * q . k_t).
@@ -346,8 +388,15 @@ int pa_stage_upload(void* dst, const void* src, int64_t bytes, void* stream);
  * workspace of at least info->workspace_bytes bytes (any contents) or NULL if
  * that is 0.  Block ids must lie in [0, num_blocks); out-of-range ids are
  * clamped so no access leaves the cache (results are then undefined).
- * The three entry points differ only in the plan kind they accept.
- * Errors: PA_ERR_ARG, PA_ERR_UNSUPPORTED, PA_ERR_LAUNCH. */
+ * Every pointer is caller-owned device memory (info: host); the call
+ * allocates nothing, writes only out, lse and the workspace, and is
+ * asynchronous on stream.  The three entry points differ only in the plan
+ * kind they accept.
+ * Errors (checked before anything is launched): PA_ERR_ARG (NULL pointer with
+ * work to do, a plan of another kind, n_seqs / total_q / num_q_heads /
+ * num_kv_heads / head_dim / dtype other than the plan's info records, a
+ * workspace smaller than info->workspace_bytes), PA_ERR_UNSUPPORTED (head_dim,
+ * block_size, dtype), PA_ERR_LAUNCH (the runtime rejected the launch). */
 int pa_attn_prefill(const void* q, const void* k_cache, const void* v_cache, int32_t num_blocks,
                     const int32_t* block_table, int32_t max_blocks_per_seq,
                     const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,
@@ -356,7 +405,10 @@ int pa_attn_prefill(const void* q, const void* k_cache, const void* v_cache, int
                     const pa_plan_info* info, void* workspace, size_t workspace_bytes,
                     void* out, float* lse, void* stream);
 
-/* Decode: one query token per sequence (plan kind PA_KIND_DECODE). */
+/* Decode: one query token per sequence (plan kind PA_KIND_DECODE); paper:
+ * Section 5.3 (short structured outputs, decode-time control) and Section 3,
+ * Table "phenotype" (long input, short JSON output).  Arguments, layouts,
+ * ownership and errors as pa_attn_prefill. */
 int pa_attn_decode(const void* q, const void* k_cache, const void* v_cache, int32_t num_blocks,
                    const int32_t* block_table, int32_t max_blocks_per_seq,
                    const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,
@@ -367,7 +419,10 @@ int pa_attn_decode(const void* q, const void* k_cache, const void* v_cache, int3
 
 /* Speculative verification: n_q = info->n_q query tokens per sequence (the
  * draft tokens and the bonus position), causal among themselves (plan kind
- * PA_KIND_VERIFY). */
+ * PA_KIND_VERIFY); paper: Section 5.3 and Table "caseb" (EAGLE-style
+ * speculative decoding, whose target-model pass scores every draft token
+ * against the cached context at once), Section 2 (speculative decoding).
+ * Arguments, layouts, ownership and errors as pa_attn_prefill. */
 int pa_attn_verify(const void* q, const void* k_cache, const void* v_cache, int32_t num_blocks,
                    const int32_t* block_table, int32_t max_blocks_per_seq,
                    const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,

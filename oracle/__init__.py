@@ -13,7 +13,7 @@ Contents
                metadata (paper: Section 2 on PagedAttention's block-granular,
                virtual-memory-like KV layout and on Automatic Prefix Caching
                reusing the KV blocks of matching prefixes; Section 3, shared
-               policy prefixes are not recomputed; Section 5.3).
+               policy prefixes are not recomputed; Section 5.4).
 ``attention``  float64 causal softmax(q k^T / sqrt(D)) v over each request's
                logical token sequence, rebuilt from its block table, plus the
                oracle's own paged KV store (the same definition of the cache

@@ -4,7 +4,7 @@ Follows the paper's description of the reuse plane: KV memory is managed in
 fixed-size blocks addressed through a per-request block table (Section 2,
 PagedAttention's virtual-memory-inspired KV layout), and Automatic Prefix
 Caching lets a request reuse the KV blocks of a matching prefix (Section 2;
-Section 3: shared policy prefixes should not be recomputed; Section 5.3: the
+Section 3: shared policy prefixes should not be recomputed; Section 5.4: the
 system prompt, policy text and schema stay identical across many requests).
 The paper states no procedure, so the rules below are the readings recorded in
 the design notes:

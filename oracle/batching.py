@@ -1,6 +1,6 @@
 """Adapter-first, length-bucketed batch forming (test infrastructure only).
 
-Follows the dispatch procedure of the paper's Section 6 ("Multi-Adapter and
+Follows the dispatch procedure of the paper's Section 5.6 ("Multi-Adapter and
 Length-Aware Batching"): each prompt of a request is taken as (adapter id,
 prompt length, original index); prompts are grouped by adapter, each adapter
 group is sub-bucketed by length range, every bucket is executed as one batch,

@@ -29,7 +29,7 @@ EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy
            "pa_pool_free_list", "pa_build_metadata", "pa_attn_plan", "pa_kv_append",
            "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify", "pa_pool_set_eviction",
            "pa_pool_get_stats", "pa_pool_kv_waste", "pa_form_batches", "pa_prepare_launch",
-           "pa_stage_upload"]
+           "pa_stage_upload", "pa_attn_workspace_size", "pa_attn_decode_workspace_size"]
 
 
 class PaError(RuntimeError):
@@ -55,7 +55,10 @@ class PlanInfo(C.Structure):
     _fields_ = [("kind", C.c_int32), ("n_q", C.c_int32), ("n_shared_items", C.c_int32),
                 ("n_tile_items", C.c_int32), ("n_row_items", C.c_int32), ("n_groups", C.c_int32),
                 ("n_merge_rows", C.c_int32), ("grid", C.c_int32), ("variant", C.c_int32),
-                ("reserved", C.c_int32), ("plan_words", C.c_int64), ("workspace_bytes", C.c_int64)]
+                ("reserved", C.c_int32), ("plan_words", C.c_int64), ("workspace_bytes", C.c_int64),
+                ("n_seqs", C.c_int32), ("total_q", C.c_int32), ("num_q_heads", C.c_int32),
+                ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("dtype", C.c_int32),
+                ("partial_rows", C.c_int64)]
 
 
 _lib = None
@@ -96,6 +99,8 @@ def lib():
                                    i32, _I32P, i64, C.POINTER(PlanInfo)]),
         "pa_kv_append": (C.c_int, [_P, _P, _P, i32, _P, _P, i32, i32, i32, i32, i32, _P]),
         "pa_stage_upload": (C.c_int, [_P, _P, i64, _P]),
+        "pa_attn_workspace_size": (C.c_int, [i32, i32, i32, i32, C.POINTER(C.c_size_t)]),
+        "pa_attn_decode_workspace_size": (C.c_int, [i32, i32, i32, i32, C.POINTER(C.c_size_t)]),
         "pa_pool_set_eviction": (C.c_int, [_P, i32]),
         "pa_pool_get_stats": (C.c_int, [_P, C.POINTER(PoolStats)]),
         "pa_pool_kv_waste": (C.c_int, [_P, i32, C.POINTER(KvWaste)]),
@@ -407,6 +412,17 @@ def plan(kind: int, n_q: int, seq_lens, cu_seqlens_q, num_q_heads: int, num_kv_h
     return arr[:info.plan_words], info
 
 
+def workspace_size(total_q: int, num_q_heads: int, head_dim: int, max_seq_len: int,
+                   decode: bool = False) -> int:
+    """Bound on the split-K workspace of any plan for such a launch
+    (pa_attn_workspace_size, or pa_attn_decode_workspace_size with total_q
+    the number of decode sequences)."""
+    n = C.c_size_t(0)
+    fn = lib().pa_attn_decode_workspace_size if decode else lib().pa_attn_workspace_size
+    _check(fn(int(total_q), int(num_q_heads), int(head_dim), int(max_seq_len), C.byref(n)))
+    return int(n.value)
+
+
 def _dptr(t) -> int:
     return 0 if t is None else int(t.data_ptr())
 
@@ -519,3 +535,4 @@ def attention(kind: int, q, k_cache, v_cache, block_table, seq_lens, cu_seqlens_
               int(block_table.shape[1]), _dptr(seq_lens), _dptr(cu_seqlens_q), n_seqs, total_q,
               hq, hkv, d, bs, float(scale), _dtype_code(q), _dptr(plan_dev), C.byref(info),
               _dptr(workspace), ws_bytes, _dptr(out), _dptr(lse), _stream(stream)))
+

@@ -62,6 +62,16 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
   if (info->kind != want_kind)
     return fail(PA_ERR_ARG, "%s: plan was built for kind %d, this call needs kind %d", fn,
                 info->kind, want_kind);
+  // the plan's items index sequences, heads and rows of the launch it was
+  // built for: any other shape could send them past the caller's buffers
+  if (info->n_seqs != n_seqs || info->total_q != total_q || info->num_q_heads != num_q_heads ||
+      info->num_kv_heads != num_kv_heads || info->head_dim != head_dim || info->dtype != dtype)
+    return fail(PA_ERR_ARG,
+                "%s: plan was built for n_seqs %d, total_q %d, heads %d/%d, head_dim %d, "
+                "dtype %d; this call has n_seqs %d, total_q %d, heads %d/%d, head_dim %d, "
+                "dtype %d", fn, info->n_seqs, info->total_q, info->num_q_heads,
+                info->num_kv_heads, info->head_dim, info->dtype, n_seqs, total_q, num_q_heads,
+                num_kv_heads, head_dim, dtype);
   if (total_q == 0 || n_seqs == 0) return PA_OK;
   if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !cu_seqlens_q || !out)
     return fail(PA_ERR_ARG, "%s: NULL device pointer", fn);
@@ -74,13 +84,15 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
     if (!plan) return fail(PA_ERR_ARG, "%s: NULL plan", fn);
     if ((info->variant & ~kVariantWideRows) != kVariantBf16 || info->grid < 0 || info->n_groups < 0 ||
         info->n_tile_items < 0 || info->n_shared_items < 0 ||
-        int64_t(info->n_tile_items) + info->n_shared_items > info->grid)
+        int64_t(info->n_tile_items) + info->n_shared_items > info->grid ||
+        info->partial_rows < 0 ||
+        info->workspace_bytes != info->partial_rows * int64_t(head_dim + 1) * 4)
       return fail(PA_ERR_ARG, "%s: corrupt plan info", fn);
     if (static_cast<int64_t>(workspace_bytes) < info->workspace_bytes ||
         (info->workspace_bytes > 0 && !workspace))
       return fail(PA_ERR_ARG, "%s: workspace of %zu bytes, plan needs %lld", fn, workspace_bytes,
                   (long long)info->workspace_bytes);
-    const int64_t partial_rows = info->workspace_bytes / (int64_t(head_dim + 1) * 4);
+    const int64_t partial_rows = info->partial_rows;
     rc = dev::launch_attn_bf16(q, k_cache, v_cache, num_blocks, block_table, max_blocks_per_seq,
                                seq_lens, cu_seqlens_q, num_q_heads, num_kv_heads, head_dim, scale,
                                plan, info->grid, info->n_shared_items + info->n_tile_items,

@@ -1,5 +1,5 @@
 // Adapter-first, length-bucketed batch forming for a request that carries
-// prompts for several adapters of one base model (paper: Section 6,
+// prompts for several adapters of one base model (paper: Section 5.6,
 // "Multi-Adapter and Length-Aware Batching"; Table "casec_adapter").  Each
 // item is (adapter id, prompt length, original index); items are grouped by
 // adapter, each adapter group is split into length buckets, every bucket is

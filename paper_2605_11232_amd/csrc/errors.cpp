@@ -24,4 +24,4 @@ void clear_error() { g_last_error.clear(); }
 }  // namespace pa
 
 extern "C" const char* pa_last_error(void) { return g_last_error.c_str(); }
-extern "C" int32_t pa_abi_version(void) { return 1; }
+extern "C" int32_t pa_abi_version(void) { return 2; }

@@ -13,7 +13,7 @@
 //
 // Shared prefixes (cascade): few-row sequences whose block tables start
 // with the same blocks read the same prefix keys (Section 2, Automatic Prefix
-// Caching; Section 5.3, the same policy prefix across thousands of requests).
+// Caching; Section 5.4, the same policy prefix across thousands of requests).
 // Their attention over the shared keys is computed once, as 128-row MFMA tiles
 // of all the group's query rows (every such query sees every shared key), and
 // merged with each sequence's private-key part by log-sum-exp: the prefix is
@@ -42,6 +42,7 @@ namespace {
 constexpr int kXcds = 8;
 constexpr int64_t kRowWavesPerCu = 16;      // row-item split target
 constexpr int64_t kPrivateTileKeys = 2048;  // most private keys a few-row tile item covers
+constexpr int64_t kMinRowKeys = 256;        // fewest keys of a split row item
 
 using Rec = std::array<int32_t, pa::kItemWords>;
 
@@ -239,7 +240,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       if (is_row(r) && !on_tiles(r))
         row_keys += int64_t(seq_lens[r] - kstart[r]) * num_kv_heads;
     const int64_t target_waves = int64_t(num_cus) * kRowWavesPerCu;
-    int64_t chunk = std::max<int64_t>(256, cdiv(row_keys, std::max<int64_t>(1, target_waves)));
+    int64_t chunk = std::max<int64_t>(kMinRowKeys, cdiv(row_keys, std::max<int64_t>(1, target_waves)));
     chunk = cdiv(chunk, pa::kKeyStep) * pa::kKeyStep;
     // a row item's block ids fit one wavefront (64 lanes): at most 1024 keys
     chunk = std::min<int64_t>(chunk, int64_t(pa::kRowItemBlocks) * block_size);
@@ -410,6 +411,13 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   info->variant = dtype == PA_F32 ? 0 : (pa::kVariantBf16 | (wide ? pa::kVariantWideRows : 0));
   info->plan_words = words;
   info->workspace_bytes = partial_rows * int64_t(head_dim + 1) * int64_t(sizeof(float));
+  info->n_seqs = n_seqs;
+  info->total_q = total_q;
+  info->num_q_heads = num_q_heads;
+  info->num_kv_heads = num_kv_heads;
+  info->head_dim = head_dim;
+  info->dtype = dtype;
+  info->partial_rows = partial_rows;
   if (!plan) return PA_OK;
   if (plan_capacity < words)
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: plan capacity %lld < %lld words",
@@ -473,4 +481,44 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       }
   }
   return PA_OK;
+}
+
+// Workspace bound.  A sequence with split keys writes one partial row per
+// (query row, part); its parts are its private key ranges (at least
+// kMinRowKeys keys each, kPrivateTileKeys for tile-run private parts) plus
+// its shared prefix's key chunks (at least kSharedChunk / 2 keys each, and
+// never more than cdiv(shared keys, kSharedChunk)).  Both counts grow with
+// the key count, so a sequence of at most L keys has at most
+// cdiv(L, kMinRowKeys) + cdiv(L, kSharedChunk) parts (no shared chunk when
+// L <= kSharedMinKeys), and a query token has num_q_heads rows.
+namespace {
+int workspace_bound(const char* fn, int32_t total_q, int32_t num_q_heads, int32_t head_dim,
+                    int32_t max_seq_len, size_t* bytes) {
+  pa::clear_error();
+  if (!bytes || total_q < 0 || num_q_heads < 0 || max_seq_len < 0)
+    return pa::fail(PA_ERR_ARG, "%s: NULL or negative argument", fn);
+  if (head_dim != 64 && head_dim != 128)
+    return pa::fail(PA_ERR_UNSUPPORTED, "%s: head_dim %d (supported: 64, 128)", fn, head_dim);
+  // a shared prefix needs kSharedMinKeys keys and leaves at least one private key
+  const int64_t shared_parts =
+      max_seq_len > pa::kSharedMinKeys ? cdiv(max_seq_len, pa::kSharedChunk) : 0;
+  const int64_t parts = cdiv(max_seq_len, kMinRowKeys) + shared_parts;
+  // a sequence with a single part writes no partial rows
+  const int64_t rows = parts > 1 ? int64_t(total_q) * num_q_heads * parts : 0;
+  *bytes = size_t(rows) * size_t(head_dim + 1) * sizeof(float);
+  return PA_OK;
+}
+}  // namespace
+
+extern "C" int pa_attn_workspace_size(int32_t total_q, int32_t num_q_heads, int32_t head_dim,
+                                      int32_t max_seq_len, size_t* bytes) {
+  return workspace_bound("pa_attn_workspace_size", total_q, num_q_heads, head_dim, max_seq_len,
+                         bytes);
+}
+
+extern "C" int pa_attn_decode_workspace_size(int32_t n_seqs, int32_t num_q_heads,
+                                             int32_t head_dim, int32_t max_seq_len,
+                                             size_t* bytes) {
+  return workspace_bound("pa_attn_decode_workspace_size", n_seqs, num_q_heads, head_dim,
+                         max_seq_len, bytes);
 }

@@ -4,7 +4,7 @@
 // Paper: Section 2 (PagedAttention's block-granular KV layout addressed through
 // a per-request block table; Automatic Prefix Caching reuses the KV blocks of
 // matching prefixes), Section 3 (shared policy prefixes are not recomputed),
-// Section 5.3 (prefixes identical across thousands of requests).
+// Section 5.4 (prefixes identical across thousands of requests).
 //
 // A cached block is identified by (predecessor block, its block_size tokens).
 // Because a block is cached only when its predecessor is cached, that pair

@@ -231,10 +231,11 @@ def _tiny(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
                     {"prefix": P, "suffix": S.tolist(), "decode_steps": n_dec})
 
 
-def _prefill(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
+def _prefill(cfg: AttnConfig, scale: float = 1.0, steps: int = 1,
+             requests: Optional[int] = None) -> Workload:
     """Suffix prefill of per-case evidence against one cached policy prefix."""
     s, bs = cfg.seed, cfg.block_size
-    R = max(1, int(round(64 * scale)))
+    R = requests or max(1, int(round(64 * scale)))
     P = max(bs, int(round(2048 * scale / bs)) * bs) if scale < 1 else 2048
     lo, hi = (256, 1024) if scale >= 1 else (max(1, int(256 * scale)), max(2, int(1024 * scale)))
     S = rng(s, TAG_LEN).integers(lo, hi + 1, size=R)
@@ -256,10 +257,11 @@ def _prefill(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
                     {"prefix": P, "suffix": S.tolist()})
 
 
-def _decode(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
+def _decode(cfg: AttnConfig, scale: float = 1.0, steps: int = 1,
+            requests: Optional[int] = None) -> Workload:
     """One decode token per sequence over prefix + evidence + generated tokens."""
     s, bs = cfg.seed, cfg.block_size
-    R = max(1, int(round(256 * scale)))
+    R = requests or max(1, int(round(256 * scale)))
     P = 2048 if scale >= 1 else max(bs, int(round(2048 * scale / bs)) * bs)
     lo, hi = (256, 1024) if scale >= 1 else (max(1, int(256 * scale)), max(2, int(1024 * scale)))
     S = rng(s, TAG_LEN, 0).integers(lo, hi + 1, size=R)
@@ -295,11 +297,12 @@ def zipf_probs(n: int, s: float = ZIPF_S) -> np.ndarray:
     return w / w.sum()
 
 
-def _mixed(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
+def _mixed(cfg: AttnConfig, scale: float = 1.0, steps: int = 1,
+           requests: Optional[int] = None) -> Workload:
     """Chunked-prefill chunks and decode tokens of many requests in one launch,
     over four cached prefixes chosen with Zipf(1.1) popularity."""
     s, bs = cfg.seed, cfg.block_size
-    R = max(2, int(round(512 * scale)))
+    R = requests or max(2, int(round(512 * scale)))
     n_chunk_req = max(1, R // 8)
     C = 512 if scale >= 1 else max(bs, int(round(512 * scale)))
     plens = [1024, 2048, 4096, 8192] if scale >= 1 else [max(bs, int(round(x * scale / bs)) * bs)
@@ -365,11 +368,12 @@ def _mixed(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
                      "chunk": C})
 
 
-def _verify(cfg: AttnConfig, scale: float = 1.0, steps: int = 1) -> Workload:
+def _verify(cfg: AttnConfig, scale: float = 1.0, steps: int = 1,
+            requests: Optional[int] = None) -> Workload:
     """Speculative verification: 4 draft tokens + 1 per request over a long
     shared prefix and a long cached private suffix, causal among the drafts."""
     s, bs = cfg.seed, cfg.block_size
-    R = max(1, int(round(32 * scale)))
+    R = requests or max(1, int(round(32 * scale)))
     P = 16384 if scale >= 1 else max(bs, int(round(16384 * scale / bs)) * bs)
     Sx = 4096 if scale >= 1 else max(1, int(round(4096 * scale)))
     NQ = 5
@@ -425,10 +429,15 @@ _BUILDERS = {"tiny": _tiny, "prefill": _prefill, "decode": _decode,
              "mixed": _mixed, "verify": _verify, "evict": _evict}
 
 
-def workload(name: str, scale: float = 1.0, steps: int = 1, **overrides) -> Workload:
+def workload(name: str, scale: float = 1.0, steps: int = 1, requests: Optional[int] = None,
+             **overrides) -> Workload:
     """Build the named workload.  ``scale < 1`` shrinks request counts and
-    lengths for parity tests (same recipe, same seeds); ``steps`` sizes the
+    lengths for parity tests (same recipe, same seeds); ``requests`` sets the
+    request count alone (prefill, decode, mixed, verify: the first requests
+    of the same draws at the given scale's lengths); ``steps`` sizes the
     block pool for that many repeated launches; ``overrides`` replace config
-    fields (e.g. ``dtype``)."""
+    fields (e.g. ``dtype``, ``head_dim``)."""
     cfg = dataclasses.replace(CONFIGS[name], **overrides) if overrides else CONFIGS[name]
+    if requests is not None:
+        return _BUILDERS[name](cfg, scale, steps, requests=requests)
     return _BUILDERS[name](cfg, scale, steps)

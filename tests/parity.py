@@ -3,6 +3,7 @@ oracle and through libpa, compare tables bit for bit, the appended cache bit
 for bit, and attention outputs within the stated tolerance."""
 from __future__ import annotations
 
+import ctypes as C
 import sys
 
 import numpy as np
@@ -56,19 +57,22 @@ def compare_cache(dev: DeviceReplay, prep, k_new, v_new):
 
 
 def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, label="",
-               staged=False, stage_kernel=True):
+               staged=False, stage_kernel=True, cascade=True):
     """Replay ``wl`` through both; returns per-launch normalized errors.
     ``staged``: the device side runs the benchmark's path (one library call
     for pool operations, metadata and plan into alternating pinned staging
     buffers, one upload each, a reused workspace, odd launches released by a
     caller's event; ``stage_kernel``: the upload by the library's kernel, else
-    by a copy-engine copy)."""
+    by a copy-engine copy; ``cascade``: shared-prefix groups in the plans).
+    The returned device replay's ``infos`` holds each launch's plan info and
+    ``outs`` its (out, lse) as float arrays."""
     cfg = wl.cfg
     atol, rtol = TOL[cfg.dtype]
     latol, lrtol = LSE_TOL[cfg.dtype]
     say(f"[parity] {label or cfg.name}: setup")
     orc = OracleReplay(wl).setup()
-    dev = DeviceReplay(wl, stage_kernel=stage_kernel).setup()
+    dev = DeviceReplay(wl, stage_kernel=stage_kernel, cascade=cascade).setup()
+    dev.infos, dev.outs = [], []
     launches = list(wl.launches[:n_launches] if n_launches else wl.launches)
     if steps:
         launches += [wl.step(s) for s in steps]
@@ -108,6 +112,10 @@ def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, lab
             compare_cache(dev, p, launch.k_new.get(), launch.v_new.get())
         out = p.out.float().cpu().numpy()
         lse = p.lse.cpu().numpy()
+        info = B.PlanInfo()
+        C.memmove(C.byref(info), C.byref(p.info), C.sizeof(info))
+        dev.infos.append(info)
+        dev.outs.append((out, lse))
         errs.append(close(out, ro["out"], atol, rtol, f"out[{li}]"))
         close(lse, ro["lse"], latol, lrtol, f"lse[{li}]")
         orc.finish(launch)

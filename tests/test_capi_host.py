@@ -31,7 +31,7 @@ def test_exports_every_declared_symbol():
     assert set(declared) == set(B.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.pa_abi_version() == 1
+    assert lib.pa_abi_version() == 2
 
 
 def _lib_apply(pool, st, toks):
@@ -263,6 +263,13 @@ def check_plan(plan, info, L, cu, G, hkv, D=128):
             assert all(ranges[i][1] == ranges[i + 1][0] for i in range(len(ranges) - 1))
     assert set(writes) == set(range(h[H_PARTIAL_ROWS])) and set(writes.values()) <= {1}
     assert int(info.workspace_bytes) == int(h[H_PARTIAL_ROWS]) * (D + 1) * 4
+    assert int(info.partial_rows) == int(h[H_PARTIAL_ROWS])
+    # the launch shape the attention calls check against
+    assert (info.n_seqs, info.total_q, info.num_kv_heads, info.head_dim) == (n, int(cu[-1]), hkv, D)
+    assert info.num_q_heads == hkv * G
+    # the plan-free workspace bound covers this plan
+    bound = B.workspace_size(int(cu[-1]), hkv * G, D, int(max(L)) if n else 0)
+    assert bound >= int(info.workspace_bytes)
 
 
 def test_plan_covers_every_row_once():
@@ -333,6 +340,9 @@ def test_device_calls_reject_bad_arguments_without_launching():
     lib = B.lib()
     info = B.PlanInfo()
     info.kind = B.KIND_DECODE
+    # the launch shape of the call below
+    info.n_seqs, info.total_q, info.num_q_heads, info.num_kv_heads = 1, 1, 8, 2
+    info.head_dim, info.dtype = 128, B.PA_BF16
     args = [None, None, None, 16, None, 4, None, None, 1, 1, 8, 2, 128, 16, 0.1, B.PA_BF16, None,
             ctypes.byref(info), None, 0, None, None, None]
     # plan kind mismatch
@@ -347,6 +357,17 @@ def test_device_calls_reject_bad_arguments_without_launching():
         assert lib.pa_attn_decode(*a) == code, idx
     # NULL device pointers with work to do
     assert lib.pa_attn_decode(*args) == B.PA_ERR_ARG
+    assert b"NULL" in lib.pa_last_error()
+    # a plan built for another launch shape is refused before anything else
+    for field, val in (("n_seqs", 2), ("total_q", 3), ("num_q_heads", 16), ("num_kv_heads", 1),
+                       ("head_dim", 64), ("dtype", B.PA_F32)):
+        bad = B.PlanInfo()
+        ctypes.memmove(ctypes.byref(bad), ctypes.byref(info), ctypes.sizeof(info))
+        setattr(bad, field, val)
+        a = list(args)
+        a[17] = ctypes.byref(bad)
+        assert lib.pa_attn_decode(*a) == B.PA_ERR_ARG, field
+        assert b"plan was built for" in lib.pa_last_error(), field
     assert lib.pa_kv_append(None, None, None, 3, None, None, 16, 2, 128, 16, B.PA_BF16, None) == B.PA_ERR_ARG
     assert lib.pa_kv_append(None, None, None, 0, None, None, 16, 2, 100, 16, B.PA_BF16, None) == B.PA_ERR_UNSUPPORTED
     # staged upload: size and alignment are checked before any runtime call
@@ -575,3 +596,52 @@ def test_prepare_launch_matches_separate_calls(name):
     assert e.value.rc == B.PA_ERR_ARG and b"capacity" in B.lib().pa_last_error()
     added = sum(len(op.tokens) for op in launch.pre if op.tokens is not None)
     assert pools[0].stats()["live_tokens"] == before + added
+
+
+def test_workspace_size_bounds_every_plan():
+    """pa_attn_workspace_size / pa_attn_decode_workspace_size bound the
+    workspace of random decode, verification and mixed plans (with and
+    without shared-prefix groups), grow with every argument, and reject bad
+    arguments."""
+    r = np.random.default_rng(11)
+    for trial in range(60):
+        n = int(r.integers(1, 300))
+        hkv = int(r.choice([1, 2, 4, 8]))
+        G = int(r.choice([1, 2, 4, 8, 16]))
+        D = int(r.choice([64, 128]))
+        kind = [B.KIND_DECODE, B.KIND_VERIFY, B.KIND_PREFILL][trial % 3]
+        n_q = int(r.integers(1, 9)) if kind == B.KIND_VERIFY else 1
+        L = r.integers(n_q, 30000, size=n)
+        if kind == B.KIND_PREFILL:
+            q = np.where(r.random(n) < 0.5, 1, np.minimum(L, r.integers(1, 700, size=n)))
+        else:
+            q = np.full(n, n_q)
+        cu = np.concatenate([[0], np.cumsum(q)]).astype(np.int32)
+        mb = int((L.max() + 15) // 16)
+        # every sequence shares its first P blocks (cascade groups), or none
+        P = int(r.integers(0, int(L.min()) // 16 + 1)) if trial % 2 else 0
+        bt = np.full((n, mb), -1, np.int32)
+        nxt = 10 ** 6
+        for s_ in range(n):
+            nb = int((L[s_] + 15) // 16)
+            bt[s_, :min(P, nb)] = np.arange(min(P, nb))
+            bt[s_, min(P, nb):nb] = np.arange(nxt, nxt + nb - min(P, nb))
+            nxt += nb
+        _, info = B.plan(kind, n_q, L, cu, hkv * G, hkv, D, 16, B.PA_BF16, 256,
+                         block_table=bt if P else None)
+        bound = B.workspace_size(int(cu[-1]), hkv * G, D, int(L.max()))
+        assert bound >= int(info.workspace_bytes), (trial, bound, int(info.workspace_bytes))
+        if kind == B.KIND_DECODE:
+            assert B.workspace_size(n, hkv * G, D, int(L.max()), decode=True) == bound
+    # the decode workload's own plan fits the decode bound
+    wl = synth.workload("decode", scale=0.25)
+    assert B.workspace_size(256, 32, 128, 4000, decode=True) >= B.workspace_size(64, 32, 128, 4000)
+    assert B.workspace_size(10, 8, 128, 256) == 0   # one part per sequence: nothing split
+    assert B.workspace_size(10, 8, 128, 257) > 0
+    lib = B.lib()
+    n_out = ctypes.c_size_t(0)
+    assert lib.pa_attn_workspace_size(-1, 8, 128, 10, ctypes.byref(n_out)) == B.PA_ERR_ARG
+    assert lib.pa_attn_decode_workspace_size(1, 8, 96, 10, ctypes.byref(n_out)) == B.PA_ERR_UNSUPPORTED
+    assert b"pa_attn_decode_workspace_size" in lib.pa_last_error()
+    assert lib.pa_attn_workspace_size(1, 8, 128, 10, None) == B.PA_ERR_ARG
+

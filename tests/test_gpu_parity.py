@@ -28,6 +28,53 @@ def test_tiny_f32_prefill_and_decode_steps():
     assert len(errs) == 9
 
 
+def test_tiny_f32_head_dim_128():
+    """The float32 kernel at head_dim 128 (the tiny recipe with D = 128):
+    prefill then eight decode steps, within 1e-5."""
+    _gpu()
+    errs, dev, _ = run_parity(synth.workload("tiny", head_dim=128), label="tiny-f32-d128")
+    say("tiny d128 normalized errors", errs)
+    assert len(errs) == 9 and all(i.head_dim == 128 for i in dev.infos)
+
+
+def test_verify_multi_chunk_shared_prefix_every_row():
+    """Verification at the full 16384-token shared prefix and 4096-token
+    private suffix, 4 requests, n_q 5, G 8: the shared prefix runs as three
+    key chunks of cascade tiles (a full and a partial 128-row tile each), the
+    40-row private parts (4101 keys) as three split tile items; every row
+    compared."""
+    _gpu()
+    wl = synth.workload("verify", requests=4, steps=2)
+    errs, dev, _ = run_parity(wl, steps=[1], label="verify-4req-full-length")
+    say("verify multi-chunk normalized errors", errs)
+    info = dev.infos[0]
+    # 3 chunks x 2 tiles of gathered rows (160 rows) x 8 kv-heads
+    assert info.n_shared_items == 3 * 2 * 8, info.n_shared_items
+    assert info.n_tile_items == 4 * 3 * 8, info.n_tile_items
+
+
+def test_prefill_long_sequences_every_row():
+    """Suffix prefill of 2 requests at full length (2048 cached prefix +
+    U[256,1024] suffix: more than 1024 keys, so the tile loop's window of
+    block ids advances past 64 blocks), every row compared."""
+    _gpu()
+    wl = synth.workload("prefill", requests=2, steps=2)
+    errs, dev, _ = run_parity(wl, steps=[1], label="prefill-2req-full-length")
+    say("prefill long normalized errors", errs)
+    assert min(wl.notes["suffix"]) + wl.notes["prefix"] > 64 * 16
+
+
+def test_mixed_full_length_every_row():
+    """The mixed launch at full lengths with 40 requests (5 prefill chunks of
+    512 tokens over 1k-8k prefixes, 35 decode tokens, cascade groups on
+    shared prefixes, the 8k prefix in two key chunks), every row compared."""
+    _gpu()
+    wl = synth.workload("mixed", requests=40, steps=2)
+    errs, dev, _ = run_parity(wl, steps=[1], label="mixed-40req-full-length")
+    say("mixed full-length normalized errors", errs)
+    assert dev.infos[0].n_shared_items > 0
+
+
 def test_tiny_in_bf16():
     _gpu()
     run_parity(synth.workload("tiny", dtype="bf16"), label="tiny-bf16")
@@ -344,22 +391,20 @@ def test_edge_cases():
 @pytest.mark.parametrize("name,scale", [("decode", 0.125), ("verify", 0.25), ("mixed", 0.125)])
 def test_shared_prefix_cascade_matches_per_sequence(name, scale):
     """With shared-prefix groups (prefix attention once for all sequences,
-    merged by log-sum-exp) and without them, outputs agree within the bf16
-    tolerance and both match the oracle."""
+    merged by log-sum-exp) and without them: both match the oracle on every
+    row, and agree with each other within the bf16 tolerance."""
     _gpu()
-    from paper_2605_11232_amd.runtime import DeviceReplay
     from tests.parity import TOL, close
     outs = []
     for cascade in (True, False):
         wl = synth.workload(name, scale=scale, steps=2)
-        d = DeviceReplay(wl, cascade=cascade).setup()
-        p = d.run(wl.launches[0])
-        torch.cuda.synchronize()
+        _, dev, _ = run_parity(wl, n_launches=1, cascade=cascade,
+                               label=f"{name}@{scale} cascade={cascade}")
         if cascade:
-            assert p.info.n_shared_items > 0
+            assert dev.infos[0].n_shared_items > 0
         else:
-            assert p.info.n_shared_items == 0
-        outs.append((p.out.float().cpu().numpy(), p.lse.cpu().numpy()))
+            assert dev.infos[0].n_shared_items == 0
+        outs.append(dev.outs[0])
     close(outs[0][0], outs[1][0], *TOL["bf16"], f"{name} cascade vs per-sequence")
     close(outs[0][1], outs[1][1], 2e-3, 1e-4, f"{name} lse cascade vs per-sequence")
 
