@@ -431,6 +431,30 @@ int pa_attn_verify(const void* q, const void* k_cache, const void* v_cache, int3
                    const pa_plan_info* info, void* workspace, size_t workspace_bytes,
                    void* out, float* lse, void* stream);
 
+/* Decode for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops that must not call hipMalloc, harnesses that
+ * forbid it): exactly pa_attn_decode with the same arguments minus the
+ * workspace.  The split-K partial results go to a device array the library
+ * owns, PA_NOALLOC_WORKSPACE_BYTES bytes on each GPU it runs on, set up on
+ * the first call on that GPU (the calling thread's current device, which must
+ * be the stream's) and held until the process ends; the call allocates
+ * nothing.  Every call on one GPU shares that array and it keeps the last
+ * call's contents (nothing in it needs to start at zero): calls ordered on
+ * one stream are safe, calls that overlap in time on one GPU (other streams,
+ * other threads) race.
+ * Errors: those of pa_attn_decode, plus PA_ERR_ARG when the plan's
+ * info->workspace_bytes exceeds PA_NOALLOC_WORKSPACE_BYTES (use
+ * pa_attn_decode with a workspace of that size instead), PA_ERR_LAUNCH when
+ * the array's device address cannot be obtained. */
+#define PA_NOALLOC_WORKSPACE_BYTES ((size_t)32 << 20)
+int pa_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                           int32_t num_blocks, const int32_t* block_table,
+                           int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                           const int32_t* cu_seqlens_q, int32_t n_seqs, int32_t total_q,
+                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                           int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                           const pa_plan_info* info, void* out, float* lse, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

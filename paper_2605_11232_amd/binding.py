@@ -29,7 +29,8 @@ EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy
            "pa_pool_free_list", "pa_build_metadata", "pa_attn_plan", "pa_kv_append",
            "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify", "pa_pool_set_eviction",
            "pa_pool_get_stats", "pa_pool_kv_waste", "pa_form_batches", "pa_prepare_launch",
-           "pa_stage_upload", "pa_attn_workspace_size", "pa_attn_decode_workspace_size"]
+           "pa_stage_upload", "pa_attn_workspace_size", "pa_attn_decode_workspace_size",
+           "pa_attn_decode_noalloc"]
 
 
 class PaError(RuntimeError):
@@ -114,6 +115,8 @@ def lib():
                       C.POINTER(PlanInfo), _P, C.c_size_t, _P, _P, _P])
     for name in ("pa_attn_prefill", "pa_attn_decode", "pa_attn_verify"):
         sig[name] = attn
+    # decode without the workspace pair
+    sig["pa_attn_decode_noalloc"] = (C.c_int, attn[1][:18] + attn[1][20:])
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
         fn.restype = res
@@ -497,6 +500,10 @@ class StreamEvent:
             self._ev = None
 
 
+# Per-device workspace held by pa_attn_decode_noalloc (PA_NOALLOC_WORKSPACE_BYTES).
+NOALLOC_WORKSPACE_BYTES = 32 << 20
+
+
 def _dtype_code(t) -> int:
     import torch
     if t.dtype == torch.bfloat16:
@@ -536,3 +543,18 @@ def attention(kind: int, q, k_cache, v_cache, block_table, seq_lens, cu_seqlens_
               hq, hkv, d, bs, float(scale), _dtype_code(q), _dptr(plan_dev), C.byref(info),
               _dptr(workspace), ws_bytes, _dptr(out), _dptr(lse), _stream(stream)))
 
+
+def attention_decode_noalloc(q, k_cache, v_cache, block_table, seq_lens, cu_seqlens_q, plan_dev,
+                             info: PlanInfo, out, lse=None, scale=None, stream=None):
+    """Decode through pa_attn_decode_noalloc (split-K partials in the
+    library's per-device array; no workspace argument)."""
+    nb, hkv, bs, d = k_cache.shape
+    total_q, hq, _ = q.shape
+    n_seqs = int(seq_lens.numel())
+    if scale is None:
+        scale = d ** -0.5
+    _check(lib().pa_attn_decode_noalloc(
+        _dptr(q), _dptr(k_cache), _dptr(v_cache), nb, _dptr(block_table),
+        int(block_table.shape[1]), _dptr(seq_lens), _dptr(cu_seqlens_q), n_seqs, total_q, hq, hkv,
+        d, bs, float(scale), _dtype_code(q), _dptr(plan_dev), C.byref(info), _dptr(out),
+        _dptr(lse), _stream(stream)))

@@ -2,6 +2,8 @@
 // on the caller's stream.  See include/pa.h for the contract of each call.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "internal.h"
 #include "plan_format.h"
 
@@ -41,13 +43,44 @@ int check_shape(const char* fn, int32_t num_blocks, int32_t num_kv_heads, int32_
   return PA_OK;
 }
 
+// Split-K workspace of pa_attn_decode_noalloc: one array per GPU, in the
+// code object's device memory.  Its name is a host-side stand-in; kernels
+// get the device address each GPU reports for it.
+static __device__ __align__(256) unsigned char scratch[PA_NOALLOC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of `scratch` on the calling thread's current device, looked
+// up once per device.
+int scratch_address(const char* fn, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess)
+    return fail(PA_ERR_LAUNCH, "%s: hipGetDevice: %s", fn, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(PA_ERR_UNSUPPORTED, "%s: device %d (at most %d devices)", fn, dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(PA_ERR_LAUNCH, "%s: hipGetSymbolAddress: %s", fn, hipGetErrorString(e));
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return PA_OK;
+}
+
 int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_cache,
                 const void* v_cache, int32_t num_blocks, const int32_t* block_table,
                 int32_t max_blocks_per_seq, const int32_t* seq_lens, const int32_t* cu_seqlens_q,
                 int32_t n_seqs, int32_t total_q, int32_t num_q_heads, int32_t num_kv_heads,
                 int32_t head_dim, int32_t block_size, float scale, int32_t dtype,
                 const int32_t* plan, const pa_plan_info* info, void* workspace,
-                size_t workspace_bytes, void* out, float* lse, void* stream) {
+                size_t workspace_bytes, void* out, float* lse, void* stream,
+                bool noalloc = false) {
   clear_error();
   int rc = check_shape(fn, num_blocks, num_kv_heads, head_dim, block_size, dtype);
   if (rc) return rc;
@@ -88,6 +121,21 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
         info->partial_rows < 0 ||
         info->workspace_bytes != info->partial_rows * int64_t(head_dim + 1) * 4)
       return fail(PA_ERR_ARG, "%s: corrupt plan info", fn);
+    if (noalloc) {
+      // the workspace is the library's per-device array
+      if (static_cast<uint64_t>(info->workspace_bytes) > PA_NOALLOC_WORKSPACE_BYTES)
+        return fail(PA_ERR_ARG, "%s: the plan needs %lld bytes of workspace, more than the "
+                    "%zu bytes this call holds per device; call pa_attn_decode with a "
+                    "workspace of that size", fn, (long long)info->workspace_bytes,
+                    (size_t)PA_NOALLOC_WORKSPACE_BYTES);
+      workspace = nullptr;
+      workspace_bytes = 0;
+      if (info->workspace_bytes > 0) {
+        rc = scratch_address(fn, &workspace);
+        if (rc) return rc;
+        workspace_bytes = PA_NOALLOC_WORKSPACE_BYTES;
+      }
+    }
     if (static_cast<int64_t>(workspace_bytes) < info->workspace_bytes ||
         (info->workspace_bytes > 0 && !workspace))
       return fail(PA_ERR_ARG, "%s: workspace of %zu bytes, plan needs %lld", fn, workspace_bytes,
@@ -189,6 +237,19 @@ int pa_attn_decode(PA_ATTN_ARGS) {
 }
 int pa_attn_verify(PA_ATTN_ARGS) {
   return pa::attn_common("pa_attn_verify", PA_KIND_VERIFY, PA_ATTN_PASS);
+}
+
+int pa_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                           int32_t num_blocks, const int32_t* block_table,
+                           int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                           const int32_t* cu_seqlens_q, int32_t n_seqs, int32_t total_q,
+                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                           int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                           const pa_plan_info* info, void* out, float* lse, void* stream) {
+  return pa::attn_common("pa_attn_decode_noalloc", PA_KIND_DECODE, q, k_cache, v_cache,
+                         num_blocks, block_table, max_blocks_per_seq, seq_lens, cu_seqlens_q,
+                         n_seqs, total_q, num_q_heads, num_kv_heads, head_dim, block_size, scale,
+                         dtype, plan, info, nullptr, 0, out, lse, stream, /*noalloc=*/true);
 }
 
 }  // extern "C"

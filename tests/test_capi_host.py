@@ -645,3 +645,33 @@ def test_workspace_size_bounds_every_plan():
     assert b"pa_attn_decode_workspace_size" in lib.pa_last_error()
     assert lib.pa_attn_workspace_size(1, 8, 128, 10, None) == B.PA_ERR_ARG
 
+
+def test_noalloc_decode_rejects_before_launching():
+    """pa_attn_decode_noalloc checks its arguments like pa_attn_decode and
+    refuses a plan whose workspace exceeds its per-device array, all before
+    any runtime call."""
+    lib = B.lib()
+    h = open(os.path.join(ROOT, "include", "pa.h")).read()
+    assert re.search(r"#define PA_NOALLOC_WORKSPACE_BYTES \(\(size_t\)32 << 20\)", h)
+    assert B.NOALLOC_WORKSPACE_BYTES == 32 << 20
+    info = B.PlanInfo()
+    info.kind = B.KIND_DECODE
+    info.n_seqs, info.total_q, info.num_q_heads, info.num_kv_heads = 1, 1, 8, 2
+    info.head_dim, info.dtype, info.variant, info.grid = 128, B.PA_BF16, 1, 1
+    args = [1, 2, 3, 16, 4, 4, 5, 6, 1, 1, 8, 2, 128, 16, 0.1, B.PA_BF16, 7,
+            ctypes.byref(info), 8, None, None]
+    # one byte too many for the per-device array
+    info.partial_rows = (B.NOALLOC_WORKSPACE_BYTES // (129 * 4)) + 1
+    info.workspace_bytes = info.partial_rows * 129 * 4
+    assert lib.pa_attn_decode_noalloc(*args) == B.PA_ERR_ARG
+    assert b"pa_attn_decode_noalloc" in lib.pa_last_error()
+    assert b"workspace" in lib.pa_last_error()
+    # a plan of another kind, and a shape other than the plan's
+    info.partial_rows, info.workspace_bytes = 0, 0
+    info.kind = B.KIND_VERIFY
+    assert lib.pa_attn_decode_noalloc(*args) == B.PA_ERR_ARG
+    assert b"kind" in lib.pa_last_error()
+    info.kind = B.KIND_DECODE
+    info.total_q = 2
+    assert lib.pa_attn_decode_noalloc(*args) == B.PA_ERR_ARG
+    assert b"plan was built for" in lib.pa_last_error()
