@@ -27,10 +27,14 @@
  *    check launches nothing.  Pool operations that fail leave the pool
  *    unchanged.
  *  - Cache layout (both tensors contiguous, element type = dtype):
- *      k_cache[num_blocks][num_kv_heads][block_size][head_dim]
+ *      k_cache[num_blocks][num_kv_heads][head_dim/32][block_size][32]
  *      v_cache[num_blocks][num_kv_heads][head_dim][block_size]
- *    A token's slot is block * block_size + offset.  Values are transposed
- *    per block so that the PV product reads keys contiguously.
+ *    A token's slot is block * block_size + offset.  Key dim d of the token
+ *    at offset o is k_cache[block][h][d/32][pos(o)][d%32], where pos(o) is o
+ *    with bits 2 and 3 swapped: each 32-dim group of a block is 1 KB (bf16,
+ *    head_dim 128) that attention reads contiguously, eight keys of a decode
+ *    tile at a time.  Values are transposed per block so that the PV product
+ *    reads keys contiguously.
  *  - Query/output layout: q[total_q][num_q_heads][head_dim] packed by
  *    sequence (sequence r owns rows cu_seqlens_q[r] .. cu_seqlens_q[r+1]-1,
  *    which are its LAST q_len positions); out has q's layout and dtype;
@@ -342,8 +346,9 @@ int pa_prepare_launch(pa_pool* pool, int32_t n_ops, const int32_t* ops,
  * Section 2, PagedAttention keeps a request's KV in blocks addressed through
  * its block table; a token's KV is written once and then reused by every
  * later step and, for cached prefix blocks, by every request that hits them):
- * k_cache[s/bs][h][s%bs][:] = k_new[i][h][:] and
- * v_cache[s/bs][h][:][s%bs] = v_new[i][h][:] for s = slot_mapping[i].
+ * k_cache[s/bs][h][d/32][pos(s%bs)][d%32] = k_new[i][h][d] and
+ * v_cache[s/bs][h][d][s%bs] = v_new[i][h][d] for s = slot_mapping[i] (the
+ * cache layout above).
  * k_new, v_new: [n_tokens][num_kv_heads][head_dim] (dtype).  A slot outside
  * [0, num_blocks*block_size) skips its token (use -1 for padding).  All
  * pointers are caller-owned device memory; asynchronous on stream; allocates

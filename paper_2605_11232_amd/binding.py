@@ -519,9 +519,19 @@ def stage_upload(dst, src, nbytes: int, stream=None):
     _check(lib().pa_stage_upload(_dptr(dst), _dptr(src), int(nbytes), _stream(stream)))
 
 
+def cache_dims(k_cache, v_cache):
+    """(num_blocks, num_kv_heads, head_dim, block_size) of a paged cache: the
+    value cache is [NB, Hkv, D, bs]; the key cache holds as many elements in
+    the grouped layout [NB, Hkv, D / 32, bs, 32]."""
+    nb, hkv, d, bs = v_cache.shape
+    if k_cache.numel() != v_cache.numel() or k_cache.dtype != v_cache.dtype:
+        raise PaError(PA_ERR_ARG, "key and value caches differ in size or dtype")
+    return int(nb), int(hkv), int(d), int(bs)
+
+
 def kv_append(k_new, v_new, slot_mapping, k_cache, v_cache, stream=None):
     """Scatter new K/V ([T, Hkv, D] device tensors) into the paged cache."""
-    nb, hkv, bs, d = k_cache.shape
+    nb, hkv, d, bs = cache_dims(k_cache, v_cache)
     _check(lib().pa_kv_append(_dptr(k_new), _dptr(v_new), _dptr(slot_mapping),
                               int(slot_mapping.numel()), _dptr(k_cache), _dptr(v_cache), nb, hkv,
                               d, bs, _dtype_code(k_cache), _stream(stream)))
@@ -530,7 +540,7 @@ def kv_append(k_new, v_new, slot_mapping, k_cache, v_cache, stream=None):
 def attention(kind: int, q, k_cache, v_cache, block_table, seq_lens, cu_seqlens_q, plan_dev,
               info: PlanInfo, workspace, out, lse=None, scale=None, stream=None):
     """Paged attention (prefill / decode / verify by ``kind``) on device tensors."""
-    nb, hkv, bs, d = k_cache.shape
+    nb, hkv, d, bs = cache_dims(k_cache, v_cache)
     total_q, hq, _ = q.shape
     n_seqs = int(seq_lens.numel())
     if scale is None:
@@ -548,7 +558,7 @@ def attention_decode_noalloc(q, k_cache, v_cache, block_table, seq_lens, cu_seql
                              info: PlanInfo, out, lse=None, scale=None, stream=None):
     """Decode through pa_attn_decode_noalloc (split-K partials in the
     library's per-device array; no workspace argument)."""
-    nb, hkv, bs, d = k_cache.shape
+    nb, hkv, d, bs = cache_dims(k_cache, v_cache)
     total_q, hq, _ = q.shape
     n_seqs = int(seq_lens.numel())
     if scale is None:

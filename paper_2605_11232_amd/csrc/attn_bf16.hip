@@ -70,13 +70,18 @@ static_assert(kTileSub == 1 || kTileSub == 2, "32- or 64-key tile steps");
 constexpr int kTileWavesPerEu = kTileSub == 1 ? 3 : 2;
 
 // LDS of a tile item: K and V^T of two steps, each step held as the cache's
-// own 2 NSUB blocks ([16 keys][D] for K, [D][16 keys] for V^T).  Blocks are
-// copied straight from global memory into LDS (no register staging); the
-// 16-byte units are XOR-swizzled so that the MFMA operand reads of 16
-// consecutive lanes fall in distinct banks:
-//  K:   key row r, column unit c (8 dims)  -> unit r * D/8 + (c ^ (r % (D/8)))
+// own 2 NSUB blocks (the grouped key layout [D/32][16 slots][32] for K,
+// [D][16 keys] for V^T).  Blocks are copied straight from global memory into
+// LDS (no register staging), each 64-unit (1 KB) piece of LDS from one
+// contiguous 1 KB of the cache; the 16-byte units are XOR-swizzled within a
+// piece so that the MFMA operand reads of 16 consecutive lanes fall in
+// distinct banks:
+//  K:   block b, 32-dim group c, slot position s, 8-dim unit p
+//         -> unit (b D/32 + c) 64 + 4 s + (p ^ (s / 4 % 4))
 //  V^T: dim row d, half h (8 keys)         -> unit 2 d + (h ^ vswz(d))
-// Row r of a step's K holds key 32 * (r / 32) + perm32(r % 32).
+// Slot position s of a block holds offset s with bits 2 and 3 swapped, so
+// row r of a step's 32-key tile (position r % 16 of its block) holds key
+// 32 * (r / 32) + perm32(r % 32).
 template <int D, int NSUB>
 struct TileSmem {
   static constexpr int BLK = kBlock * D;  // bf16 per block of K or V^T
@@ -156,7 +161,6 @@ template <int D, int NSUB, bool SHARED, bool FULL>
 __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB>& sm) {
   constexpr int KT = 32 * NSUB;     // keys per step
   constexpr int NB = KT / kBlock;   // blocks per step
-  constexpr int CU = D / 8;         // 16-byte units per K row
   constexpr int NI = NSUB * D / 64; // LDS copies per wavefront per step, for each of K and V^T
   constexpr int BLK = TileSmem<D, NSUB>::BLK;
   const int tid = threadIdx.x, lane = tid & 63, j = lane & 31, hh = lane >> 5;
@@ -221,10 +225,10 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int U = 64 * (4 * i + w) + lane;
-    const int r = U / CU, cs = U % CU;
-    const int col = cs ^ (r % CU);
-    const int key = 32 * (r / 32) + perm32(r % 32);
-    koff[i] = (uint32_t)(((key % kBlock) * D + 8 * col) * 2);
+    // K: LDS piece 4 i + w is 32-dim group (4 i + w) % (D/32) of a block
+    const int grp = (4 * i + w) % (D / kKeyGroup), pos = lane >> 2;
+    const int unit = (lane & 3) ^ ((pos >> 2) & 3);
+    koff[i] = (uint32_t)((grp * kBlock * kKeyGroup + pos * kKeyGroup + 8 * unit) * 2);
     const int u = U % (2 * D), d = u >> 1, h = (u & 1) ^ vswz(d);
     voff[i] = (uint32_t)((d * kBlock + 8 * h) * 2);
   }
@@ -275,7 +279,11 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
   // register plus an immediate offset.
   uint32_t kofs[D / 16];
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) kofs[ks] = 16u * (j * CU + ((2 * ks + hh) ^ (j % CU)));
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const int pos = j % kBlock;
+    kofs[ks] = 16u * (((j / kBlock) * (D / kKeyGroup) + ks / 2) * 64 + 4 * pos +
+                      ((2 * (ks % 2) + hh) ^ ((pos >> 2) & 3)));
+  }
   const uint32_t vofs = 16u * (2 * j + (hh ^ vswz(j)));  // vswz(32 dt + j) == vswz(j)
   auto lds_at = [](const __bf16* base, uint32_t byte_off) {
     return reinterpret_cast<const __bf16*>(reinterpret_cast<const char*>(base) + byte_off);
@@ -556,8 +564,8 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
   const int32_t* bt = a.bt + (int64_t)r * a.max_blocks;
   const int64_t blk_k = (int64_t)a.hkv * kBlock * D, head_k = (int64_t)g * kBlock * D;
   const int64_t blk_v = (int64_t)a.hkv * D * kBlock, head_v = (int64_t)g * D * kBlock;
-  // K operand row j of score tile tt holds key 8 * (j / 4) + 4 * tt + j % 4.
-  const int kA0 = 8 * (j >> 2) + (j & 3);
+  // K operand row j of score tile tt holds key 8 * (j / 4) + 4 * tt + j % 4,
+  // so each lane's score elements are eight consecutive keys (8 g4 .. + 7).
 
   // One register set for K and one for V^T: the next step's K loads are
   // issued as soon as the score MFMAs have consumed K, and its V^T loads as
@@ -574,14 +582,17 @@ __device__ void row_item(const int32_t* it, const AttnArgs& a) {
     b0 = clamp_block(win.get(jb), a.num_blocks);
     b1 = t0 + 16 < kv1 ? clamp_block(win.get(jb + 1), a.num_blocks) : b0;
   };
+  // That key sits in block j / 8 at slot position 8 tt + j % 8 (the grouped
+  // key layout): each load reads, per block, eight
+  // consecutive 64-byte slot rows of one 32-dim group, 512 contiguous bytes.
   auto load_k = [&]() {
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
-      const int kk = kA0 + 4 * tt;
-      const int blk = kk < 16 ? b0 : b1;
-      const __bf16* p = a.kc + blk * blk_k + head_k + (kk & 15) * D + 8 * g4;
+      const int blk = j < 8 ? b0 : b1;
+      const __bf16* p = a.kc + blk * blk_k + head_k + (8 * tt + (j & 7)) * kKeyGroup + 8 * g4;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kreg[tt][ks] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p + 32 * ks));
+      for (int ks = 0; ks < KS; ++ks)
+        kreg[tt][ks] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p + kBlock * kKeyGroup * ks));
     }
   };
   auto load_v = [&]() {

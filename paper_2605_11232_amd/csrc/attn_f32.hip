@@ -48,10 +48,14 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
     int blk = 0;
     if (vis) {
       blk = clamp_block(row[min(key / kBlock, max_blocks - 1)], num_blocks);
-      const float* kp = kc + (((int64_t)blk * hkv + g) * kBlock + key % kBlock) * D;
+      // the key's 32-dim runs in the grouped key layout
+      const float* kp = kc + ((int64_t)blk * hkv + g) * kBlock * D + key_elem(key % kBlock, 0);
       float dot = 0.f;
+#pragma unroll
+      for (int gd = 0; gd < D; gd += kKeyGroup)
 #pragma unroll 8
-      for (int d = 0; d < D; ++d) dot = fmaf(qsh[d], kp[d], dot);
+        for (int d = 0; d < kKeyGroup; ++d)
+          dot = fmaf(qsh[gd + d], kp[gd * kBlock + d], dot);
       s = dot * scale;
     }
     float cm = s;

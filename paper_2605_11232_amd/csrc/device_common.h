@@ -103,6 +103,20 @@ struct BlockSpan {
   }
 };
 
+// Key cache layout.  One (block, kv-head) of keys is [D/32][16][32]: for each
+// group of 32 head dimensions, the block's 16 token slots of 32 dims each.
+// A slot's position inside a group is its offset with bits 2 and 3 swapped,
+// so the eight keys a decode MFMA tile needs from one block (offsets
+// 0-3 and 8-11, or 4-7 and 12-15) are 256 contiguous bytes of each group.
+constexpr int kKeyGroup = 32;
+__host__ __device__ constexpr int key_slot_pos(int off) {
+  return (off & ~12) | ((off & 4) << 1) | ((off & 8) >> 1);
+}
+// Element offset of (token offset off, dim d) inside one (block, kv-head).
+__host__ __device__ constexpr int key_elem(int off, int d) {
+  return (d / kKeyGroup) * (kBlock * kKeyGroup) + key_slot_pos(off) * kKeyGroup + d % kKeyGroup;
+}
+
 __device__ __forceinline__ int clamp_block(int b, int num_blocks) {
   return b < 0 ? 0 : (b >= num_blocks ? num_blocks - 1 : b);
 }

@@ -1,9 +1,10 @@
 // KV append: scatter the keys/values of new tokens into their cache slots.
 //
 // Paper: Section 2 (PagedAttention keeps each token's keys and values in the
-// block and offset its block table maps it to).  Keys keep their row layout
-// ([block][head][offset][dim]): each token-head row is copied with 16-byte
-// loads and stores.  Values are stored transposed per block
+// block and offset its block table maps it to).  Keys go to the grouped
+// layout of device_common.h ([block][head][dim / 32][slot position][32]):
+// each token-head row is copied with 16-byte loads and stores, as 64-byte
+// (bf16) or 128-byte (fp32) runs per 32-dim group.  Values are stored transposed per block
 // ([block][head][dim][offset]) so attention reads keys contiguously in the PV
 // product; a workgroup stages 16 consecutive tokens of one head in LDS and
 // writes each dimension's 16 offsets as neighbouring elements, so tokens that
@@ -43,7 +44,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const T* __restrict__ k_
       kx = ld16(k_new + src);
       vx = ld16(v_new + src);
       const int blk = s / kBlock, off = s % kBlock;
-      st16(kc + (((int64_t)blk * hkv + h) * kBlock + off) * D + part * E, kx);
+      st16(kc + ((int64_t)blk * hkv + h) * kBlock * D + key_elem(off, part * E), kx);
     }
     st16(&tile[tt][part * E], vx);
   }

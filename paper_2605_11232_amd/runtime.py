@@ -124,7 +124,8 @@ class DeviceReplay:
         self.tdtype = torch_dtype(cfg.dtype)
         self.dcode = B.PA_BF16 if cfg.dtype == "bf16" else B.PA_F32
         self.pool = B.Pool(wl.num_blocks, cfg.block_size, wl.free_order, evict=wl.evict)
-        shape_k = (wl.num_blocks, cfg.num_kv_heads, cfg.block_size, cfg.head_dim)
+        # keys in the grouped layout [block][head][dim / 32][slot position][32]
+        shape_k = (wl.num_blocks, cfg.num_kv_heads, cfg.head_dim // 32, cfg.block_size, 32)
         shape_v = (wl.num_blocks, cfg.num_kv_heads, cfg.head_dim, cfg.block_size)
         # Uninitialised on purpose: the kernels must never read unwritten slots.
         self.k_cache = torch.empty(shape_k, dtype=self.tdtype, device=self.device)

@@ -42,15 +42,25 @@ def close(out, ref, atol, rtol, what):
     return err.max() / rms
 
 
+def key_slot_pos(off):
+    """Position of token offset ``off`` inside a 32-dim group of the key
+    cache (include/pa.h: the offset with bits 2 and 3 swapped)."""
+    off = np.asarray(off)
+    return (off & ~12) | ((off & 4) << 1) | ((off & 8) >> 1)
+
+
 def compare_cache(dev: DeviceReplay, prep, k_new, v_new):
-    """The appended K/V sit at their slots bit for bit (layouts as documented)."""
+    """The appended K/V sit at their slots bit for bit (layouts as documented:
+    keys [block][head][dim / 32][slot position][32], values
+    [block][head][dim][offset])."""
     slots = prep.meta["slot_mapping"].astype(np.int64)
     if slots.size == 0:
         return
     bs = dev.cfg.block_size
     blk = torch.from_numpy(slots // bs).to(dev.device)
     off = torch.from_numpy(slots % bs).to(dev.device)
-    kd = dev.k_cache[blk, :, off, :].float().cpu().numpy()
+    pos = torch.from_numpy(key_slot_pos(slots % bs)).to(dev.device)
+    kd = dev.k_cache[blk, :, :, pos, :].float().cpu().numpy().reshape(k_new.shape)
     vd = dev.v_cache[blk, :, :, off].float().cpu().numpy()
     np.testing.assert_array_equal(kd, k_new)
     np.testing.assert_array_equal(vd, v_new)

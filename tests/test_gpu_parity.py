@@ -11,7 +11,7 @@ import pytest
 import torch
 
 from paper_2605_11232_amd import synth
-from tests.parity import run_parity, sample_rows, say
+from tests.parity import key_slot_pos, run_parity, sample_rows, say
 
 pytestmark = pytest.mark.gpu
 
@@ -298,7 +298,8 @@ def test_needle_through_block_table():
             # private positions only: prefix blocks are shared by every request
             t = int(r.integers(P, L[i] - 5))
             needles[(i, g)] = t
-            d.k_cache[int(bt[i][t // 16]), g, t % 16, 0] = beta
+            # dim 0 of key t: group 0, slot position of offset t % 16
+            d.k_cache[int(bt[i][t // 16]), g, 0, int(key_slot_pos(t % 16)), 0] = beta
     p.k_new.zero_()
     q = torch.zeros_like(p.q)
     q[:, :, 0] = alpha
