@@ -158,7 +158,7 @@ __device__ __forceinline__ float max_halves(float x) {
 // t + 1.  K of step t + 2 and V^T of step t + 1 are copied into the LDS
 // buffers freed by steps t and t - 1 during step t.
 template <int D, int NSUB, bool SHARED, bool FULL>
-__device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB>& sm) {
+__device__ __forceinline__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB>& sm) {
   constexpr int KT = 32 * NSUB;     // keys per step
   constexpr int NB = KT / kBlock;   // blocks per step
   constexpr int NI = NSUB * D / 64; // LDS copies per wavefront per step, for each of K and V^T
@@ -516,7 +516,7 @@ __device__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB
 // n_q * G rows (NC = 2), so the keys are streamed from memory once per 32
 // rows.  Sequences with more rows use tile items.
 template <int D, int NC>
-__device__ void row_item(const int32_t* it, const AttnArgs& a) {
+__device__ __forceinline__ void row_item(const int32_t* it, const AttnArgs& a) {
   constexpr int KS = D / 32;  // k-steps of the QK product (32 dims each)
   constexpr int DT = D / 16;  // 16-row tiles of O^T
   const int r = it[I_SEQ];
