@@ -41,7 +41,7 @@ namespace {
 
 constexpr int kXcds = 8;
 constexpr int64_t kRowWavesPerCu = 16;      // row-item split target
-constexpr int64_t kPrivateTileKeys = 2048;  // most private keys a few-row tile item covers
+constexpr int64_t kPrivateTileKeys = 4160;  // most private keys a few-row tile item covers
 constexpr int64_t kMinRowKeys = 256;        // fewest keys of a split row item
 
 using Rec = std::array<int32_t, pa::kItemWords>;

@@ -41,7 +41,7 @@ def test_verify_multi_chunk_shared_prefix_every_row():
     """Verification at the full 16384-token shared prefix and 4096-token
     private suffix, 4 requests, n_q 5, G 8: the shared prefix runs as three
     key chunks of cascade tiles (a full and a partial 128-row tile each), the
-    40-row private parts (4101 keys) as three split tile items; every row
+    40-row private parts (4101 keys) as one tile item each; every row
     compared."""
     _gpu()
     wl = synth.workload("verify", requests=4, steps=2)
@@ -50,7 +50,7 @@ def test_verify_multi_chunk_shared_prefix_every_row():
     info = dev.infos[0]
     # 3 chunks x 2 tiles of gathered rows (160 rows) x 8 kv-heads
     assert info.n_shared_items == 3 * 2 * 8, info.n_shared_items
-    assert info.n_tile_items == 4 * 3 * 8, info.n_tile_items
+    assert info.n_tile_items == 4 * 1 * 8, info.n_tile_items
 
 
 def test_prefill_long_sequences_every_row():
@@ -371,13 +371,17 @@ def test_edge_cases():
             close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"edge{ci}")
     # verify with n_q = 8: G = 2 gives 16 rows per sequence (one 16-row row
     # item per key range); G = 3 gives 24 rows (a row item of two 16-column
-    # tiles); G = 8 gives 64 rows (tile items over split private key ranges,
-    # two of the four wavefronts idle); G = 16 gives 128 rows (one tile item)
-    for G, want_tiles, want_wide in ((2, False, False), (3, False, True), (8, True, False),
-                                     (16, True, False)):
+    # tiles); G = 8 gives 64 rows (tile items, two of the four wavefronts
+    # idle; 4400 keys are two split ranges merged by log-sum-exp); G = 16
+    # gives 128 rows (one tile item)
+    for G, want_tiles, want_wide, lens in ((2, False, False, [40, 517]), (3, False, True, [40, 517]),
+                                           (8, True, False, [40, 517]), (8, True, False, [40, 4400]),
+                                           (16, True, False, [40, 517])):
         cfg8 = synth.AttnConfig(f"edge-g{G}", "bf16", 2 * G, 2, 128, 16, 78)
-        setup, launch = mk([8, 8], [40, 517], 9, cfg=cfg8)
-        wl = synth.Workload(cfg8, 128, np.arange(128, dtype=np.int32), setup, [launch], None, 40)
+        setup, launch = mk([8, 8], lens, 9, cfg=cfg8)
+        nb = sum(-(-L // 16) for L in lens) + 8
+        wl = synth.Workload(cfg8, nb, np.arange(nb, dtype=np.int32), setup, [launch], None,
+                            -(-max(lens) // 16))
         o = OracleReplay(wl).setup()
         dv = DeviceReplay(wl, kind="verify").setup()
         ro = o.launch(wl.launches[0])
@@ -386,7 +390,9 @@ def test_edge_cases():
         assert (p.info.n_tile_items > 0) == want_tiles
         assert (p.info.n_row_items > 0) == (not want_tiles)
         assert bool(p.info.variant & 2) == want_wide
-        close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"verify-G{G}")
+        if max(lens) > 4160:   # the private keys run as split tile items
+            assert p.info.n_tile_items > 2 * cfg8.num_kv_heads and p.info.n_groups > 0
+        close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"verify-G{G}-{max(lens)}")
 
 
 @pytest.mark.parametrize("name,scale", [("decode", 0.125), ("verify", 0.25), ("mixed", 0.125)])
