@@ -279,6 +279,56 @@ def run_workload(name, W, K, C, cpu_budget, profile=False):
     return res
 
 
+def measured_ceilings():
+    """What the device's own libraries reach in this process, as context for
+    the roofline fractions: a bf16 GEMM (torch.matmul, 8192^3), a read of 1 GiB
+    (torch sum) and a 1 GiB device-to-device copy (bytes read + written), each
+    timed with HIP events after a warm-up."""
+    import torch
+    from paper_2605_11232_amd import binding as B
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        a, b = B.StreamEvent(timing=True), B.StreamEvent(timing=True)
+        stream = torch.cuda.current_stream()
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e-3 / reps
+
+    n = 8192
+    g = torch.Generator(device="cuda").manual_seed(0)
+    x = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16)
+    y = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16)
+    gemm_s = timed(lambda: torch.matmul(x, y), 10)
+    del x, y
+    src = torch.ones(1 << 29, dtype=torch.bfloat16, device="cuda")  # 1 GiB
+    dst = torch.empty_like(src)
+    read_s = timed(lambda: src.sum(), 5)
+    copy_s = timed(lambda: dst.copy_(src), 5)
+    nbytes = src.numel() * 2
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bf16_gemm_tflops": round(2 * n ** 3 / gemm_s / 1e12, 1),
+            "hbm_read_gbs": round(nbytes / read_s / 1e9, 1),
+            "hbm_copy_gbs": round(2 * nbytes / copy_s / 1e9, 1),
+            "note": "torch.matmul bf16 8192^3, torch sum over 1 GiB, 1 GiB device copy "
+                    "(read + write bytes), timed in this run; context for the roofline "
+                    "fractions, which use the published peaks"}
+
+
+def add_measured_fraction(summary, ceilings):
+    """The roofline object's achieved figure against the measured ceiling of
+    its bound (bf16 GEMM for MFMA-bound calls, the 1 GiB read for HBM-bound)."""
+    key = {"mfma": "bf16_gemm_tflops", "hbm": "hbm_read_gbs"}.get(summary["bound"])
+    if key:
+        summary["frac_of_measured_ceiling"] = round(summary["achieved"] / ceilings[key], 4)
+        summary["measured_ceiling"] = key
+
+
 def call_summary(res):
     """Attention-call figures of one workload (the roofline object's body)."""
     per = np.asarray(res["per_ms"])
@@ -414,6 +464,13 @@ def main():
                 w["cpu_baseline"] = r2["cpu_baseline"]
             wls[other] = w
         rec["workloads"] = wls
+    if not profile:
+        # after every timed step, so the extra work cannot disturb them
+        ceil = measured_ceilings()
+        rec["measured_ceilings"] = ceil
+        add_measured_fraction(rec["roofline"], ceil)
+        for w in rec.get("workloads", {}).values():
+            add_measured_fraction(w["roofline"], ceil)
     print(json.dumps(rec), flush=True)
 
 
