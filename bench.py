@@ -281,9 +281,10 @@ def run_workload(name, W, K, C, cpu_budget, profile=False):
 
 def measured_ceilings():
     """What the device's own libraries reach in this process, as context for
-    the roofline fractions: a bf16 GEMM (torch.matmul, 8192^3), a read of 1 GiB
-    (torch sum) and a 1 GiB device-to-device copy (bytes read + written), each
-    timed with HIP events after a warm-up."""
+    the roofline fractions: a bf16 GEMM (torch.matmul, 16384^3), a read of 1 GiB
+    (float32 row sums of a [65536, 4096] array, the fastest of torch's
+    reductions on this device) and a 1 GiB device-to-device copy (bytes read +
+    written), each timed with HIP events after a warm-up."""
     import torch
     from paper_2605_11232_amd import binding as B
 
@@ -299,24 +300,25 @@ def measured_ceilings():
         torch.cuda.synchronize()
         return a.elapsed_time(b) * 1e-3 / reps
 
-    n = 8192
+    n = 16384
     g = torch.Generator(device="cuda").manual_seed(0)
     x = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16)
     y = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16)
-    gemm_s = timed(lambda: torch.matmul(x, y), 10)
+    gemm_s = timed(lambda: torch.matmul(x, y), 5)
     del x, y
-    src = torch.ones(1 << 29, dtype=torch.bfloat16, device="cuda")  # 1 GiB
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
     dst = torch.empty_like(src)
-    read_s = timed(lambda: src.sum(), 5)
+    rows = src.view(1 << 16, -1)
+    read_s = timed(lambda: rows.sum(dim=1), 5)
     copy_s = timed(lambda: dst.copy_(src), 5)
-    nbytes = src.numel() * 2
-    del src, dst
+    nbytes = src.numel() * 4
+    del src, dst, rows
     torch.cuda.empty_cache()
     return {"bf16_gemm_tflops": round(2 * n ** 3 / gemm_s / 1e12, 1),
             "hbm_read_gbs": round(nbytes / read_s / 1e9, 1),
             "hbm_copy_gbs": round(2 * nbytes / copy_s / 1e9, 1),
-            "note": "torch.matmul bf16 8192^3, torch sum over 1 GiB, 1 GiB device copy "
-                    "(read + write bytes), timed in this run; context for the roofline "
+            "note": "torch.matmul bf16 16384^3, float32 row sums over 1 GiB, 1 GiB device "
+                    "copy (read + write bytes), timed in this run; context for the roofline "
                     "fractions, which use the published peaks"}
 
 
