@@ -324,6 +324,34 @@ def test_needle_through_block_table():
                 assert np.all(np.abs(got - want) <= 1e-2 + 2e-2 * np.abs(want)), (i, j, h)
 
 
+class _Scaled:
+    """A launch's queries multiplied by a factor, rounded back to bf16 (both
+    the oracle and the library read these exact values)."""
+
+    def __init__(self, values, factor):
+        self.values, self.factor = values, factor
+
+    def get(self):
+        return synth.round_to_dtype(self.values.get() * np.float32(self.factor), "bf16")
+
+
+@pytest.mark.parametrize("factor", [24.0, 1e-3])
+@pytest.mark.parametrize("name,scale", [("prefill", 0.0625), ("decode", 0.0625),
+                                        ("verify", 0.125), ("mixed", 0.0625)])
+def test_extreme_score_scales(name, scale, factor):
+    """Queries scaled by 24 (scores of standard deviation ~24 nats: nearly
+    one-hot rows, the running maximum moves many times, most probabilities
+    underflow) or by 1e-3 (nearly uniform rows) on every path: tile items,
+    row items, shared-prefix items and their merge, against the oracle."""
+    _gpu()
+    wl = synth.workload(name, scale=scale, steps=2)
+    launch = wl.launches[0]
+    wl.launches = [synth.Launch(launch.pre, launch.seq_ids, launch.q_lens,
+                                _Scaled(launch.q, factor), launch.k_new, launch.v_new, launch.post)]
+    errs, dev, _ = run_parity(wl, n_launches=1, label=f"{name}@{scale} q x {factor}")
+    say(f"{name} q x {factor} normalized errors", errs)
+
+
 def test_edge_cases():
     """Empty launch, zero-query sequences mixed in, a one-token sequence,
     head_dim 64 in bf16, G = 1, verify with 16 to 128 rows per sequence (narrow
