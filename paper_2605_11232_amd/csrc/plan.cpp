@@ -32,6 +32,7 @@
 #include <array>
 #include <climits>
 #include <cstdint>
+#include <unordered_map>
 #include <vector>
 
 #include "internal.h"
@@ -79,6 +80,27 @@ std::vector<int32_t> order_longest_first(const std::vector<int64_t>& cost) {
   }
   for (int b = 0; b < 256; ++b) cnt[b + 1] += cnt[b];
   for (size_t i = 0; i < n; ++i) out[cnt[key[i]]++] = static_cast<int32_t>(i);
+  return out;
+}
+
+// Tile items grouped by sequence: sequences by their total cost, longest
+// first, and each sequence's items longest first.  The items of one sequence
+// then run at about the same time on its kv-head's XCDs and share its keys
+// in L2.
+std::vector<int32_t> order_by_sequence(const std::vector<int64_t>& cost,
+                                       const std::vector<std::array<int32_t, 8>>& items) {
+  const size_t n = cost.size();
+  std::unordered_map<int32_t, int64_t> total;
+  for (size_t i = 0; i < n; ++i) total[items[i][0]] += cost[i];
+  std::vector<int32_t> out(n);
+  for (size_t i = 0; i < n; ++i) out[i] = static_cast<int32_t>(i);
+  std::stable_sort(out.begin(), out.end(), [&](int32_t a, int32_t b) {
+    const int32_t ra = items[a][0], rb = items[b][0];
+    const int64_t ta = total[ra], tb = total[rb];
+    if (ta != tb) return ta > tb;
+    if (ra != rb) return ra < rb;
+    return cost[a] > cost[b];
+  });
   return out;
 }
 
@@ -350,8 +372,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     // head's XCD queues (which stay longest first).
     std::vector<std::vector<int>> xs_of(num_kv_heads);
     for (int32_t g = 0; g < num_kv_heads; ++g) xs_of[g] = xcds_of_head(g, num_kv_heads);
-    auto deal = [&](const std::vector<int64_t>& costs) {
-      const auto ord = order_longest_first(costs);
+    auto deal = [&](const std::vector<int64_t>& costs, const std::vector<Rec>* by_seq) {
+      const auto ord = by_seq ? order_by_sequence(costs, *by_seq) : order_longest_first(costs);
       std::vector<std::vector<Ref>> q(kXcds);
       for (auto& x : q) x.reserve(ord.size() * num_kv_heads / kXcds + ord.size());
       for (int32_t g = 0; g < num_kv_heads; ++g) {
@@ -361,8 +383,11 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       }
       return interleave(q);
     };
-    shared = deal(shared_cost);
-    tiles = deal(tile_cost);
+    shared = deal(shared_cost, nullptr);
+#ifndef PA_TILE_ORDER
+#define PA_TILE_ORDER 1
+#endif
+    tiles = deal(tile_cost, PA_TILE_ORDER ? &t_tiles : nullptr);
     // Row items: per head, longest first, four to a workgroup (padded with
     // empty items) so a workgroup's waves share one kv-head.
     {
