@@ -466,7 +466,8 @@ def main():
                 w["cpu_baseline"] = r2["cpu_baseline"]
             wls[other] = w
         rec["workloads"] = wls
-    if not profile:
+    if name == "prefill" and not args.no_secondary and not profile:
+        # the full run only (profiling runs keep their traces to the hot path),
         # after every timed step, so the extra work cannot disturb them
         ceil = measured_ceilings()
         rec["measured_ceilings"] = ceil
