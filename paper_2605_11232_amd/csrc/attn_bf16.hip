@@ -158,7 +158,8 @@ __device__ __forceinline__ float max_halves(float x) {
 // t + 1.  K of step t + 2 and V^T of step t + 1 are copied into the LDS
 // buffers freed by steps t and t - 1 during step t.
 template <int D, int NSUB, bool SHARED, bool FULL>
-__device__ __forceinline__ void tile_item(const int32_t* it, const AttnArgs& a, TileSmem<D, NSUB>& sm) {
+__device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, const AttnArgs& a,
+                                          TileSmem<D, NSUB>& sm) {
   constexpr int KT = 32 * NSUB;     // keys per step
   constexpr int NB = KT / kBlock;   // blocks per step
   constexpr int NI = NSUB * D / 64; // LDS copies per wavefront per step, for each of K and V^T
@@ -167,7 +168,7 @@ __device__ __forceinline__ void tile_item(const int32_t* it, const AttnArgs& a, 
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;
   const int G = a.group;
   const int lr = w * 32 + j;
-  const int g = it[I_KVH], row0 = it[I_ROW0], nrows = it[I_NROWS], kv0 = it[I_KV0];
+  const int row0 = it[I_ROW0], nrows = it[I_NROWS], kv0 = it[I_KV0];
   const bool valid = lr < nrows;
   int key_seq, kend, qs, qi, hq, apos, wg_amin, part;
   if constexpr (SHARED) {
@@ -180,7 +181,7 @@ __device__ __forceinline__ void tile_item(const int32_t* it, const AttnArgs& a, 
     qs = a.cu_q[seq];
     qi = rl / G;
     hq = g * G + (rl - qi * G);
-    part = mem[1] + rl;
+    part = mem[1] + poff + rl;
     key_seq = it[S_BLOCK_SEQ];
     kend = it[S_KV1];
     apos = valid ? kend - 1 : -1;  // every shared key is visible
@@ -193,7 +194,7 @@ __device__ __forceinline__ void tile_item(const int32_t* it, const AttnArgs& a, 
     const int rho = row0 + lr;
     qi = rho / G;
     hq = g * G + (rho - qi * G);
-    part = it[I_PART] < 0 ? -1 : it[I_PART] + lr;
+    part = it[I_PART] < 0 ? -1 : it[I_PART] + poff + lr;
     key_seq = r;
     kend = min(it[I_KV1], L);
     apos = valid ? L - n + qi : -1;
@@ -516,13 +517,13 @@ __device__ __forceinline__ void tile_item(const int32_t* it, const AttnArgs& a, 
 // n_q * G rows (NC = 2), so the keys are streamed from memory once per 32
 // rows.  Sequences with more rows use tile items.
 template <int D, int NC>
-__device__ __forceinline__ void row_item(const int32_t* it, const AttnArgs& a) {
+__device__ __forceinline__ void row_item(const int32_t* it, int g, int poff, const AttnArgs& a) {
   constexpr int KS = D / 32;  // k-steps of the QK product (32 dims each)
   constexpr int DT = D / 16;  // 16-row tiles of O^T
   const int r = it[I_SEQ];
   if (r < 0) return;
-  const int g = it[I_KVH], row0 = it[I_ROW0], nrows = it[I_NROWS];
-  const int kv0 = it[I_KV0], part = it[I_PART];
+  const int row0 = it[I_ROW0], nrows = it[I_NROWS];
+  const int kv0 = it[I_KV0], part = it[I_PART] < 0 ? -1 : it[I_PART] + poff;
   const int lane = threadIdx.x & 63, j = lane & 15, g4 = lane >> 4;
   const int L = a.seq_lens[r];
   const int qs = a.cu_q[r], n = a.cu_q[r + 1] - qs;
@@ -712,36 +713,41 @@ constexpr int waves_per_eu() { return MIX == 2 ? 3 : kTileWavesPerEu; }
 template <int D, int MIX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_eu<MIX>()))) void attn_bf16_kernel(AttnArgs a) {
   const int32_t* plan = a.plan;
-  const int n_tile = plan[H_N_SHARED] + plan[H_N_TILE];  // workgroups before the row quads
+  const int n_shared = plan[H_N_SHARED];
+  const int n_tile = n_shared + plan[H_N_TILE];  // workgroups before the row quads
   const int b = blockIdx.x;
+  // this workgroup's kv-head and template (the dispatch list follows the
+  // header, so its word loads together with the header words)
+  const int wd = plan[kHeaderWords + b];
+  const int g = wd >> kDispatchHeadShift, ti = wd & kDispatchIndexMask;
+  const int poff = g * plan[H_HEAD_PARTIAL];  // the kv-head's partial rows
   if constexpr (MIX & 1) {
     __shared__ TileSmem<D, kTileSub> sm;
-    const int n_shared = plan[H_N_SHARED];
     if (b < n_shared) {
-      const int32_t* it = plan + plan[H_SHARED_OFF] + b * kSharedWords;
-      if (it[S_NROWS] > kTileRows - 32) tile_item<D, kTileSub, true, true>(it, a, sm);
-      else tile_item<D, kTileSub, true, false>(it, a, sm);
+      const int32_t* it = plan + plan[H_SHARED_OFF] + ti * kSharedWords;
+      if (it[S_NROWS] > kTileRows - 32) tile_item<D, kTileSub, true, true>(it, g, poff, a, sm);
+      else tile_item<D, kTileSub, true, false>(it, g, poff, a, sm);
       return;
     }
     if (b < n_tile) {
-      const int32_t* it = plan + plan[H_TILE_OFF] + (b - n_shared) * kItemWords;
+      const int32_t* it = plan + plan[H_TILE_OFF] + ti * kItemWords;
       // every wavefront has rows: the plain path; otherwise idle ones skip compute
-      if (it[I_NROWS] > kTileRows - 32) tile_item<D, kTileSub, false, true>(it, a, sm);
-      else tile_item<D, kTileSub, false, false>(it, a, sm);
+      if (it[I_NROWS] > kTileRows - 32) tile_item<D, kTileSub, false, true>(it, g, poff, a, sm);
+      else tile_item<D, kTileSub, false, false>(it, g, poff, a, sm);
       return;
     }
   }
   if constexpr ((MIX & 6) != 0) {
-    const int idx = 4 * (b - n_tile) + (threadIdx.x >> 6);
-    if (b >= n_tile && idx < plan[H_N_ROW]) {
-      const int32_t* it = plan + plan[H_ROW_OFF] + idx * kItemWords;
+    if (b >= n_tile) {
+      // a quad of row templates, one per wavefront
+      const int32_t* it = plan + plan[H_ROW_OFF] + (ti + (threadIdx.x >> 6)) * kItemWords;
       if constexpr ((MIX & 4) != 0) {
         if (it[I_NROWS] > 16) {
-          row_item<D, 2>(it, a);
+          row_item<D, 2>(it, g, poff, a);
           return;
         }
       }
-      row_item<D, 1>(it, a);
+      row_item<D, 1>(it, g, poff, a);
     }
   }
 }
@@ -756,15 +762,20 @@ __global__ __launch_bounds__(kMergeRows * 32) void merge_kernel(AttnArgs a) {
   constexpr int VD = D / 32;  // output dims per lane
   constexpr int C = 16;       // parts whose loads are in flight together
   typedef float vecf __attribute__((ext_vector_type(VD)));
-  const int32_t* gr = a.plan + a.plan[H_GROUP_OFF] + blockIdx.x * kGroupWords;
+  // merge group blockIdx.x: template blockIdx.x % N_GROUP_TMPL of kv-head
+  // blockIdx.x / N_GROUP_TMPL
+  const int ntg = a.plan[H_N_GROUP_TMPL];
+  const int g = blockIdx.x / ntg;
+  const int32_t* gr = a.plan + a.plan[H_GROUP_OFF] + (blockIdx.x - g * ntg) * kGroupWords;
   const int lr = threadIdx.x >> 5, lane = threadIdx.x & 31;
   const int half = threadIdx.x & 32;  // first lane of this row's half wavefront
   const int nrows = gr[G_NROWS];
   const bool valid = lr < nrows;
-  const int r = gr[G_SEQ], g = gr[G_KVH], row0 = gr[G_ROW0];
+  const int r = gr[G_SEQ], row0 = gr[G_ROW0];
   const int nsplit = gr[G_NSPLIT], stride = gr[G_STRIDE];
-  // rows past nrows repeat the group's last row (in bounds) and store nothing
-  const int64_t prow = (int64_t)gr[G_PART] + min(lr, nrows - 1);  // partial row of split 0
+  // partial row of split 0 (rows past nrows repeat the group's last row, in
+  // bounds, and store nothing)
+  const int64_t prow = (int64_t)gr[G_PART] + (int64_t)g * a.plan[H_HEAD_PARTIAL] + min(lr, nrows - 1);
   auto part_o = [&](int s) {
     return reinterpret_cast<const vecf*>(a.ws_o + (prow + (int64_t)s * stride) * D) + lane;
   };

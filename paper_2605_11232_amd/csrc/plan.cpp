@@ -411,14 +411,20 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   const int64_t n_row = int64_t(quads.size()) * 4;
   const int64_t n_groups = int64_t(t_groups.size()) * num_kv_heads;
   const int64_t head_members = int64_t(t_members.size());
-  const int64_t shared_off = pa::kHeaderWords;
-  const int64_t tile_off = shared_off + int64_t(shared.size()) * pa::kSharedWords;
-  const int64_t row_off = tile_off + int64_t(tiles.size()) * pa::kItemWords;
-  const int64_t group_off = row_off + n_row * pa::kItemWords;
-  const int64_t member_off = group_off + n_groups * pa::kGroupWords;
-  const int64_t words = member_off + head_members * num_kv_heads;
   const int64_t grid = dtype == PA_F32 ? int64_t(total_q) * num_q_heads
                                        : int64_t(shared.size() + tiles.size() + quads.size());
+  // layout: header, dispatch list, templates (shared, tile, row, group), member table
+  const int64_t dispatch_off = pa::kHeaderWords;
+  const int64_t shared_off = dispatch_off + (dtype == PA_F32 ? 0 : grid);
+  const int64_t tile_off = shared_off + int64_t(t_shared.size()) * pa::kSharedWords;
+  const int64_t row_off = tile_off + int64_t(t_tiles.size()) * pa::kItemWords;
+  const int64_t group_off = row_off + int64_t(sorted_rows.size()) * pa::kItemWords;
+  const int64_t member_off = group_off + int64_t(t_groups.size()) * pa::kGroupWords;
+  const int64_t words = member_off + head_members;
+  if (dtype == PA_BF16 &&
+      (num_kv_heads >= (1 << (31 - pa::kDispatchHeadShift)) ||
+       std::max({t_shared.size(), t_tiles.size(), sorted_rows.size()}) > size_t(pa::kDispatchIndexMask)))
+    return pa::fail(PA_ERR_ARG, "pa_attn_plan: launch too large");
   if (words >= (int64_t{1} << 31) || grid >= (int64_t{1} << 31) || partial_rows >= (int64_t{1} << 31))
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: launch too large");
 
@@ -467,43 +473,28 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   h[pa::H_GROUP_OFF] = int32_t(group_off);
   h[pa::H_MEMBER_OFF] = int32_t(member_off);
   h[pa::H_PARTIAL_ROWS] = int32_t(partial_rows);
-  // an item template stamped for kv-head g (empty slots stay as they are);
-  // partial rows fit int32 (checked above)
-  auto put_item = [&](int32_t* q, const Rec& t, int32_t g) {
-    const bool live = t[pa::I_SEQ] >= 0;
-    const int32_t part = t[pa::I_PART];
-    std::copy(t.begin(), t.end(), q);
-    q[pa::I_KVH] = live ? g : t[pa::I_KVH];
-    q[pa::I_PART] = live && part >= 0 ? part + int32_t(g * head_partial) : part;
-  };
-  int32_t* p = plan + shared_off;
-  for (const auto& [g, i] : shared) {
-    const Rec& t = t_shared[i];
-    std::copy(t.begin(), t.end(), p);
-    p[pa::S_KVH] = g;
-    // absolute word offset of head g's copy of the member table
-    p[pa::S_MEMBERS] = int32_t(member_off + g * head_members + t[pa::S_MEMBERS]);
-    p += pa::kSharedWords;
-  }
-  for (const auto& [g, i] : tiles) {
-    put_item(p, t_tiles[i], g);
-    p += pa::kItemWords;
-  }
-  for (const auto& [g, q0] : quads)
-    for (int32_t k = 0; k < 4; ++k, p += pa::kItemWords) put_item(p, sorted_rows[q0 + k], g);
+  h[pa::H_DISPATCH_OFF] = int32_t(dispatch_off);
+  h[pa::H_HEAD_PARTIAL] = int32_t(head_partial);
+  h[pa::H_N_SHARED_TMPL] = int32_t(t_shared.size());
+  h[pa::H_N_TILE_TMPL] = int32_t(t_tiles.size());
+  h[pa::H_N_ROW_TMPL] = int32_t(sorted_rows.size());
+  h[pa::H_N_GROUP_TMPL] = int32_t(t_groups.size());
   if (dtype == PA_BF16) {
-    for (int32_t g = 0; g < num_kv_heads; ++g)
-      for (const auto& t : t_groups) {
-        std::copy(t.begin(), t.end(), p);
-        p[pa::G_KVH] = g;
-        p[pa::G_PART] = int32_t(t[pa::G_PART] + g * head_partial);
-        p += pa::kGroupWords;
-      }
-    for (int32_t g = 0; g < num_kv_heads; ++g)
-      for (int64_t m = 0; m < head_members; m += 2) {
-        *p++ = t_members[m];
-        *p++ = int32_t(t_members[m + 1] + g * head_partial);
-      }
+    int32_t* p = plan + dispatch_off;
+    auto word = [](const Ref& r) { return (r.first << pa::kDispatchHeadShift) | r.second; };
+    for (const auto& r : shared) *p++ = word(r);
+    for (const auto& r : tiles) *p++ = word(r);
+    for (const auto& r : quads) *p++ = word(r);
+    p = plan + shared_off;
+    for (const auto& t : t_shared) {
+      std::copy(t.begin(), t.end(), p);
+      p[pa::S_MEMBERS] = int32_t(member_off + t[pa::S_MEMBERS]);  // absolute word offset
+      p += pa::kSharedWords;
+    }
+    for (const auto& t : t_tiles) p = std::copy(t.begin(), t.end(), p);
+    for (const auto& t : sorted_rows) p = std::copy(t.begin(), t.end(), p);
+    for (const auto& t : t_groups) p = std::copy(t.begin(), t.end(), p);
+    p = std::copy(t_members.begin(), t_members.end(), p);
   }
   return PA_OK;
 }

@@ -9,30 +9,48 @@ namespace pa {
 constexpr int32_t kPlanMagic = 0x31304150;  // "PA01"
 
 // Header words.
+//
+// Work is described once, as templates for kv-head 0, and a dispatch list
+// assigns each workgroup of the attention launch a kv-head and a template:
+// dispatch word (g << kDispatchHeadShift) | i.  Workgroups [0, N_SHARED) run
+// shared-prefix template i, [N_SHARED, N_SHARED + N_TILE) tile template i,
+// the rest row templates i .. i + 3 (one per wavefront).  Kv-head g's items
+// write the partial rows of head 0's template plus g * HEAD_PARTIAL; merge
+// group b of the merge launch is group template b % N_GROUP_TMPL of kv-head
+// b / N_GROUP_TMPL.
 enum : int32_t {
   H_MAGIC = 0,
   H_KIND,
-  H_N_SHARED,      // shared-prefix tile items (cascade), one workgroup each
-  H_N_TILE,        // 128-row items, one workgroup each
-  H_N_ROW,         // <= kRowItemRows-row items, one wavefront each (multiple of 4, padded)
-  H_N_GROUPS,      // merge groups combined by the merge kernel
+  H_N_SHARED,      // shared-prefix (cascade) workgroups, all kv-heads
+  H_N_TILE,        // tile workgroups (128-row items), all kv-heads
+  H_N_ROW,         // row items (one wavefront each), all kv-heads, padded to whole workgroups
+  H_N_GROUPS,      // merge groups, all kv-heads
   H_GRID,          // workgroups of the attention launch = N_SHARED + N_TILE + N_ROW / 4
   H_HQ,
   H_HKV,
   H_D,
   H_N_SEQS,
   H_TOTAL_Q,
-  H_SHARED_OFF,    // word offset of the shared items
-  H_TILE_OFF,      // word offset of the tile items
-  H_ROW_OFF,       // word offset of the row items
-  H_GROUP_OFF,     // word offset of the merge groups
-  H_MEMBER_OFF,    // word offset of the cascade member tables
-  H_PARTIAL_ROWS,  // rows of partial results in the workspace
+  H_SHARED_OFF,    // word offset of the shared-prefix templates
+  H_TILE_OFF,      // word offset of the tile templates
+  H_ROW_OFF,       // word offset of the row templates (whole quads, padded)
+  H_GROUP_OFF,     // word offset of the merge-group templates
+  H_MEMBER_OFF,    // word offset of the cascade member tables (kv-head 0)
+  H_PARTIAL_ROWS,  // rows of partial results in the workspace, all kv-heads
+  H_DISPATCH_OFF,  // word offset of the dispatch list (GRID words): kHeaderWords
+  H_HEAD_PARTIAL,  // partial rows of one kv-head
+  H_N_SHARED_TMPL, // templates of each kind
+  H_N_TILE_TMPL,
+  H_N_ROW_TMPL,
+  H_N_GROUP_TMPL,
   kHeaderWords = 24
 };
+constexpr int32_t kDispatchHeadShift = 24;  // template index < 2^24, kv-head < 2^7
+constexpr int32_t kDispatchIndexMask = (1 << kDispatchHeadShift) - 1;
 
-// Work item (tile or row item): rows [row0, row0 + nrows) of sequence seq's
-// packed (query, head-in-group) rows for kv-head kvh, keys [kv0, kv1).
+// Work item (tile or row item; templates hold kvh = 0): rows [row0, row0 +
+// nrows) of sequence seq's packed (query, head-in-group) rows for kv-head
+// kvh, keys [kv0, kv1).
 // Row rho is query rho / G, q-head kvh * G + rho % G.  part = -1: write the
 // final output; otherwise the item writes normalised partial outputs and
 // log-sum-exps at workspace rows part + (rho - row0).  seq = -1: empty slot.
@@ -46,8 +64,8 @@ enum : int32_t {
 // rows in order) for kv-head kvh, over the group's shared keys [kv0, kv1),
 // which every member's block table maps to the same blocks (read from
 // sequence block_seq's row).  The member table at word offset members holds
-// (sequence, partial base) pairs; member m's row rho goes to partial row
-// base + rho (split 0 of its merge group).
+// (sequence, partial base) pairs for kv-head 0; member m's row rho goes to
+// partial row base + rho (+ the kv-head's partial offset).
 enum : int32_t {
   S_MEMBERS = 0, S_KVH, S_ROW0, S_NROWS, S_KV0, S_KV1, S_RPM, S_BLOCK_SEQ,
   kSharedWords = 8

@@ -198,6 +198,9 @@ def test_workload_tables_bit_exact(name):
 # plan layout (plan_format.h): header words, record sizes
 H_N_SHARED, H_N_TILE, H_N_ROW, H_N_GROUPS, H_GRID = 2, 3, 4, 5, 6
 H_SHARED_OFF, H_TILE_OFF, H_ROW_OFF, H_GROUP_OFF, H_MEMBER_OFF, H_PARTIAL_ROWS = 12, 13, 14, 15, 16, 17
+H_DISPATCH_OFF, H_HEAD_PARTIAL, H_HKV = 18, 19, 8
+H_N_SHARED_TMPL, H_N_TILE_TMPL, H_N_ROW_TMPL, H_N_GROUP_TMPL = 20, 21, 22, 23
+HEAD_SHIFT = 24           # dispatch word: (kv-head << 24) | template index
 WAVES = 4                 # wavefronts per workgroup: row items come WAVES to a workgroup
 TILE_ROWS = 32 * WAVES    # rows of a tile or shared item (32 per wavefront)
 ROW_ITEM_ROWS = 32        # rows of a row item (two 16-column MFMA tiles)
@@ -205,10 +208,35 @@ VARIANT_WIDE_ROWS = 2     # plan info variant bit: some row item has more than 1
 
 
 def parse_plan(plan):
+    """The plan's work per workgroup, expanded from the dispatch list and the
+    kv-head-0 templates: shared items as (member table, kvh, row0, nrows,
+    kv0, kv1, rows per member, block sequence, partial offset), tile and row
+    items and merge groups with their kv-head and partial rows stamped."""
     h = plan[:24]
-    rec = lambda off, n: plan[off:off + 8 * n].reshape(-1, 8).tolist()
-    return (h, rec(h[H_SHARED_OFF], h[H_N_SHARED]), rec(h[H_TILE_OFF], h[H_N_TILE]),
-            rec(h[H_ROW_OFF], h[H_N_ROW]), rec(h[H_GROUP_OFF], h[H_N_GROUPS]))
+    hp = int(h[H_HEAD_PARTIAL])
+    tmpl = lambda off, n: plan[off:off + 8 * n].reshape(-1, 8).tolist()
+    ts, tt = tmpl(h[H_SHARED_OFF], h[H_N_SHARED_TMPL]), tmpl(h[H_TILE_OFF], h[H_N_TILE_TMPL])
+    tr, tg = tmpl(h[H_ROW_OFF], h[H_N_ROW_TMPL]), tmpl(h[H_GROUP_OFF], h[H_N_GROUP_TMPL])
+    disp = plan[h[H_DISPATCH_OFF]:h[H_DISPATCH_OFF] + h[H_GRID]].tolist()
+    assert all(w >= 0 for w in disp)
+    split = [(w >> HEAD_SHIFT, w & ((1 << HEAD_SHIFT) - 1)) for w in disp]
+    ns, nt = h[H_N_SHARED], h[H_N_TILE]
+
+    def stamp(t, g):
+        t = list(t)
+        assert t[1] == 0            # templates are kv-head 0's
+        if t[0] >= 0:
+            t[1] = g
+            if t[6] >= 0:
+                t[6] += g * hp
+        return t
+    shared = [tuple(ts[i][:1]) + (g,) + tuple(ts[i][2:]) + (g * hp,) for g, i in split[:ns]]
+    tiles = [stamp(tt[i], g) for g, i in split[ns:ns + nt]]
+    rows = [stamp(tr[i + k], g) for g, i in split[ns + nt:] for k in range(WAVES)]
+    groups = [[t[0], g, t[2], t[3], t[4], t[5] + g * hp, t[6], t[7]]
+              for g in range(h[H_HKV]) for t in tg]
+    assert len(groups) == h[H_N_GROUPS] and len(rows) == h[H_N_ROW]
+    return h, shared, tiles, rows, groups
 
 
 def check_plan(plan, info, L, cu, G, hkv, D=128):
@@ -238,12 +266,12 @@ def check_plan(plan, info, L, cu, G, hkv, D=128):
         assert kv0 % 16 == 0 and 0 <= kv0 < kv1 <= L[seq]
         for lr in range(nrows):
             add((seq, kvh, row0 + lr), kv0, kv1, -1 if part < 0 else part + lr)
-    for moff, kvh, row0, nrows, kv0, kv1, rpm, bseq in shared:
+    for moff, kvh, row0, nrows, kv0, kv1, rpm, bseq, poff in shared:
         assert kv0 % 64 == 0 and kv1 % 64 == 0
         for lr in range(nrows):
             rg = row0 + lr
             m, rl = divmod(rg, rpm)
-            seq, base = plan[moff + 2 * m], plan[moff + 2 * m + 1]
+            seq, base = plan[moff + 2 * m], plan[moff + 2 * m + 1] + poff
             assert kv1 <= L[seq] - q[seq]          # every shared key is visible
             add((seq, kvh, rl), kv0, kv1, base + rl)
     assert len(cover) == sum(int(q[s]) * G * hkv for s in range(n))
