@@ -213,6 +213,7 @@ def parse_plan(plan):
     kv0, kv1, rows per member, block sequence, partial offset), tile and row
     items and merge groups with their kv-head and partial rows stamped."""
     h = plan[:24]
+    assert h[H_DISPATCH_OFF] == 24   # the dispatch list follows the header
     hp = int(h[H_HEAD_PARTIAL])
     tmpl = lambda off, n: plan[off:off + 8 * n].reshape(-1, 8).tolist()
     ts, tt = tmpl(h[H_SHARED_OFF], h[H_N_SHARED_TMPL]), tmpl(h[H_TILE_OFF], h[H_N_TILE_TMPL])
