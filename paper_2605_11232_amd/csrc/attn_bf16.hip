@@ -238,38 +238,42 @@ __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, co
   const char* vbase = reinterpret_cast<const char*>(a.vc + (int64_t)g * D * kBlock);
   const int64_t blk_bytes = (int64_t)a.hkv * kBlock * D * 2;  // one block, all kv-heads
 
-  // Block ids of a step (wave-uniform).  Blocks at or past kend alias the
-  // step's first block, so every copy reads inside the cache; their keys are
-  // masked and their values zeroed before use.
+  // Block ids of a step (wave-uniform), clamped into the cache when the
+  // window of 64 table entries is fetched.  Blocks at or past kend read the
+  // item's last block again, so every copy reads inside the cache; their keys
+  // are masked and their values zeroed before use.  Steps advance NB blocks
+  // from the window's first block, so a step's blocks never straddle two
+  // windows: one window check per step.
   BlockWindow win;
-  win.init(bt, a.max_blocks, kv0 / kBlock);
-  auto step_blocks = [&](int t0, int (&blk)[NB]) {
+  win.init(bt, kend > 0 ? (kend - 1) / kBlock : 0, a.num_blocks, kv0 / kBlock);
+  // blk[b]: byte offset of the step's block b (all kv-heads per block), so
+  // each block's address is computed once for its K and its V^T copies
+  auto step_blocks = [&](int t0, int64_t (&blk)[NB]) {
     const int jb = t0 / kBlock;
-    blk[0] = clamp_block(win.get(jb), a.num_blocks);
+    win.seek(jb);
 #pragma unroll
-    for (int b = 1; b < NB; ++b)
-      blk[b] = t0 + kBlock * b < kend ? clamp_block(win.get(jb + b), a.num_blocks) : blk[0];
+    for (int b = 0; b < NB; ++b) blk[b] = (int64_t)win.at(jb + b) * blk_bytes;
   };
   // Copy slot i of wavefront w lands in block (4 i + w) * 64 / (2 D) of the
   // step: block i for D = 128, block 2 i + w / 2 for D = 64.
   static_assert(NI >= 1, "at least one copy per wavefront");
   static_assert(D == 64 || D == 128, "head_dim 64 or 128");
-  auto copy_block = [&](const int (&blk)[NB], int i) {
+  auto copy_block = [&](const int64_t (&blk)[NB], int i) {
     if constexpr (D == 128) return blk[i];
     else return blk[2 * i] + ((w >> 1) & 1) * (blk[2 * i + 1] - blk[2 * i]);  // no indexed array
   };
   // one (block, kv-head) of K or V^T: kBlock * D bf16 at the block's address
   constexpr int kHeadBytes = kBlock * D * 2;
-  auto issue_k = [&](const int (&blk)[NB], int buf) {
+  auto issue_k = [&](const int64_t (&blk)[NB], int buf) {
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      copy16_to_lds(kbase + (int64_t)copy_block(blk, i) * blk_bytes, kHeadBytes, koff[i],
+      copy16_to_lds(kbase + copy_block(blk, i), kHeadBytes, koff[i],
                     &sm.k[buf][512 * (4 * i + w)]);
   };
-  auto issue_v = [&](const int (&blk)[NB], int buf) {
+  auto issue_v = [&](const int64_t (&blk)[NB], int buf) {
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      copy16_to_lds(vbase + (int64_t)copy_block(blk, i) * blk_bytes, kHeadBytes, voff[i],
+      copy16_to_lds(vbase + copy_block(blk, i), kHeadBytes, voff[i],
                     &sm.v[buf][512 * (4 * i + w)]);
   };
 
@@ -378,7 +382,7 @@ __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, co
   // steps [0, n_plain) need no causal or tail mask for any row of the item
   const int n_plain = min(ntiles, max(0, (wg_amin + 1 - kv0) / KT));
   if (ntiles > 0) {
-    int bk[NB] = {}, bv[NB];
+    int64_t bk[NB] = {}, bv[NB];
     step_blocks(kv0, bv);
     issue_k(bv, 0);
     issue_v(bv, 0);

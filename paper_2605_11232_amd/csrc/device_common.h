@@ -59,29 +59,42 @@ __device__ __forceinline__ float wave_xor(float v, int mask) { return __shfl_xor
 // v_readlane (no scalar-memory wait inside the key loop).
 struct BlockWindow {
   const int32_t* row;
-  int max_blocks;
-  int base;  // first block index held in `cur`
+  int last;        // table index of the last block in use; later entries read it again
+  int num_blocks;  // ids are clamped to [0, num_blocks) when fetched
+  int base;        // first block index held in `cur`
   int cur, next;
 
   __device__ __forceinline__ int fetch(int first) const {
     const int j = first + (threadIdx.x & 63);
-    return row[j < max_blocks ? j : max_blocks - 1];
+    const int id = row[j < last ? j : last];
+    return id < 0 ? 0 : (id >= num_blocks ? num_blocks - 1 : id);
   }
-  __device__ __forceinline__ void init(const int32_t* r, int mb, int first_block) {
+  __device__ __forceinline__ void init(const int32_t* r, int last_block, int nblocks, int first_block) {
     row = r;
-    max_blocks = mb;
+    last = last_block;
+    num_blocks = nblocks;
     base = first_block;
     cur = fetch(base);
     next = fetch(base + 64);
   }
-  // Block id of logical block jb (wave-uniform, jb >= base, non-decreasing).
-  __device__ __forceinline__ int get(int jb) {
+  // Make logical blocks jb .. jb + n - 1 readable with at() (wave-uniform;
+  // jb >= base, non-decreasing; the n blocks must not straddle a window, which
+  // holds when the caller steps through its blocks n at a time from the first
+  // block it passed to init).
+  __device__ __forceinline__ void seek(int jb) {
     while (jb - base >= 64) {
       base += 64;
       cur = next;
       next = fetch(base + 64);
     }
+  }
+  __device__ __forceinline__ int at(int jb) const {
     return __builtin_amdgcn_readlane(cur, jb - base);
+  }
+  // Block id of logical block jb (wave-uniform, jb >= base, non-decreasing).
+  __device__ __forceinline__ int get(int jb) {
+    seek(jb);
+    return at(jb);
   }
 };
 
