@@ -252,7 +252,8 @@ __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, co
     const int jb = t0 / kBlock;
     win.seek(jb);
 #pragma unroll
-    for (int b = 0; b < NB; ++b) blk[b] = (int64_t)win.at(jb + b) * blk_bytes;
+    for (int b = 0; b < NB; ++b)
+      blk[b] = (int64_t)((uint64_t)(uint32_t)win.at(jb + b) * (uint32_t)blk_bytes);  // ids >= 0
   };
   // Copy slot i of wavefront w lands in block (4 i + w) * 64 / (2 D) of the
   // step: block i for D = 128, block 2 i + w / 2 for D = 64.
@@ -382,13 +383,15 @@ __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, co
   // steps [0, n_plain) need no causal or tail mask for any row of the item
   const int n_plain = min(ntiles, max(0, (wg_amin + 1 - kv0) / KT));
   if (ntiles > 0) {
-    int64_t bk[NB] = {}, bv[NB];
-    step_blocks(kv0, bv);
-    issue_k(bv, 0);
-    issue_v(bv, 0);
+    // blk[t % 2]: byte offsets of step t's blocks, found two steps ahead
+    // (for the K copy) and used again one step ahead (for the V^T copy)
+    int64_t blk[2][NB] = {};
+    step_blocks(kv0, blk[0]);
+    issue_k(blk[0], 0);
+    issue_v(blk[0], 0);
     if (ntiles > 1) {
-      step_blocks(kv0 + KT, bv);
-      issue_k(bv, 1);
+      step_blocks(kv0 + KT, blk[1]);
+      issue_k(blk[1], 1);
     }
     wait_vmem();
     __syncthreads();
@@ -411,12 +414,10 @@ __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, co
       constexpr int buf = decltype(buf_c)::value;
       const int t0 = kv0 + KT * t;
       if (t + 2 < ntiles) {
-        step_blocks(t0 + 2 * KT, bk);
-        issue_k(bk, buf);
+        step_blocks(t0 + 2 * KT, blk[buf]);
+        issue_k(blk[buf], buf);
       }
-      issue_v(bv, 1 - buf);  // blocks of step t + 1, found one step earlier
-#pragma unroll
-      for (int b = 0; b < NB; ++b) bv[b] = bk[b];
+      issue_v(blk[1 - buf], 1 - buf);  // blocks of step t + 1, found one step earlier
       bf16x8 p[NSUB][2];
       f32x16 sn[NSUB];
       probs(s, p);
@@ -438,15 +439,14 @@ __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, co
 #pragma unroll
       for (int u = 0; u < NSUB; ++u) s[u] = sn[u];
     };
-    auto idle_step = [&](int t) {
+    auto idle_step = [&](int t, auto buf_c) {
+      constexpr int buf = decltype(buf_c)::value;
       const int t0 = kv0 + KT * t;
       if (t + 2 < ntiles) {
-        step_blocks(t0 + 2 * KT, bk);
-        issue_k(bk, t & 1);
+        step_blocks(t0 + 2 * KT, blk[buf]);
+        issue_k(blk[buf], buf);
       }
-      issue_v(bv, (t + 1) & 1);
-#pragma unroll
-      for (int b = 0; b < NB; ++b) bv[b] = bk[b];
+      issue_v(blk[1 - buf], 1 - buf);
       wait_vmem();
       __syncthreads();
     };
@@ -466,7 +466,11 @@ __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, co
       run(t, min(n_plain, ntiles) - 1, std::false_type{});
       run(t, ntiles - 1, std::true_type{});
     } else {
-      for (; t + 1 < ntiles; ++t) idle_step(t);
+      for (; t + 2 < ntiles; t += 2) {
+        idle_step(t, B0{});
+        idle_step(t + 1, B1{});
+      }
+      if (t + 1 < ntiles) idle_step(t++, B0{});
     }
     // last step: softmax + PV only
     const int t0 = kv0 + KT * t;
