@@ -372,14 +372,40 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     // head's XCD queues (which stay longest first).
     std::vector<std::vector<int>> xs_of(num_kv_heads);
     for (int32_t g = 0; g < num_kv_heads; ++g) xs_of[g] = xcds_of_head(g, num_kv_heads);
+    // With by_seq (tile items grouped by sequence), a head spread over
+    // several XCDs gets each sequence's items on one XCD, the least loaded so
+    // far, so the sequence's keys are fetched into one L2; a sequence costing
+    // more than half an XCD's share is still dealt round robin.
     auto deal = [&](const std::vector<int64_t>& costs, const std::vector<Rec>* by_seq) {
       const auto ord = by_seq ? order_by_sequence(costs, *by_seq) : order_longest_first(costs);
       std::vector<std::vector<Ref>> q(kXcds);
       for (auto& x : q) x.reserve(ord.size() * num_kv_heads / kXcds + ord.size());
+      int64_t total = 0;
+      for (int64_t c : costs) total += c;
+      std::array<int64_t, kXcds> load{};
       for (int32_t g = 0; g < num_kv_heads; ++g) {
         const auto& xs = xs_of[g];
-        for (size_t i = 0, x = 0; i < ord.size(); ++i, x = x + 1 == xs.size() ? 0 : x + 1)
-          q[xs[x]].push_back({g, ord[i]});
+        size_t x = 0;
+        for (size_t i = 0; i < ord.size();) {
+          size_t e = i + 1;  // the run of items of one sequence
+          int64_t run = costs[ord[i]];
+          if (by_seq && xs.size() > 1) {
+            while (e < ord.size() && (*by_seq)[ord[e]][pa::I_SEQ] == (*by_seq)[ord[i]][pa::I_SEQ])
+              run += costs[ord[e++]];
+          }
+          if (e - i > 1 && 2 * run * int64_t(xs.size()) <= total) {
+            size_t best = 0;
+            for (size_t k = 1; k < xs.size(); ++k)
+              if (load[xs[k]] < load[xs[best]]) best = k;
+            for (; i < e; ++i) q[xs[best]].push_back({g, ord[i]});
+            load[xs[best]] += run;
+          } else {
+            for (; i < e; ++i, x = x + 1 == xs.size() ? 0 : x + 1) {
+              q[xs[x]].push_back({g, ord[i]});
+              load[xs[x]] += costs[ord[i]];
+            }
+          }
+        }
       }
       return interleave(q);
     };
