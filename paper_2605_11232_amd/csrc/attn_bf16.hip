@@ -721,24 +721,24 @@ constexpr int waves_per_eu() { return MIX == 2 ? 3 : kTileWavesPerEu; }
 template <int D, int MIX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_eu<MIX>()))) void attn_bf16_kernel(AttnArgs a) {
   const int32_t* plan = a.plan;
-  const int n_shared = plan[H_N_SHARED];
-  const int n_tile = n_shared + plan[H_N_TILE];  // workgroups before the row quads
-  const int b = blockIdx.x;
   // this workgroup's kv-head and template (the dispatch list follows the
-  // header, so its word loads together with the header words)
-  const int wd = plan[kHeaderWords + b];
+  // header, so its word loads together with the header words); template
+  // indices run over the shared, tile and row templates in that order
+  const int wd = plan[kHeaderWords + blockIdx.x];
   const int g = wd >> kDispatchHeadShift, ti = wd & kDispatchIndexMask;
+  const int n_shared = plan[H_N_SHARED_TMPL];
+  const int n_tile = n_shared + plan[H_N_TILE_TMPL];  // templates before the row templates
   const int poff = g * plan[H_HEAD_PARTIAL];  // the kv-head's partial rows
   if constexpr (MIX & 1) {
     __shared__ TileSmem<D, kTileSub> sm;
-    if (b < n_shared) {
+    if (ti < n_shared) {
       const int32_t* it = plan + plan[H_SHARED_OFF] + ti * kSharedWords;
       if (it[S_NROWS] > kTileRows - 32) tile_item<D, kTileSub, true, true>(it, g, poff, a, sm);
       else tile_item<D, kTileSub, true, false>(it, g, poff, a, sm);
       return;
     }
-    if (b < n_tile) {
-      const int32_t* it = plan + plan[H_TILE_OFF] + ti * kItemWords;
+    if (ti < n_tile) {
+      const int32_t* it = plan + plan[H_TILE_OFF] + (ti - n_shared) * kItemWords;
       // every wavefront has rows: the plain path; otherwise idle ones skip compute
       if (it[I_NROWS] > kTileRows - 32) tile_item<D, kTileSub, false, true>(it, g, poff, a, sm);
       else tile_item<D, kTileSub, false, false>(it, g, poff, a, sm);
@@ -746,9 +746,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_e
     }
   }
   if constexpr ((MIX & 6) != 0) {
-    if (b >= n_tile) {
+    if (ti >= n_tile) {
       // a quad of row templates, one per wavefront
-      const int32_t* it = plan + plan[H_ROW_OFF] + (ti + (threadIdx.x >> 6)) * kItemWords;
+      const int32_t* it =
+          plan + plan[H_ROW_OFF] + (ti - n_tile + (threadIdx.x >> 6)) * kItemWords;
       if constexpr ((MIX & 4) != 0) {
         if (it[I_NROWS] > 16) {
           row_item<D, 2>(it, g, poff, a);

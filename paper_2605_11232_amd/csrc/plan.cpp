@@ -117,16 +117,17 @@ int64_t common_prefix(const int32_t* a, const int32_t* b, int64_t n) {
   return k;
 }
 
-// Interleave per-XCD queues of units into dispatch order: unit slot b goes to
-// queue b % kXcds while it has units, else to the longest remaining queue.
+// Append per-XCD queues of units to dispatch list `out`: the unit at dispatch
+// position b goes to queue b % kXcds (the XCD that runs workgroup b) while it
+// has units, else to the longest remaining queue.
 template <class U>
-std::vector<U> interleave(const std::vector<std::vector<U>>& queues) {
-  std::vector<U> out;
+void interleave(std::vector<U>& out, const std::vector<std::vector<U>>& queues) {
   std::vector<size_t> pos(queues.size(), 0);
   size_t total = 0;
   for (auto& q : queues) total += q.size();
-  out.reserve(total);
-  for (size_t b = 0, slot = 0; b < total; ++b, slot = slot + 1 == queues.size() ? 0 : slot + 1) {
+  out.reserve(out.size() + total);
+  for (size_t b = 0, slot = out.size() % queues.size(); b < total;
+       ++b, slot = slot + 1 == queues.size() ? 0 : slot + 1) {
     size_t q = slot;
     if (pos[q] >= queues[q].size()) {
       size_t best = q;
@@ -137,7 +138,6 @@ std::vector<U> interleave(const std::vector<std::vector<U>>& queues) {
     }
     out.push_back(queues[q][pos[q]++]);
   }
-  return out;
 }
 
 }  // namespace
@@ -198,7 +198,11 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   std::vector<int32_t> t_members;  // head 0's member tables: (sequence, partial base) pairs
   std::vector<Rec> sorted_rows;    // row templates, longest first, padded to whole quads
   int64_t head_partial = 0;
-  std::vector<Ref> shared, tiles, quads;  // quads: (kv-head, first index into sorted_rows)
+  // dispatch list: (kv-head, template index) per workgroup; template indices
+  // run over the shared, tile and row templates in that order (a row
+  // workgroup names the first of its four row templates)
+  std::vector<Ref> dispatch;
+  int64_t n_shared_wg = 0, n_tile_wg = 0, n_quads = 0;
 
   if (dtype == PA_BF16) {
     auto qlen = [&](int32_t r) { return cu_seqlens_q[r + 1] - cu_seqlens_q[r]; };
@@ -407,13 +411,18 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
           }
         }
       }
-      return interleave(q);
+      return q;
     };
-    shared = deal(shared_cost, nullptr);
+    auto shift = [](std::vector<std::vector<Ref>>& q, int32_t by) {
+      for (auto& x : q)
+        for (auto& r : x) r.second += by;
+    };
+    auto shared_q = deal(shared_cost, nullptr);
 #ifndef PA_TILE_ORDER
 #define PA_TILE_ORDER 1
 #endif
-    tiles = deal(tile_cost, PA_TILE_ORDER ? &t_tiles : nullptr);
+    auto tile_q = deal(tile_cost, PA_TILE_ORDER ? &t_tiles : nullptr);
+    shift(tile_q, int32_t(t_shared.size()));
     // Row items: per head, longest first, four to a workgroup (padded with
     // empty items) so a workgroup's waves share one kv-head.
     {
@@ -423,22 +432,45 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       while (sorted_rows.size() % 4) sorted_rows.push_back({-1, 0, 0, 0, 0, 0, -1, 0});
     }
     const int32_t nq = int32_t(sorted_rows.size() / 4);
+    const int32_t row_base = int32_t(t_shared.size() + t_tiles.size());
     std::vector<std::vector<Ref>> quad_q(kXcds);
     for (auto& x : quad_q) x.reserve(size_t(nq) * num_kv_heads / kXcds + nq);
     for (int32_t g = 0; g < num_kv_heads; ++g) {
       const auto& xs = xs_of[g];
       for (size_t q = 0, x = 0; q < size_t(nq); ++q, x = x + 1 == xs.size() ? 0 : x + 1)
-        quad_q[xs[x]].push_back({g, int32_t(4 * q)});
+        quad_q[xs[x]].push_back({g, row_base + int32_t(4 * q)});
     }
-    quads = interleave(quad_q);
+    for (const auto& x : shared_q) n_shared_wg += int64_t(x.size());
+    for (const auto& x : tile_q) n_tile_wg += int64_t(x.size());
+    n_quads = int64_t(nq) * num_kv_heads;
+    // Dispatch order: shared-prefix items first, one per CU at most, then the
+    // tile items, then the remaining shared items, then the row quads.  With
+    // more shared items than CUs, every CU then starts one shared item beside
+    // one tile item, and the rest of the shared work takes the slots the
+    // (memory-bound, shorter) tile items free.
+    {
+      const size_t per_xcd = size_t(cdiv(num_cus > 0 ? num_cus : 256, kXcds));
+      std::vector<std::vector<Ref>> first(kXcds), rest(kXcds);
+      for (int x = 0; x < kXcds; ++x) {
+        const auto& v = shared_q[x];
+        const size_t k = std::min(v.size(), per_xcd);
+        first[x].assign(v.begin(), v.begin() + k);
+        rest[x].assign(v.begin() + k, v.end());
+      }
+      dispatch.reserve(size_t(n_shared_wg + n_tile_wg + n_quads));
+      interleave(dispatch, first);
+      interleave(dispatch, tile_q);
+      interleave(dispatch, rest);
+      interleave(dispatch, quad_q);
+    }
   }
 
   const int64_t partial_rows = head_partial * num_kv_heads;
-  const int64_t n_row = int64_t(quads.size()) * 4;
+  const int64_t n_row = n_quads * 4;
   const int64_t n_groups = int64_t(t_groups.size()) * num_kv_heads;
   const int64_t head_members = int64_t(t_members.size());
   const int64_t grid = dtype == PA_F32 ? int64_t(total_q) * num_q_heads
-                                       : int64_t(shared.size() + tiles.size() + quads.size());
+                                       : int64_t(dispatch.size());
   // layout: header, dispatch list, templates (shared, tile, row, group), member table
   const int64_t dispatch_off = pa::kHeaderWords;
   const int64_t shared_off = dispatch_off + (dtype == PA_F32 ? 0 : grid);
@@ -449,15 +481,15 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   const int64_t words = member_off + head_members;
   if (dtype == PA_BF16 &&
       (num_kv_heads >= (1 << (31 - pa::kDispatchHeadShift)) ||
-       std::max({t_shared.size(), t_tiles.size(), sorted_rows.size()}) > size_t(pa::kDispatchIndexMask)))
+       t_shared.size() + t_tiles.size() + sorted_rows.size() > size_t(pa::kDispatchIndexMask)))
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: launch too large");
   if (words >= (int64_t{1} << 31) || grid >= (int64_t{1} << 31) || partial_rows >= (int64_t{1} << 31))
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: launch too large");
 
   info->kind = kind;
   info->n_q = n_q;
-  info->n_shared_items = int32_t(shared.size());
-  info->n_tile_items = int32_t(tiles.size());
+  info->n_shared_items = int32_t(n_shared_wg);
+  info->n_tile_items = int32_t(n_tile_wg);
   info->n_row_items = int32_t(n_row);
   info->n_groups = int32_t(n_groups);
   info->n_merge_rows = 0;
@@ -483,8 +515,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   std::fill(h, h + pa::kHeaderWords, 0);
   h[pa::H_MAGIC] = pa::kPlanMagic;
   h[pa::H_KIND] = kind;
-  h[pa::H_N_SHARED] = int32_t(shared.size());
-  h[pa::H_N_TILE] = int32_t(tiles.size());
+  h[pa::H_N_SHARED] = int32_t(n_shared_wg);
+  h[pa::H_N_TILE] = int32_t(n_tile_wg);
   h[pa::H_N_ROW] = int32_t(n_row);
   h[pa::H_N_GROUPS] = int32_t(n_groups);
   h[pa::H_GRID] = int32_t(grid);
@@ -508,9 +540,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   if (dtype == PA_BF16) {
     int32_t* p = plan + dispatch_off;
     auto word = [](const Ref& r) { return (r.first << pa::kDispatchHeadShift) | r.second; };
-    for (const auto& r : shared) *p++ = word(r);
-    for (const auto& r : tiles) *p++ = word(r);
-    for (const auto& r : quads) *p++ = word(r);
+    for (const auto& r : dispatch) *p++ = word(r);
     p = plan + shared_off;
     for (const auto& t : t_shared) {
       std::copy(t.begin(), t.end(), p);

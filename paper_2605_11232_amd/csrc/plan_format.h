@@ -12,9 +12,11 @@ constexpr int32_t kPlanMagic = 0x31304150;  // "PA01"
 //
 // Work is described once, as templates for kv-head 0, and a dispatch list
 // assigns each workgroup of the attention launch a kv-head and a template:
-// dispatch word (g << kDispatchHeadShift) | i.  Workgroups [0, N_SHARED) run
-// shared-prefix template i, [N_SHARED, N_SHARED + N_TILE) tile template i,
-// the rest row templates i .. i + 3 (one per wavefront).  Kv-head g's items
+// dispatch word (g << kDispatchHeadShift) | i, where i indexes the shared-
+// prefix, tile and row templates in that order: i < N_SHARED_TMPL names
+// shared-prefix template i, the next N_TILE_TMPL indices the tile templates,
+// the rest the first of four row templates (one per wavefront); the kinds
+// may interleave in the dispatch list.  Kv-head g's items
 // write the partial rows of head 0's template plus g * HEAD_PARTIAL; merge
 // group b of the merge launch is group template b % N_GROUP_TMPL of kv-head
 // b / N_GROUP_TMPL.
@@ -45,7 +47,7 @@ enum : int32_t {
   H_N_GROUP_TMPL,
   kHeaderWords = 24
 };
-constexpr int32_t kDispatchHeadShift = 24;  // template index < 2^24, kv-head < 2^7
+constexpr int32_t kDispatchHeadShift = 24;  // template index < 2^24 (all kinds), kv-head < 2^7
 constexpr int32_t kDispatchIndexMask = (1 << kDispatchHeadShift) - 1;
 
 // Work item (tile or row item; templates hold kvh = 0): rows [row0, row0 +

@@ -221,7 +221,13 @@ def parse_plan(plan):
     disp = plan[h[H_DISPATCH_OFF]:h[H_DISPATCH_OFF] + h[H_GRID]].tolist()
     assert all(w >= 0 for w in disp)
     split = [(w >> HEAD_SHIFT, w & ((1 << HEAD_SHIFT) - 1)) for w in disp]
-    ns, nt = h[H_N_SHARED], h[H_N_TILE]
+    # template indices run over the shared, tile and row templates in order
+    n_st, n_tt = h[H_N_SHARED_TMPL], h[H_N_TILE_TMPL]
+    s_split = [(g, i) for g, i in split if i < n_st]
+    t_split = [(g, i - n_st) for g, i in split if n_st <= i < n_st + n_tt]
+    r_split = [(g, i - n_st - n_tt) for g, i in split if i >= n_st + n_tt]
+    assert len(s_split) == h[H_N_SHARED] and len(t_split) == h[H_N_TILE]
+    assert all(i % WAVES == 0 and i < h[H_N_ROW_TMPL] for _, i in r_split)
 
     def stamp(t, g):
         t = list(t)
@@ -231,9 +237,9 @@ def parse_plan(plan):
             if t[6] >= 0:
                 t[6] += g * hp
         return t
-    shared = [tuple(ts[i][:1]) + (g,) + tuple(ts[i][2:]) + (g * hp,) for g, i in split[:ns]]
-    tiles = [stamp(tt[i], g) for g, i in split[ns:ns + nt]]
-    rows = [stamp(tr[i + k], g) for g, i in split[ns + nt:] for k in range(WAVES)]
+    shared = [tuple(ts[i][:1]) + (g,) + tuple(ts[i][2:]) + (g * hp,) for g, i in s_split]
+    tiles = [stamp(tt[i], g) for g, i in t_split]
+    rows = [stamp(tr[i + k], g) for g, i in r_split for k in range(WAVES)]
     groups = [[t[0], g, t[2], t[3], t[4], t[5] + g * hp, t[6], t[7]]
               for g in range(h[H_HKV]) for t in tg]
     assert len(groups) == h[H_N_GROUPS] and len(rows) == h[H_N_ROW]
