@@ -345,6 +345,39 @@ def test_plan_covers_every_row_once():
                 assert info.n_shared_items == 0
 
 
+def _workload_plan(name, scale):
+    wl = synth.workload(name, scale=scale)
+    o = PrefixCacheOracle(wl.num_blocks, wl.cfg.block_size, wl.free_order)
+    for op in wl.setup:
+        if op.kind == "add":
+            o.add(op.seq_id, op.tokens)
+        elif op.kind == "free":
+            o.free_seq(op.seq_id)
+    launch = wl.step(0) if wl.step else wl.launches[0]
+    for op in launch.pre:
+        (o.add if op.kind == "add" else o.extend)(op.seq_id, op.tokens)
+    md = o.metadata(launch.seq_ids, launch.q_lens, wl.max_blocks_per_seq)
+    cfg = wl.cfg
+    kind = {"decode": B.KIND_DECODE, "verify": B.KIND_VERIFY}.get(name, B.KIND_PREFILL)
+    plan, info = B.plan(kind, int(max(launch.q_lens)), md["seq_lens"], md["cu_seqlens_q"],
+                        cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 16, B.PA_BF16, 256,
+                        block_table=md["block_table"])
+    return plan, info, md, cfg
+
+
+@pytest.mark.parametrize("name", ["prefill", "decode", "mixed", "verify"])
+def test_dispatch_keeps_kv_heads_on_their_xcds(name):
+    """Workgroup b runs on XCD b % 8; a kv-head's work goes to the XCDs
+    g (mod Hkv) only, segment after segment of the dispatch list."""
+    plan, info, md, cfg = _workload_plan(name, 0.25)
+    hkv = cfg.num_kv_heads
+    disp = plan[24:24 + info.grid]
+    heads = disp >> HEAD_SHIFT
+    xcd = np.arange(info.grid) % 8
+    assert np.array_equal(xcd % hkv, heads % 8 if hkv >= 8 else heads)
+    check_plan(plan, info, md["seq_lens"], md["cu_seqlens_q"], cfg.group, hkv)
+
+
 def test_plan_finds_shared_prefix_of_workloads():
     """The decode and verify workloads share their whole cached prefix."""
     for name, prefix in (("decode", 2048), ("verify", 16384)):
