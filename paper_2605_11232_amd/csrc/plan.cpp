@@ -26,8 +26,12 @@
 // Dispatch order: workgroup ids are handed to the eight XCDs round robin, and
 // each XCD has its own L2.  Items are queued per XCD by kv-head so that all
 // work of one kv-head -- and so the shared prefix blocks of that head, which
-// every sequence reads -- stays in one XCD's L2.  Within a queue, items are
-// ordered longest first (coarse counting sort) to shorten the tail.
+// every sequence reads -- stays in one XCD's L2.  Within a queue, shared and
+// row items are ordered longest first (coarse counting sort) to shorten the
+// tail, tile items grouped by sequence (each sequence's keys are re-read from
+// L2 by its tiles running together).  The dispatch list is the queues
+// interleaved segment by segment: shared items (at most one per CU), tile
+// items, the remaining shared items, row quads.
 #include <algorithm>
 #include <array>
 #include <climits>
@@ -372,8 +376,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         }
       }
     }
-    // Shared and tile items: per head, longest first, dealt round robin to the
-    // head's XCD queues (which stay longest first).
+    // Shared and tile items: per head, in the order above, dealt round robin
+    // to the head's XCD queues.
     std::vector<std::vector<int>> xs_of(num_kv_heads);
     for (int32_t g = 0; g < num_kv_heads; ++g) xs_of[g] = xcds_of_head(g, num_kv_heads);
     // With by_seq (tile items grouped by sequence), a head spread over
