@@ -47,7 +47,8 @@ namespace {
 constexpr int kXcds = 8;
 constexpr int64_t kRowWavesPerCu = 16;      // row-item split target
 constexpr int64_t kPrivateTileKeys = 4160;  // most private keys a few-row tile item covers
-constexpr int64_t kMinRowKeys = 256;        // fewest keys of a split row item
+constexpr int64_t kMinRowKeys = 256;        // split target floor of row items
+constexpr int64_t kTailWorkPct = 10;        // row work given half-length items (per cent)
 
 using Rec = std::array<int32_t, pa::kItemWords>;
 
@@ -264,7 +265,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
 
     // Key-range split of row items (private keys only for cascade members):
     // aim for enough single-wave items to keep kRowWavesPerCu wavefronts per
-    // CU busy, never below 256 keys and never above 1024 keys per item.
+    // CU busy, a split target of at least kMinRowKeys and at most 1024 keys
+    // per item (halved for the tail below).
     int64_t row_keys = 0;
     for (int32_t r = 0; r < n_seqs; ++r)
       if (is_row(r) && !on_tiles(r))
@@ -274,6 +276,24 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     chunk = cdiv(chunk, pa::kKeyStep) * pa::kKeyStep;
     // a row item's block ids fit one wavefront (64 lanes): at most 1024 keys
     chunk = std::min<int64_t>(chunk, int64_t(pa::kRowItemBlocks) * block_size);
+    // The sequences with the fewest private keys, up to kTailWork of the row
+    // work, get half-length items: ordered longest first, those run last, so
+    // the launch drains sooner.  A sequence keeps at most cdiv(L, kMinRowKeys)
+    // private parts (the workspace bound).
+    std::vector<int64_t> row_chunk(n_seqs, chunk);
+    if (row_keys > 0) {
+      std::vector<std::pair<int64_t, int32_t>> by_len;
+      for (int32_t r = 0; r < n_seqs; ++r)
+        if (is_row(r) && !on_tiles(r)) by_len.push_back({int64_t(seq_lens[r] - kstart[r]), r});
+      std::sort(by_len.begin(), by_len.end());
+      const int64_t half = std::max<int64_t>(pa::kKeyStep, chunk / 2 / pa::kKeyStep * pa::kKeyStep);
+      int64_t acc = 0;
+      for (const auto& [len, r] : by_len) {
+        acc += len * num_kv_heads;
+        if (acc > row_keys * kTailWorkPct / 100) break;
+        if (cdiv(len, half) <= cdiv(seq_lens[r], kMinRowKeys)) row_chunk[r] = half;
+      }
+    }
 
     std::vector<int64_t> tile_cost, row_cost, shared_cost;
     // head-0 partial base of a cascade member's merge group
@@ -287,7 +307,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         if (is_row(r) && on_tiles(r))
           nt += cdiv(seq_lens[r] - kstart[r], kPrivateTileKeys);
         else if (is_row(r))
-          nr += std::max<int64_t>(1, cdiv(seq_lens[r] - kstart[r], chunk));
+          nr += std::max<int64_t>(1, cdiv(seq_lens[r] - kstart[r], row_chunk[r]));
         else
           nt += cdiv(int64_t(qlen(r)) * G, pa::kTileRows);
       }
@@ -305,7 +325,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       if (is_row(r)) {
         const int32_t k0s = kstart[r];
         const bool tiled = on_tiles(r);
-        const int64_t split = tiled ? kPrivateTileKeys : chunk;
+        const int64_t split = tiled ? kPrivateTileKeys : row_chunk[r];
         const int64_t kstep = tiled ? pa::kTileStep : pa::kKeyStep;
         const int32_t nsplit = static_cast<int32_t>(std::max<int64_t>(1, cdiv(L - k0s, split)));
         // equal private key ranges, multiples of the key step, covering [k0s, L)
