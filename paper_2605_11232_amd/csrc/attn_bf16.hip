@@ -91,6 +91,9 @@ struct TileSmem {
 
 __device__ __forceinline__ int vswz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
 
+// Cache-policy bits of a buffer load on gfx950: non-temporal.
+constexpr int kCachePolicyNonTemporal = 2;
+
 // s_waitcnt vmcnt(0): every global load of this wavefront, including the
 // copies into LDS, has completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
@@ -100,10 +103,14 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70)
 // scalar registers, so the per-copy address work is scalar) and writes them
 // to bytes [16 l, 16 l + 16) after `lds` (wave-uniform).  Offsets at or past
 // `bytes` read zeros instead of faulting.
+// STREAM: the non-temporal cache policy (data read once: the lines are not
+// kept in L2 at the expense of data other items re-read).
+template <bool STREAM = false>
 __device__ __forceinline__ void copy16_to_lds(const void* base, int bytes, uint32_t off, __bf16* lds) {
   const __amdgpu_buffer_rsrc_t r =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0,
+                                           STREAM ? kCachePolicyNonTemporal : 0);
 }
 
 // Sum of the eight bf16 values of a vector added to acc (v_dot2 with ones).
@@ -157,7 +164,7 @@ __device__ __forceinline__ float max_halves(float x) {
 // matrix cores, and the PV MFMAs of step t overlap the row maxima of step
 // t + 1.  K of step t + 2 and V^T of step t + 1 are copied into the LDS
 // buffers freed by steps t and t - 1 during step t.
-template <int D, int NSUB, bool SHARED, bool FULL>
+template <int D, int NSUB, bool SHARED, bool FULL, bool STREAM = false>
 __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, const AttnArgs& a,
                                           TileSmem<D, NSUB>& sm) {
   constexpr int KT = 32 * NSUB;     // keys per step
@@ -265,17 +272,20 @@ __device__ __forceinline__ void tile_item(const int32_t* it, int g, int poff, co
   };
   // one (block, kv-head) of K or V^T: kBlock * D bf16 at the block's address
   constexpr int kHeadBytes = kBlock * D * 2;
+  // STREAM items (keys no other item reads) copy with the non-temporal
+  // policy, leaving L2 to the keys other items re-read (shared prefixes,
+  // the other tiles of a long sequence).
   auto issue_k = [&](const int64_t (&blk)[NB], int buf) {
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      copy16_to_lds(kbase + copy_block(blk, i), kHeadBytes, koff[i],
-                    &sm.k[buf][512 * (4 * i + w)]);
+      copy16_to_lds<STREAM>(kbase + copy_block(blk, i), kHeadBytes, koff[i],
+                            &sm.k[buf][512 * (4 * i + w)]);
   };
   auto issue_v = [&](const int64_t (&blk)[NB], int buf) {
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      copy16_to_lds(vbase + copy_block(blk, i), kHeadBytes, voff[i],
-                    &sm.v[buf][512 * (4 * i + w)]);
+      copy16_to_lds<STREAM>(vbase + copy_block(blk, i), kHeadBytes, voff[i],
+                            &sm.v[buf][512 * (4 * i + w)]);
   };
 
   // LDS operand addresses: per lane, the byte offset of its K unit for each
@@ -739,8 +749,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_e
     }
     if (ti < n_tile) {
       const int32_t* it = plan + plan[H_TILE_OFF] + (ti - n_shared) * kItemWords;
-      // every wavefront has rows: the plain path; otherwise idle ones skip compute
+      // every wavefront has rows: the plain path; otherwise idle ones skip
+      // compute, and a few-row sequence's private keys are streamed
       if (it[I_NROWS] > kTileRows - 32) tile_item<D, kTileSub, false, true>(it, g, poff, a, sm);
+      else if (it[I_FLAGS] & kItemStream) tile_item<D, kTileSub, false, false, true>(it, g, poff, a, sm);
       else tile_item<D, kTileSub, false, false>(it, g, poff, a, sm);
       return;
     }

@@ -350,7 +350,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
           const int64_t k0 = k0s + sp * per, k1 = std::min<int64_t>(L, k0s + (sp + 1) * per);
           const int32_t part = base < 0 ? -1 : int32_t(base + int64_t(sp + first) * rows);
           if (tiled) {
-            t_tiles.push_back({r, 0, 0, rows, int32_t(k0), int32_t(k1), part, 0});
+            t_tiles.push_back({r, 0, 0, rows, int32_t(k0), int32_t(k1), part, pa::kItemStream});
             tile_cost.push_back((k1 - k0) * rows);
           } else {
             t_rows.push_back({r, 0, 0, rows, int32_t(k0), int32_t(k1), part, 0});

@@ -56,10 +56,14 @@ constexpr int32_t kDispatchIndexMask = (1 << kDispatchHeadShift) - 1;
 // Row rho is query rho / G, q-head kvh * G + rho % G.  part = -1: write the
 // final output; otherwise the item writes normalised partial outputs and
 // log-sum-exps at workspace rows part + (rho - row0).  seq = -1: empty slot.
+// flags: kItemStream = no other item reads the item's keys (a few-row
+// sequence's private key range), so its copies need not stay in L2.
 enum : int32_t {
-  I_SEQ = 0, I_KVH, I_ROW0, I_NROWS, I_KV0, I_KV1, I_PART, I_PAD,
+  I_SEQ = 0, I_KVH, I_ROW0, I_NROWS, I_KV0, I_KV1, I_PART, I_FLAGS,
   kItemWords = 8
 };
+
+constexpr int32_t kItemStream = 1;
 
 // Shared-prefix item: gathered rows [row0, row0 + nrows) of a cascade group's
 // members (member m owns gathered rows m * rpm .. m * rpm + rpm - 1, its own

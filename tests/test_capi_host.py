@@ -201,6 +201,7 @@ H_SHARED_OFF, H_TILE_OFF, H_ROW_OFF, H_GROUP_OFF, H_MEMBER_OFF, H_PARTIAL_ROWS =
 H_DISPATCH_OFF, H_HEAD_PARTIAL, H_HKV = 18, 19, 8
 H_N_SHARED_TMPL, H_N_TILE_TMPL, H_N_ROW_TMPL, H_N_GROUP_TMPL = 20, 21, 22, 23
 HEAD_SHIFT = 24           # dispatch word: (kv-head << 24) | template index
+STREAM_FLAG = 1           # item flags word: no other item reads the item's keys
 WAVES = 4                 # wavefronts per workgroup: row items come WAVES to a workgroup
 TILE_ROWS = 32 * WAVES    # rows of a tile or shared item (32 per wavefront)
 ROW_ITEM_ROWS = 32        # rows of a row item (two 16-column MFMA tiles)
@@ -397,11 +398,22 @@ def test_plan_finds_shared_prefix_of_workloads():
         plan, info = B.plan(kind, launch.q_lens[0], md["seq_lens"], md["cu_seqlens_q"],
                             cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 16, B.PA_BF16,
                             block_table=md["block_table"])
-        h, shared, *_ = parse_plan(plan)
+        h, shared, tiles, *_ = parse_plan(plan)
         assert info.n_shared_items > 0
         P = wl.notes["prefix"]
         assert max(s[5] for s in shared) == P // 64 * 64
+        # verify's 40-row private parts are tile items marked as streamed
+        # (no other item reads their keys)
+        assert (len(tiles) > 0) == (name == "verify")
+        assert all(t[7] == STREAM_FLAG for t in tiles)
         check_plan(plan, info, md["seq_lens"], md["cu_seqlens_q"], cfg.group, cfg.num_kv_heads)
+
+
+def test_prefill_tiles_are_not_streamed():
+    """Tiles of a long sequence share its keys: none carries the stream flag."""
+    plan, info, md, cfg = _workload_plan("prefill", 0.25)
+    _, _, tiles, _, _ = parse_plan(plan)
+    assert tiles and not any(t[7] & STREAM_FLAG for t in tiles)
 
 
 def test_device_calls_reject_bad_arguments_without_launching():
