@@ -4,9 +4,12 @@
 // Section 3, cached prefixes give the recomputed result): causal softmax over
 // keys 0..a of the request's logical sequence, read through its block table.
 // One wavefront per (query token, q-head); a 64-key chunk puts one key in each
-// lane for the scores, then the lanes switch to owning head dimensions for
-// the weighted value sum.  All arithmetic is float32 with fused multiply-adds;
-// exp/log are the device library's float32 functions.
+// lane for the scores (16-byte loads of the key's 32-dim runs, four partial
+// sums), then the lanes switch to owning head dimensions for the weighted
+// value sum: each lane reads one dimension's 16 offsets of a block as four
+// 16-byte loads and takes the probabilities from LDS, keys in order.  All
+// arithmetic is float32 with fused multiply-adds; exp/log are the device
+// library's float32 functions.
 #include "device_common.h"
 
 namespace pa {
@@ -19,7 +22,11 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
     const int32_t* __restrict__ bt, int32_t max_blocks, const int32_t* __restrict__ seq_lens,
     const int32_t* __restrict__ cu_q, int32_t n_seqs, int32_t hq, int32_t hkv, int32_t num_blocks,
     float scale, float* __restrict__ out, float* __restrict__ lse) {
+  constexpr int DL = D / 64;  // value dimensions per lane
+  static_assert(D % 64 == 0, "head_dim 64 or 128");
   __shared__ float qsh[D];
+  __shared__ float psh[64];
+  __shared__ int bsh[64 / kBlock];
   const int token = blockIdx.x / hq, h = blockIdx.x % hq;
   const int lane = threadIdx.x;
   // sequence r: the last r with cu_q[r] <= token (empty sequences are skipped)
@@ -37,26 +44,32 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
   for (int d = lane; d < D; d += 64) qsh[d] = q[((int64_t)token * hq + h) * D + d];
   __syncthreads();
 
-  float od[(D + 63) / 64];
+  float od[DL];
 #pragma unroll
-  for (int k = 0; k < (D + 63) / 64; ++k) od[k] = 0.f;
+  for (int k = 0; k < DL; ++k) od[k] = 0.f;
   float m = kNegInf, l = 0.f;
   for (int c0 = 0; c0 <= a; c0 += 64) {
     const int key = c0 + lane;
     const bool vis = key <= a;
+    // every lane's block id is a clamped table entry, so each address below
+    // is inside the cache
+    const int blk = clamp_block(row[min(key / kBlock, max_blocks - 1)], num_blocks);
     float s = kNegInf;
-    int blk = 0;
     if (vis) {
-      blk = clamp_block(row[min(key / kBlock, max_blocks - 1)], num_blocks);
-      // the key's 32-dim runs in the grouped key layout
+      // the key's 32-dim runs in the grouped key layout, 32 floats each
       const float* kp = kc + ((int64_t)blk * hkv + g) * kBlock * D + key_elem(key % kBlock, 0);
-      float dot = 0.f;
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int gd = 0; gd < D; gd += kKeyGroup)
-#pragma unroll 8
-        for (int d = 0; d < kKeyGroup; ++d)
-          dot = fmaf(qsh[gd + d], kp[gd * kBlock + d], dot);
-      s = dot * scale;
+      for (int gd = 0; gd < D; gd += kKeyGroup) {
+        const f32x4* k4 = reinterpret_cast<const f32x4*>(kp + gd * kBlock);
+#pragma unroll
+        for (int j = 0; j < kKeyGroup / 4; ++j) {
+          const f32x4 kv = k4[j];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[j % 4] = fmaf(qsh[gd + 4 * j + e], kv[e], acc[j % 4]);
+        }
+      }
+      s = ((acc[0] + acc[1]) + (acc[2] + acc[3])) * scale;
     }
     float cm = s;
 #pragma unroll
@@ -70,26 +83,37 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
     l = l * alpha + ps;
     m = mnew;
 #pragma unroll
-    for (int k = 0; k < (D + 63) / 64; ++k) od[k] *= alpha;
+    for (int k = 0; k < DL; ++k) od[k] *= alpha;
+    psh[lane] = p;
+    if (lane % kBlock == 0) bsh[lane / kBlock] = blk;
+    __syncthreads();
+    // keys c0 .. c0 + nk - 1 are visible; the chunk starts on a block boundary
     const int nk = min(64, a + 1 - c0);
-    for (int kk = 0; kk < nk; ++kk) {
-      const float pk = __shfl(p, kk, 64);
-      const int bk = __shfl(blk, kk, 64);
-      const int off = (c0 + kk) % kBlock;
-      const float* vp = vc + ((int64_t)bk * hkv + g) * D * kBlock + off;
+    for (int b = 0; b * kBlock < nk; ++b) {
+      const float* vb = vc + ((int64_t)bsh[b] * hkv + g) * D * kBlock;
+      const int kb = b * kBlock, nb = min(kBlock, nk - kb);
 #pragma unroll
-      for (int k = 0; k < (D + 63) / 64; ++k) {
-        const int d = lane + 64 * k;
-        if (d < D) od[k] = fmaf(pk, vp[d * kBlock], od[k]);
+      for (int k = 0; k < DL; ++k) {
+        const f32x4* v4 = reinterpret_cast<const f32x4*>(vb + (lane + 64 * k) * kBlock);
+        f32x4 vv[kBlock / 4];
+#pragma unroll
+        for (int j = 0; j < kBlock / 4; ++j) vv[j] = v4[j];
+        if (nb == kBlock) {
+#pragma unroll
+          for (int j = 0; j < kBlock; ++j) od[k] = fmaf(psh[kb + j], vv[j / 4][j % 4], od[k]);
+        } else {
+          // keys past the last visible one: slots that may never have been written
+#pragma unroll
+          for (int j = 0; j < kBlock; ++j)
+            if (j < nb) od[k] = fmaf(psh[kb + j], vv[j / 4][j % 4], od[k]);
+        }
       }
     }
+    __syncthreads();  // psh and bsh are rewritten by the next chunk
   }
   const float inv = 1.f / l;
 #pragma unroll
-  for (int k = 0; k < (D + 63) / 64; ++k) {
-    const int d = lane + 64 * k;
-    if (d < D) out[((int64_t)token * hq + h) * D + d] = od[k] * inv;
-  }
+  for (int k = 0; k < DL; ++k) out[((int64_t)token * hq + h) * D + lane + 64 * k] = od[k] * inv;
   if (lse && lane == 0) lse[(int64_t)token * hq + h] = m + logf(l);
 }
 
