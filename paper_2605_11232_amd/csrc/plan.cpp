@@ -31,7 +31,8 @@
 // tail, tile items grouped by sequence (each sequence's keys are re-read from
 // L2 by its tiles running together).  The dispatch list is the queues
 // interleaved segment by segment: shared items (at most one per CU), tile
-// items, the remaining shared items, row quads.
+// items with the row quads spread evenly among them, the remaining shared
+// items.
 #include <algorithm>
 #include <array>
 #include <climits>
@@ -468,10 +469,10 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     for (const auto& x : tile_q) n_tile_wg += int64_t(x.size());
     n_quads = int64_t(nq) * num_kv_heads;
     // Dispatch order: shared-prefix items first, one per CU at most, then the
-    // tile items, then the remaining shared items, then the row quads.  With
-    // more shared items than CUs, every CU then starts one shared item beside
-    // one tile item, and the rest of the shared work takes the slots the
-    // (memory-bound, shorter) tile items free.
+    // tile items with the row quads among them, then the remaining shared
+    // items.  With more shared items than CUs, every CU then starts one shared
+    // item beside one tile item, and the rest of the shared work takes the
+    // slots the (memory-bound, shorter) tile items free.
     {
       const size_t per_xcd = size_t(cdiv(num_cus > 0 ? num_cus : 256, kXcds));
       std::vector<std::vector<Ref>> first(kXcds), rest(kXcds);
@@ -481,11 +482,25 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         first[x].assign(v.begin(), v.begin() + k);
         rest[x].assign(v.begin() + k, v.end());
       }
+      // Row quads (memory-bound) are spread evenly through each XCD's tile
+      // items (matrix-bound) instead of following them, so a mixed launch
+      // streams its decode rows while the tiles keep the matrix cores busy.
+      std::vector<std::vector<Ref>> body(kXcds);
+      for (int x = 0; x < kXcds; ++x) {
+        const auto& t = tile_q[x];
+        const auto& rq = quad_q[x];
+        const size_t nt = t.size(), nr = rq.size();
+        body[x].reserve(nt + nr);
+        for (size_t it = 0, ir = 0; it < nt || ir < nr;) {
+          // a quad goes next while the quads are not ahead of the tiles
+          if (ir < nr && (it >= nt || ir * nt <= it * nr)) body[x].push_back(rq[ir++]);
+          else body[x].push_back(t[it++]);
+        }
+      }
       dispatch.reserve(size_t(n_shared_wg + n_tile_wg + n_quads));
       interleave(dispatch, first);
-      interleave(dispatch, tile_q);
+      interleave(dispatch, body);
       interleave(dispatch, rest);
-      interleave(dispatch, quad_q);
     }
   }
 
