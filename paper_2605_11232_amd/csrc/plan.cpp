@@ -30,9 +30,8 @@
 // row items are ordered longest first (coarse counting sort) to shorten the
 // tail, tile items grouped by sequence (each sequence's keys are re-read from
 // L2 by its tiles running together).  The dispatch list is the queues
-// interleaved segment by segment: shared items (at most one per CU), tile
-// items with the row quads spread evenly among them, the remaining shared
-// items.
+// interleaved segment by segment: shared items, then tile items with the row
+// quads spread evenly among them.
 #include <algorithm>
 #include <array>
 #include <climits>
@@ -468,20 +467,10 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
     for (const auto& x : shared_q) n_shared_wg += int64_t(x.size());
     for (const auto& x : tile_q) n_tile_wg += int64_t(x.size());
     n_quads = int64_t(nq) * num_kv_heads;
-    // Dispatch order: shared-prefix items first, one per CU at most, then the
-    // tile items with the row quads among them, then the remaining shared
-    // items.  With more shared items than CUs, every CU then starts one shared
-    // item beside one tile item, and the rest of the shared work takes the
-    // slots the (memory-bound, shorter) tile items free.
+    // Dispatch order: shared-prefix items first (the longest items, each a
+    // cascade chunk over all its group's rows), then the tile items with the
+    // row quads among them.
     {
-      const size_t per_xcd = size_t(cdiv(num_cus > 0 ? num_cus : 256, kXcds));
-      std::vector<std::vector<Ref>> first(kXcds), rest(kXcds);
-      for (int x = 0; x < kXcds; ++x) {
-        const auto& v = shared_q[x];
-        const size_t k = std::min(v.size(), per_xcd);
-        first[x].assign(v.begin(), v.begin() + k);
-        rest[x].assign(v.begin() + k, v.end());
-      }
       // Row quads (memory-bound) are spread evenly through each XCD's tile
       // items (matrix-bound) instead of following them, so a mixed launch
       // streams its decode rows while the tiles keep the matrix cores busy.
@@ -498,9 +487,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
         }
       }
       dispatch.reserve(size_t(n_shared_wg + n_tile_wg + n_quads));
-      interleave(dispatch, first);
+      interleave(dispatch, shared_q);
       interleave(dispatch, body);
-      interleave(dispatch, rest);
     }
   }
 
