@@ -133,9 +133,10 @@ def cpu_baseline(wl, launch, budget_s: float = 12.0):
     return dt, done, flops, threads, sub
 
 
-def run_workload(name, W, K, C, cpu_budget, profile=False):
-    """Warm up W steps, time K steps (HIP events around every attention
-    call), then C cold-cache steps; returns the figures of one workload."""
+def run_workload(name, W, K, C, cpu_budget, profile=False, settle_ms=0.0):
+    """Settle the device clock (untimed steps for settle_ms of device load),
+    warm up W steps, time K steps (HIP events around every attention call),
+    then C cold-cache steps; returns the figures of one workload."""
     import torch
     from paper_2605_11232_amd import binding as B, perf, synth
     from paper_2605_11232_amd.runtime import DeviceReplay, Staging, plan_words_bound, marshal_launch
@@ -198,6 +199,32 @@ def run_workload(name, W, K, C, cpu_budget, profile=False):
     gc.collect()
     gc.freeze()
     gc.disable()
+    # The device has idled through the host-side setup (and, for the later
+    # configurations of a full run, through the previous one's oracle timing).
+    # Under load after idle its power management runs a transient (a fast
+    # call, then 10-20 calls 5-30 % slower) before the clock settles, so a
+    # short warm-up would leave the timed steps inside it.  One step, then its
+    # attention call again and again (same inputs, output overwritten; paced
+    # by events so at most 2 * SETTLE_BATCH calls are queued and the host
+    # mostly waits) keep the device loaded for settle_ms first (at least
+    # SETTLE_MIN_CALLS calls); the W warm-up and K timed steps follow without
+    # a pause, whatever W is.
+    n_settle = 0
+    settle_s = 0.0
+    if settle_ms > 0:
+        p0 = step(0)
+        t_s = time.perf_counter()
+        pace = []
+        while n_settle < SETTLE_MIN_CALLS or settle_s * 1e3 < settle_ms:
+            for _ in range(SETTLE_BATCH):
+                dev.attend(p0)
+            n_settle += SETTLE_BATCH
+            ev = B.StreamEvent()
+            ev.record(stream)
+            pace.append(ev)
+            if len(pace) > 2:
+                pace.pop(0).synchronize()
+            settle_s = time.perf_counter() - t_s
     for s in range(W):
         p = step(s)
     torch.cuda.synchronize()
@@ -253,6 +280,7 @@ def run_workload(name, W, K, C, cpu_budget, profile=False):
         "peak": peak, "achieved": achieved, "attn_ms": attn_ms, "per_ms": per_ms, "runs": runs,
         "run_achieved": [work / (r * 1e-3) / scale_u for r in runs], "kv_memory": kv_memory,
         "W": W, "K": K,
+        "settle": {"attention_calls": n_settle, "ms": round(settle_s * 1e3, 1)},
     }
     if cold_ms is not None:
         cold_ach = work / (cold_ms * 1e-3) / scale_u
@@ -354,6 +382,8 @@ def call_summary(res):
 
 # The other configurations, measured in the same run after the headline.
 SECONDARY = ["decode", "verify", "mixed", "tiny"]
+SETTLE_MIN_CALLS = 24
+SETTLE_BATCH = 8
 
 
 def main():
@@ -374,6 +404,11 @@ def main():
                     help="seconds of float64 oracle per secondary configuration")
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="run only this many steps without the CPU baseline (profiling)")
+    ap.add_argument("--settle-ms", type=float, default=200.0,
+                    help="before the warm-up, one step and then its attention call repeated "
+                         "until the device has been under load this long (at least 24 calls), "
+                         "so the timed steps start in the clock's steady state after the idle "
+                         "setup; 0 skips it")
     ap.add_argument("--cold-steps", type=int, default=5,
                     help="extra steps, after the timed ones, whose attention call runs after a "
                          "1 GiB device read has flushed the caches (0 skips them)")
@@ -420,7 +455,8 @@ def main():
         W, K = 1, args.profile_steps
     profile = bool(args.profile_steps)
     budget = 0.0 if args.no_cpu_baseline else 10.0
-    res = run_workload(name, W, K, C, budget, profile)
+    settle = 0.0 if profile else max(0.0, args.settle_ms)
+    res = run_workload(name, W, K, C, budget, profile, settle)
     cfg = res["cfg"]
     rec = {
         "metric": METRIC,
@@ -429,6 +465,7 @@ def main():
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
+        "settle": res["settle"],
         "ms_per_step": round(res["ms"], 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -455,11 +492,13 @@ def main():
         for other in SECONDARY:
             print(f"[bench] {other}", file=sys.stderr, flush=True)
             r2 = run_workload(other, args.secondary_warmup, args.secondary_steps, 0,
-                              0.0 if args.no_cpu_baseline else args.secondary_cpu_budget)
+                              0.0 if args.no_cpu_baseline else args.secondary_cpu_budget,
+                              settle_ms=settle)
             w = {"workload": DESCRIPTIONS[other], "dtype": r2["cfg"].dtype,
                  "requests": r2["requests"], "query_tokens": r2["query_tokens"],
                  "attn_flops": r2["flops"], "attn_unique_bytes": r2["attn_bytes"],
-                 "steps": r2["K"], "warmup": r2["W"], "ms_per_step": round(r2["ms"], 4),
+                 "steps": r2["K"], "warmup": r2["W"], "settle": r2["settle"],
+                 "ms_per_step": round(r2["ms"], 4),
                  "step_value": round(r2["value"], 3), "step_unit": r2["unit"],
                  "roofline": call_summary(r2)}
             if "cpu_baseline" in r2:
