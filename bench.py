@@ -166,9 +166,10 @@ def run_workload(name, W, K, C, cpu_budget, profile=False, settle_ms=0.0):
     scrub_sink = []
 
     def step(s, record=None):
-        # a timed warm-cache step records the attention call's start event
-        # after the KV append, where it also releases the staging buffer: one
-        # event marker fewer per step than a separate release event
+        # A timed step's attention call carries its start and stop events on
+        # its first and last kernel dispatches (no event packets between the
+        # kernels); in a warm-cache step the start event also releases the
+        # staging buffer, so the step records no event of its own.
         share = record is not None and state["scrub"] is None
         p = dev.prepare_staged(launches[s], stagings[s % 2], q, k_new, v_new, out, lse,
                                guard=record[0] if share else None)
@@ -176,16 +177,12 @@ def run_workload(name, W, K, C, cpu_budget, profile=False, settle_ms=0.0):
             # KV memory of the live batch: blocks versus contiguous reservations
             # of the block-table capacity (outside the timed steps)
             kv_memory.update(dev.pool.kv_waste(wl.max_blocks_per_seq * cfg.block_size))
-        dev.append(p)
+        dev.append(p, record_guard=False)
         if state["scrub"] is not None:
             # read 1 GiB: L2 and MALL then hold none of the inputs (a read leaves
             # no dirty lines whose write-back would compete with the call)
             scrub_sink.append(state["scrub"].sum())
-        if record is not None and not share:
-            record[0].record(stream)
-        dev.attend(p)
-        if record is not None:
-            record[1].record(stream)
+        dev.attend(p, events=record)
         dev.finish(launches[s], batched=True)
         return p
 

@@ -460,6 +460,20 @@ int pa_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cac
                            int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
                            const pa_plan_info* info, void* out, float* lse, void* stream);
 
+/* Timing hook, for callers that time attention calls on the device
+ * (benchmarks, profilers) without event packets between kernels: the next
+ * pa_attn_* call on this thread attaches start_event to the dispatch of its
+ * first kernel (recorded when that kernel starts) and stop_event to the
+ * dispatch of its last (recorded when it ends), through hipExtLaunchKernel,
+ * instead of separate event records, each of which idles the device for a
+ * few microseconds between back-to-back kernels.  Either may be NULL.  The
+ * events are hipEvent_t handles the caller created (with timing, for
+ * hipEventElapsedTime), passed as void*, and stay the caller's.  That call
+ * consumes the setting, also when it fails; later calls attach nothing
+ * until it is set again.  A call that launches no kernel records both
+ * events on its stream.  Errors: none. */
+int pa_set_launch_events(void* start_event, void* stop_event);
+
 #ifdef __cplusplus
 }
 #endif

@@ -30,7 +30,7 @@ EXPORTS = ["pa_last_error", "pa_abi_version", "pa_pool_create", "pa_pool_destroy
            "pa_attn_prefill", "pa_attn_decode", "pa_attn_verify", "pa_pool_set_eviction",
            "pa_pool_get_stats", "pa_pool_kv_waste", "pa_form_batches", "pa_prepare_launch",
            "pa_stage_upload", "pa_attn_workspace_size", "pa_attn_decode_workspace_size",
-           "pa_attn_decode_noalloc"]
+           "pa_attn_decode_noalloc", "pa_set_launch_events"]
 
 
 class PaError(RuntimeError):
@@ -117,6 +117,7 @@ def lib():
         sig[name] = attn
     # decode without the workspace pair
     sig["pa_attn_decode_noalloc"] = (C.c_int, attn[1][:18] + attn[1][20:])
+    sig["pa_set_launch_events"] = (C.c_int, [_P, _P])
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
         fn.restype = res
@@ -552,6 +553,14 @@ def attention(kind: int, q, k_cache, v_cache, block_table, seq_lens, cu_seqlens_
               int(block_table.shape[1]), _dptr(seq_lens), _dptr(cu_seqlens_q), n_seqs, total_q,
               hq, hkv, d, bs, float(scale), _dtype_code(q), _dptr(plan_dev), C.byref(info),
               _dptr(workspace), ws_bytes, _dptr(out), _dptr(lse), _stream(stream)))
+
+
+def set_launch_events(start: "StreamEvent | None", stop: "StreamEvent | None"):
+    """The next attention call on this thread records start when its first
+    kernel starts and stop when its last kernel ends (events carried by the
+    kernel dispatches, no event packets between kernels)."""
+    _check(lib().pa_set_launch_events(start._ev if start is not None else None,
+                                      stop._ev if stop is not None else None))
 
 
 def attention_decode_noalloc(q, k_cache, v_cache, block_table, seq_lens, cu_seqlens_q, plan_dev,

@@ -14,11 +14,12 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
                      const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
                      const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
                      bool wide_rows, int64_t partial_rows, void* ws, void* out, float* lse,
-                     hipStream_t stream);
+                     hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop);
 int launch_attn_f32(const void* q, const void* kc, const void* vc, int32_t num_blocks,
                     const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
                     const int32_t* cu_q, int32_t n_seqs, int32_t total_q, int32_t hq, int32_t hkv,
-                    int32_t d, float scale, void* out, float* lse, hipStream_t stream);
+                    int32_t d, float scale, void* out, float* lse, hipStream_t stream,
+                    hipEvent_t ev_start, hipEvent_t ev_stop);
 int launch_kv_append(const void* kn, const void* vn, const int32_t* slots, int32_t n, void* kc,
                      void* vc, int32_t nb, int32_t hkv, int32_t d, int32_t dtype,
                      hipStream_t stream);
@@ -26,6 +27,10 @@ int launch_stage_upload(const void* src, void* dst, int64_t n_dwords, hipStream_
 }  // namespace dev
 
 namespace {
+
+// Timing events for the next attention call on this thread
+// (pa_set_launch_events); each call takes them and clears them.
+thread_local hipEvent_t t_ev_start = nullptr, t_ev_stop = nullptr;
 
 int check_shape(const char* fn, int32_t num_blocks, int32_t num_kv_heads, int32_t head_dim,
                 int32_t block_size, int32_t dtype) {
@@ -82,6 +87,8 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
                 size_t workspace_bytes, void* out, float* lse, void* stream,
                 bool noalloc = false) {
   clear_error();
+  const hipEvent_t ev_start = t_ev_start, ev_stop = t_ev_stop;
+  t_ev_start = t_ev_stop = nullptr;
   int rc = check_shape(fn, num_blocks, num_kv_heads, head_dim, block_size, dtype);
   if (rc) return rc;
   if (num_q_heads <= 0 || num_q_heads % num_kv_heads)
@@ -105,14 +112,22 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
                 "dtype %d", fn, info->n_seqs, info->total_q, info->num_q_heads,
                 info->num_kv_heads, info->head_dim, info->dtype, n_seqs, total_q, num_q_heads,
                 num_kv_heads, head_dim, dtype);
-  if (total_q == 0 || n_seqs == 0) return PA_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (total_q == 0 || n_seqs == 0) {
+    // nothing to launch: the events still mark this point of the stream
+    for (hipEvent_t ev : {ev_start, ev_stop}) {
+      const hipError_t e = ev ? hipEventRecord(ev, st) : hipSuccess;
+      if (e != hipSuccess)
+        return fail(PA_ERR_LAUNCH, "%s: hipEventRecord: %s", fn, hipGetErrorString(e));
+    }
+    return PA_OK;
+  }
   if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !cu_seqlens_q || !out)
     return fail(PA_ERR_ARG, "%s: NULL device pointer", fn);
-  hipStream_t st = static_cast<hipStream_t>(stream);
   if (dtype == PA_F32) {
     rc = dev::launch_attn_f32(q, k_cache, v_cache, num_blocks, block_table, max_blocks_per_seq,
                               seq_lens, cu_seqlens_q, n_seqs, total_q, num_q_heads, num_kv_heads,
-                              head_dim, scale, out, lse, st);
+                              head_dim, scale, out, lse, st, ev_start, ev_stop);
   } else {
     if (!plan) return fail(PA_ERR_ARG, "%s: NULL plan", fn);
     if ((info->variant & ~kVariantWideRows) != kVariantBf16 || info->grid < 0 || info->n_groups < 0 ||
@@ -146,7 +161,7 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
                                plan, info->grid, info->n_shared_items + info->n_tile_items,
                                info->n_groups, (info->variant & kVariantWideRows) != 0,
                                partial_rows,
-                               workspace, out, lse, st);
+                               workspace, out, lse, st, ev_start, ev_stop);
   }
   if (rc) return fail(PA_ERR_LAUNCH, "%s: %s", fn, hipGetErrorString(static_cast<hipError_t>(rc)));
   return PA_OK;
@@ -250,6 +265,13 @@ int pa_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cac
                          num_blocks, block_table, max_blocks_per_seq, seq_lens, cu_seqlens_q,
                          n_seqs, total_q, num_q_heads, num_kv_heads, head_dim, block_size, scale,
                          dtype, plan, info, nullptr, 0, out, lse, stream, /*noalloc=*/true);
+}
+
+int pa_set_launch_events(void* start_event, void* stop_event) {
+  pa::clear_error();
+  pa::t_ev_start = static_cast<hipEvent_t>(start_event);
+  pa::t_ev_stop = static_cast<hipEvent_t>(stop_event);
+  return PA_OK;
 }
 
 }  // extern "C"

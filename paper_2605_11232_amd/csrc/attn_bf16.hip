@@ -27,6 +27,8 @@
 //
 // Scores are scaled by scale * log2(e) and exponentiated with exp2; the
 // natural-log LSE is recovered as ln2 * (m + log2 l).
+#include <hip/hip_ext.h>
+
 #include "device_common.h"
 #include "plan_format.h"
 
@@ -859,7 +861,7 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
                      const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
                      const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
                      bool wide_rows, int64_t partial_rows, void* ws, void* out, float* lse,
-                     hipStream_t stream) {
+                     hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
   AttnArgs a;
   a.q = static_cast<const __bf16*>(q);
   a.kc = static_cast<const __bf16*>(kc);
@@ -883,8 +885,12 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
     // wide row path too
     const bool rows = grid > n_tile;
     const int mix = n_tile == 0 ? (wide_rows ? 6 : 2) : (rows ? 7 : 1);
-#define PA_LAUNCH(DD, MM) \
-  hipLaunchKernelGGL((attn_bf16_kernel<DD, MM>), dim3(grid), dim3(256), 0, stream, a)
+    // the caller's timing events ride on the dispatches (start on the first
+    // kernel, stop on the last): no event packets between the kernels
+    hipEvent_t stop_here = n_groups > 0 ? nullptr : ev_stop;
+#define PA_LAUNCH(DD, MM)                                                                     \
+  hipExtLaunchKernelGGL((attn_bf16_kernel<DD, MM>), dim3(grid), dim3(256), 0, stream, ev_start, \
+                        stop_here, 0, a)
 #define PA_LAUNCH_D(DD)                      \
   switch (mix) {                             \
     case 1: PA_LAUNCH(DD, 1); break;         \
@@ -903,12 +909,22 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
     if (e != hipSuccess) return static_cast<int>(e);
   }
   if (n_groups > 0) {
+    hipEvent_t start_here = grid > 0 ? nullptr : ev_start;
     if (d == 128)
-      hipLaunchKernelGGL(merge_kernel<128>, dim3(n_groups), dim3(kMergeRows * 32), 0, stream, a);
+      hipExtLaunchKernelGGL(merge_kernel<128>, dim3(n_groups), dim3(kMergeRows * 32), 0, stream,
+                            start_here, ev_stop, 0, a);
     else
-      hipLaunchKernelGGL(merge_kernel<64>, dim3(n_groups), dim3(kMergeRows * 32), 0, stream, a);
+      hipExtLaunchKernelGGL(merge_kernel<64>, dim3(n_groups), dim3(kMergeRows * 32), 0, stream,
+                            start_here, ev_stop, 0, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return static_cast<int>(e);
+  }
+  if (grid <= 0 && n_groups <= 0) {
+    // nothing launched: the events still mark this point of the stream
+    for (hipEvent_t ev : {ev_start, ev_stop}) {
+      const hipError_t e = ev ? hipEventRecord(ev, stream) : hipSuccess;
+      if (e != hipSuccess) return static_cast<int>(e);
+    }
   }
   return 0;
 }

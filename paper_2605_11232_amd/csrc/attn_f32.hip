@@ -10,6 +10,8 @@
 // 16-byte loads and takes the probabilities from LDS, keys in order.  All
 // arithmetic is float32 with fused multiply-adds; exp/log are the device
 // library's float32 functions.
+#include <hip/hip_ext.h>
+
 #include "device_common.h"
 
 namespace pa {
@@ -122,19 +124,28 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
 int launch_attn_f32(const void* q, const void* kc, const void* vc, int32_t num_blocks,
                     const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
                     const int32_t* cu_q, int32_t n_seqs, int32_t total_q, int32_t hq, int32_t hkv,
-                    int32_t d, float scale, void* out, float* lse, hipStream_t stream) {
+                    int32_t d, float scale, void* out, float* lse, hipStream_t stream,
+                    hipEvent_t ev_start, hipEvent_t ev_stop) {
   const int64_t grid = int64_t(total_q) * hq;
-  if (grid == 0) return 0;
+  if (grid == 0) {
+    // nothing launched: the events still mark this point of the stream
+    for (hipEvent_t ev : {ev_start, ev_stop}) {
+      const hipError_t e = ev ? hipEventRecord(ev, stream) : hipSuccess;
+      if (e != hipSuccess) return static_cast<int>(e);
+    }
+    return 0;
+  }
+  // the caller's timing events ride on the dispatch (no event packets)
   if (d == 128)
-    hipLaunchKernelGGL(attn_f32_kernel<128>, dim3(grid), dim3(64), 0, stream,
-                       static_cast<const float*>(q), static_cast<const float*>(kc),
-                       static_cast<const float*>(vc), bt, max_blocks, seq_lens, cu_q, n_seqs, hq,
-                       hkv, num_blocks, scale, static_cast<float*>(out), lse);
+    hipExtLaunchKernelGGL(attn_f32_kernel<128>, dim3(grid), dim3(64), 0, stream, ev_start, ev_stop,
+                          0, static_cast<const float*>(q), static_cast<const float*>(kc),
+                          static_cast<const float*>(vc), bt, max_blocks, seq_lens, cu_q, n_seqs,
+                          hq, hkv, num_blocks, scale, static_cast<float*>(out), lse);
   else
-    hipLaunchKernelGGL(attn_f32_kernel<64>, dim3(grid), dim3(64), 0, stream,
-                       static_cast<const float*>(q), static_cast<const float*>(kc),
-                       static_cast<const float*>(vc), bt, max_blocks, seq_lens, cu_q, n_seqs, hq,
-                       hkv, num_blocks, scale, static_cast<float*>(out), lse);
+    hipExtLaunchKernelGGL(attn_f32_kernel<64>, dim3(grid), dim3(64), 0, stream, ev_start, ev_stop,
+                          0, static_cast<const float*>(q), static_cast<const float*>(kc),
+                          static_cast<const float*>(vc), bt, max_blocks, seq_lens, cu_q, n_seqs,
+                          hq, hkv, num_blocks, scale, static_cast<float*>(out), lse);
   return static_cast<int>(hipGetLastError());
 }
 

@@ -270,13 +270,20 @@ class DeviceReplay:
             cu=cu, slots=slots, plan=st.plan[1], q=q, k_new=k_new, v_new=v_new, ws=ws, out=out,
             lse=lse, n_cached=self.n_cached, guard=guard)
 
-    def append(self, p: Prepared, stream=None):
+    def append(self, p: Prepared, stream=None, record_guard: bool = True):
+        """KV append of the launch; records the caller's staging guard after
+        it unless record_guard is False (the guard is then the start event the
+        caller hands to ``attend``)."""
         B.kv_append(p.k_new, p.v_new, p.slots, self.k_cache, self.v_cache, stream)
         guard = getattr(p, "guard", None)
-        if guard is not None:
+        if guard is not None and record_guard:
             guard.record(stream)
 
-    def attend(self, p: Prepared, stream=None):
+    def attend(self, p: Prepared, stream=None, events=None):
+        """The attention call; events = (start, stop) ride on its first and
+        last kernel dispatches (pa_set_launch_events)."""
+        if events is not None:
+            B.set_launch_events(*events)
         B.attention(KIND[p.kind], p.q, self.k_cache, self.v_cache, p.block_table, p.seq_lens, p.cu,
                     p.plan, p.info, p.ws, p.out, p.lse, stream=stream)
 

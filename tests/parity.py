@@ -105,16 +105,20 @@ def run_parity(wl, n_launches=None, rows=None, steps=None, check_cache=True, lab
             out = torch.empty((T, cfg.num_q_heads, cfg.head_dim), dtype=dev.tdtype,
                               device=dev.device)
             lse = torch.empty((T, cfg.num_q_heads), dtype=torch.float32, device=dev.device)
-            # odd launches release their staging buffer through a caller's
-            # event recorded after the KV append (the benchmark's timed steps)
-            guard = B.StreamEvent() if li % 2 else None
+            # odd launches release their staging buffer through the start
+            # event of the attention call, carried by its first kernel's
+            # dispatch, and time the call (the benchmark's timed steps)
+            timed = (B.StreamEvent(timing=True), B.StreamEvent(timing=True)) if li % 2 else None
             p = dev.prepare_staged(launch, stagings[li % 2], q, k_new, v_new, out, lse,
-                                   guard=guard)
-            dev.append(p)
-            dev.attend(p)
+                                   guard=timed[0] if timed else None)
+            dev.append(p, record_guard=False)
+            dev.attend(p, events=timed)
         else:
             p = dev.run(launch)
+            timed = None
         torch.cuda.synchronize()
+        if timed:
+            assert timed[0].elapsed_time(timed[1]) > 0.0
         for k in ("block_table", "seq_lens", "cu_seqlens_q", "slot_mapping"):
             np.testing.assert_array_equal(p.meta[k], ro["meta"][k], err_msg=k)
         assert p.n_cached == ro["n_cached"]
