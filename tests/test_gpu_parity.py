@@ -355,9 +355,12 @@ def test_extreme_score_scales(name, scale, factor):
 def test_edge_cases():
     """Empty launch, zero-query sequences mixed in, a one-token sequence,
     head_dim 64 in bf16, G = 1, verify with 16 to 128 rows per sequence (narrow
-    and wide row items, tile items)."""
+    and wide row items, tile items).  Each launch runs once more with timing
+    events on its kernels: the same output bit for bit, and the events
+    recorded also when nothing is launched."""
     _gpu()
     from oracle.run import OracleReplay
+    from paper_2605_11232_amd import binding as B
     from paper_2605_11232_amd.runtime import DeviceReplay
     from tests.parity import TOL, close
     cfg = synth.AttnConfig("edge", "bf16", 4, 4, 64, 16, 77)
@@ -397,6 +400,13 @@ def test_edge_cases():
         torch.cuda.synchronize()
         if sum(ql):
             close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"edge{ci}")
+        first = p.out.clone()
+        ev = (B.StreamEvent(timing=True), B.StreamEvent(timing=True))
+        dv.attend(p, events=ev)
+        ev[1].synchronize()
+        ms = ev[0].elapsed_time(ev[1])
+        assert (ms > 0.0) if sum(ql) else (ms >= 0.0), ms
+        assert torch.equal(p.out, first)
     # verify with n_q = 8: G = 2 gives 16 rows per sequence (one 16-row row
     # item per key range); G = 3 gives 24 rows (a row item of two 16-column
     # tiles); G = 8 gives 64 rows (tile items, two of the four wavefronts
