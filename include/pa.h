@@ -394,7 +394,11 @@ int pa_stage_upload(void* dst, const void* src, int64_t bytes, void* stream);
  * that is 0.  Block ids must lie in [0, num_blocks); out-of-range ids are
  * clamped so no access leaves the cache (results are then undefined).
  * Every pointer is caller-owned device memory (info: host); the call
- * allocates nothing, writes only out, lse and the workspace, and is
+ * allocates nothing, writes only out, lse, the workspace and two counter
+ * words of the plan's header, which its work-stealing workgroups count on
+ * (device-scope atomics) and which it leaves zero, as pa_attn_plan wrote
+ * them, so one device plan serves any number of calls ordered on a stream
+ * (calls sharing one device plan must not overlap in time), and is
  * asynchronous on stream.  The three entry points differ only in the plan
  * kind they accept.
  * Errors (checked before anything is launched): PA_ERR_ARG (NULL pointer with
@@ -406,7 +410,7 @@ int pa_attn_prefill(const void* q, const void* k_cache, const void* v_cache, int
                     const int32_t* block_table, int32_t max_blocks_per_seq,
                     const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,
                     int32_t total_q, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                    int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                    int32_t block_size, float scale, int32_t dtype, int32_t* plan,
                     const pa_plan_info* info, void* workspace, size_t workspace_bytes,
                     void* out, float* lse, void* stream);
 
@@ -418,7 +422,7 @@ int pa_attn_decode(const void* q, const void* k_cache, const void* v_cache, int3
                    const int32_t* block_table, int32_t max_blocks_per_seq,
                    const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,
                    int32_t total_q, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                   int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                   int32_t block_size, float scale, int32_t dtype, int32_t* plan,
                    const pa_plan_info* info, void* workspace, size_t workspace_bytes,
                    void* out, float* lse, void* stream);
 
@@ -432,7 +436,7 @@ int pa_attn_verify(const void* q, const void* k_cache, const void* v_cache, int3
                    const int32_t* block_table, int32_t max_blocks_per_seq,
                    const int32_t* seq_lens, const int32_t* cu_seqlens_q, int32_t n_seqs,
                    int32_t total_q, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                   int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                   int32_t block_size, float scale, int32_t dtype, int32_t* plan,
                    const pa_plan_info* info, void* workspace, size_t workspace_bytes,
                    void* out, float* lse, void* stream);
 
@@ -457,7 +461,7 @@ int pa_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cac
                            int32_t max_blocks_per_seq, const int32_t* seq_lens,
                            const int32_t* cu_seqlens_q, int32_t n_seqs, int32_t total_q,
                            int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                           int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                           int32_t block_size, float scale, int32_t dtype, int32_t* plan,
                            const pa_plan_info* info, void* out, float* lse, void* stream);
 
 /* Timing hook, for callers that time attention calls on the device

@@ -13,8 +13,8 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
                      const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
                      const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
                      const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
-                     bool wide_rows, int64_t partial_rows, void* ws, void* out, float* lse,
-                     hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop);
+                     bool wide_rows, bool tail, int64_t partial_rows, void* ws, void* out,
+                     float* lse, hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop);
 int launch_attn_f32(const void* q, const void* kc, const void* vc, int32_t num_blocks,
                     const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
                     const int32_t* cu_q, int32_t n_seqs, int32_t total_q, int32_t hq, int32_t hkv,
@@ -130,7 +130,8 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
                               head_dim, scale, out, lse, st, ev_start, ev_stop);
   } else {
     if (!plan) return fail(PA_ERR_ARG, "%s: NULL plan", fn);
-    if ((info->variant & ~kVariantWideRows) != kVariantBf16 || info->grid < 0 || info->n_groups < 0 ||
+    if ((info->variant & ~(kVariantWideRows | kVariantTail)) != kVariantBf16 || info->grid < 0 ||
+        info->n_groups < 0 ||
         info->n_tile_items < 0 || info->n_shared_items < 0 ||
         int64_t(info->n_tile_items) + info->n_shared_items > info->grid ||
         info->partial_rows < 0 ||
@@ -160,6 +161,7 @@ int attn_common(const char* fn, int32_t want_kind, const void* q, const void* k_
                                seq_lens, cu_seqlens_q, num_q_heads, num_kv_heads, head_dim, scale,
                                plan, info->grid, info->n_shared_items + info->n_tile_items,
                                info->n_groups, (info->variant & kVariantWideRows) != 0,
+                               (info->variant & kVariantTail) != 0,
                                partial_rows,
                                workspace, out, lse, st, ev_start, ev_stop);
   }
@@ -237,7 +239,7 @@ int pa_stage_upload(void* dst, const void* src, int64_t bytes, void* stream) {
       const int32_t *block_table, int32_t max_blocks_per_seq, const int32_t *seq_lens,          \
       const int32_t *cu_seqlens_q, int32_t n_seqs, int32_t total_q, int32_t num_q_heads,        \
       int32_t num_kv_heads, int32_t head_dim, int32_t block_size, float scale, int32_t dtype,   \
-      const int32_t *plan, const pa_plan_info *info, void *workspace, size_t workspace_bytes,   \
+      int32_t *plan, const pa_plan_info *info, void *workspace, size_t workspace_bytes,         \
       void *out, float *lse, void *stream
 #define PA_ATTN_PASS                                                                            \
   q, k_cache, v_cache, num_blocks, block_table, max_blocks_per_seq, seq_lens, cu_seqlens_q,     \
@@ -259,7 +261,7 @@ int pa_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cac
                            int32_t max_blocks_per_seq, const int32_t* seq_lens,
                            const int32_t* cu_seqlens_q, int32_t n_seqs, int32_t total_q,
                            int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                           int32_t block_size, float scale, int32_t dtype, const int32_t* plan,
+                           int32_t block_size, float scale, int32_t dtype, int32_t* plan,
                            const pa_plan_info* info, void* out, float* lse, void* stream) {
   return pa::attn_common("pa_attn_decode_noalloc", PA_KIND_DECODE, q, k_cache, v_cache,
                          num_blocks, block_table, max_blocks_per_seq, seq_lens, cu_seqlens_q,

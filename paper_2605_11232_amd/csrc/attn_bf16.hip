@@ -724,9 +724,11 @@ __device__ __forceinline__ void row_item(const int32_t* it, int g, int poff, con
 }
 
 // MIX bits: 1 = tile and shared items, 2 = row items of at most 16 rows,
-// 4 = row items of up to 32 rows.  Separate instantiations keep a pure
-// prefill or pure decode launch from paying the other paths' registers and
-// LDS; a launch with only 16-row row items runs at three waves per SIMD.
+// 4 = row items of up to 32 rows, 8 = wildcard workgroups (tail lists).
+// Separate instantiations keep a pure prefill or pure decode launch from
+// paying the other paths' registers and LDS, and a plan without tail lists
+// from paying for the wildcard loop; a launch with only 16-row row items
+// runs at three waves per SIMD.
 template <int MIX>
 constexpr int waves_per_eu() { return MIX == 2 ? 3 : kTileWavesPerEu; }
 
@@ -743,6 +745,77 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_e
   const int poff = g * plan[H_HEAD_PARTIAL];  // the kv-head's partial rows
   if constexpr (MIX & 1) {
     __shared__ TileSmem<D, kTileSub> sm;
+    if constexpr ((MIX & 8) != 0) {
+    if (ti == kWildcard) {
+      // Take tail items (full tiles) from this XCD queue's list, then from
+      // the other queues' lists while any has items left.  Each list has its
+      // own counter in the plan (device-scope atomics, one cache line each);
+      // the last wildcard workgroup to finish resets them, so the plan serves
+      // the next call on the stream as uploaded.
+      __shared__ int claim_sh;
+      uint32_t* ctr = reinterpret_cast<uint32_t*>(const_cast<int32_t*>(plan)) + plan[H_CTR_OFF];
+      const int32_t* tab = plan + plan[H_TAIL_OFF];
+      const int32_t* tiles = plan + plan[H_TILE_OFF] - n_shared * kItemWords;
+      const int home = blockIdx.x % kXcdQueues;  // the XCD queue this workgroup runs in
+      // next item of list q, or past its end (every thread calls this)
+      auto claim = [&](int q) {
+        if (threadIdx.x == 0)
+          claim_sh = int(__hip_atomic_fetch_add(ctr + q * kCounterWords, 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT));
+        __syncthreads();  // also: every wavefront is done with the previous item's LDS
+        const int c = __builtin_amdgcn_readfirstlane(claim_sh);
+        __syncthreads();  // claim_sh is written again next round
+        return c;
+      };
+      auto run = [&](int q, int c) {
+        const int tw = plan[tab[q] + c];
+        const int tg = tw >> kDispatchHeadShift;
+        tile_item<D, kTileSub, false, true>(tiles + (tw & kDispatchIndexMask) * kItemWords, tg,
+                                            tg * plan[H_HEAD_PARTIAL], a, sm);
+      };
+      for (;;) {
+        const int c = claim(home);
+        if (c >= tab[kXcdQueues + home]) break;
+        run(home, c);
+      }
+      // Other lists: one round trip reads their counters (lanes of the first
+      // wavefront, atomic reads at the same coherence point as the claims)
+      // and picks the first, in queue order after this one, with items left.
+      // Every claim advances a counter, so the loop ends; the bound is a
+      // second guarantee.
+      for (int round = 0; round <= plan[H_N_TAIL] + kXcdQueues; ++round) {
+        if (threadIdx.x < 64) {
+          const int l = threadIdx.x;
+          const int q = home + 1 + l < kXcdQueues ? home + 1 + l : home + 1 + l - kXcdQueues;
+          bool left = false;
+          if (l < kXcdQueues - 1)
+            left = int(__hip_atomic_fetch_add(ctr + q * kCounterWords, 0u, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT)) < tab[kXcdQueues + q];
+          const uint64_t m = __ballot(left);
+          if (l == 0) {
+            const int f = m ? __builtin_ctzll(m) : -1;
+            claim_sh = f < 0 ? -1 : (home + 1 + f) % kXcdQueues;
+          }
+        }
+        __syncthreads();
+        const int q = __builtin_amdgcn_readfirstlane(claim_sh);
+        __syncthreads();
+        if (q < 0) break;
+        const int c = claim(q);
+        if (c < tab[kXcdQueues + q]) run(q, c);
+      }
+      uint32_t* done = ctr + kXcdQueues * kCounterWords;
+      if (threadIdx.x == 0 &&
+          __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 ==
+              uint32_t(plan[H_N_WILD])) {
+        // every other wildcard workgroup has made its last claims
+        for (int q = 0; q <= kXcdQueues; ++q)
+          __hip_atomic_exchange(ctr + q * kCounterWords, 0u, __ATOMIC_RELAXED,
+                                __HIP_MEMORY_SCOPE_AGENT);
+      }
+      return;
+    }
+    }
     if (ti < n_shared) {
       const int32_t* it = plan + plan[H_SHARED_OFF] + ti * kSharedWords;
       if (it[S_NROWS] > kTileRows - 32) tile_item<D, kTileSub, true, true>(it, g, poff, a, sm);
@@ -860,8 +933,8 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
                      const int32_t* bt, int32_t max_blocks, const int32_t* seq_lens,
                      const int32_t* cu_q, int32_t hq, int32_t hkv, int32_t d, float scale,
                      const int32_t* plan, int32_t grid, int32_t n_tile, int32_t n_groups,
-                     bool wide_rows, int64_t partial_rows, void* ws, void* out, float* lse,
-                     hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                     bool wide_rows, bool tail, int64_t partial_rows, void* ws, void* out,
+                     float* lse, hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
   AttnArgs a;
   a.q = static_cast<const __bf16*>(q);
   a.kc = static_cast<const __bf16*>(kc);
@@ -884,7 +957,7 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
     // tiles and rows together: the tile path's register budget holds the
     // wide row path too
     const bool rows = grid > n_tile;
-    const int mix = n_tile == 0 ? (wide_rows ? 6 : 2) : (rows ? 7 : 1);
+    const int mix = (n_tile == 0 ? (wide_rows ? 6 : 2) : (rows ? 7 : 1)) | (tail ? 8 : 0);
     // the caller's timing events ride on the dispatches (start on the first
     // kernel, stop on the last): no event packets between the kernels
     hipEvent_t stop_here = n_groups > 0 ? nullptr : ev_stop;
@@ -896,6 +969,8 @@ int launch_attn_bf16(const void* q, const void* kc, const void* vc, int32_t num_
     case 1: PA_LAUNCH(DD, 1); break;         \
     case 2: PA_LAUNCH(DD, 2); break;         \
     case 6: PA_LAUNCH(DD, 6); break;         \
+    case 9: PA_LAUNCH(DD, 9); break;         \
+    case 15: PA_LAUNCH(DD, 15); break;       \
     default: PA_LAUNCH(DD, 7); break;        \
   }
     if (d == 128) {

@@ -31,7 +31,9 @@
 // tail, tile items grouped by sequence (each sequence's keys are re-read from
 // L2 by its tiles running together).  The dispatch list is the queues
 // interleaved segment by segment: shared items, then tile items with the row
-// quads spread evenly among them.
+// quads spread evenly among them.  The last full tiles in that order form a
+// tail list that wildcard workgroups take at run time from whichever XCD
+// gets to them first.
 #include <algorithm>
 #include <array>
 #include <climits>
@@ -49,6 +51,7 @@ constexpr int64_t kRowWavesPerCu = 16;      // row-item split target
 constexpr int64_t kPrivateTileKeys = 4160;  // most private keys a few-row tile item covers
 constexpr int64_t kMinRowKeys = 256;        // split target floor of row items
 constexpr int64_t kTailWorkPct = 10;        // row work given half-length items (per cent)
+constexpr int64_t kStealPct = 5;            // tile work in the tail list (per cent)
 
 using Rec = std::array<int32_t, pa::kItemWords>;
 
@@ -207,6 +210,8 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   // run over the shared, tile and row templates in that order (a row
   // workgroup names the first of its four row templates)
   std::vector<Ref> dispatch;
+  // per XCD queue, the tile items wildcard workgroups take at run time
+  std::array<std::vector<Ref>, pa::kXcdQueues> tail;
   int64_t n_shared_wg = 0, n_tile_wg = 0, n_quads = 0;
 
   if (dtype == PA_BF16) {
@@ -490,6 +495,35 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
       interleave(dispatch, shared_q);
       interleave(dispatch, body);
     }
+    // Tail stealing: the XCDs run at slightly different speeds (equal work
+    // ends up to ~7 % apart), which no static order can know.  The last
+    // plain full-tile items in dispatch order, kStealPct of the tile work,
+    // move to the tail list of their XCD queue, in dispatch order, and their
+    // dispatch slots become wildcards that take tail items until none is
+    // left anywhere: XCDs that run ahead take over the others' last items.
+    static_assert(pa::kXcdQueues == kXcds, "one tail list per XCD queue");
+    if (kStealPct > 0) {
+      const int32_t t_lo = int32_t(t_shared.size()), t_hi = t_lo + int32_t(t_tiles.size());
+      auto stealable = [&](const Ref& r) {
+        if (r.second < t_lo || r.second >= t_hi) return false;
+        const Rec& t = t_tiles[r.second - t_lo];
+        return t[pa::I_NROWS] > pa::kTileRows - 32 && t[pa::I_FLAGS] == 0;
+      };
+      int64_t total = 0;
+      for (const auto& r : dispatch)
+        if (stealable(r)) total += tile_cost[r.second - t_lo];
+      const int64_t budget = total * kStealPct / 100;
+      int64_t acc = 0;
+      for (size_t b = dispatch.size(); b-- > 0 && acc < budget;) {
+        if (!stealable(dispatch[b])) continue;
+        acc += tile_cost[dispatch[b].second - t_lo];
+        tail[b % kXcds].push_back(dispatch[b]);
+        dispatch[b] = {0, pa::kWildcard};
+      }
+      // the walk ran backwards: each list back in dispatch order (a
+      // sequence's tiles together, the longest sequences first)
+      for (auto& l : tail) std::reverse(l.begin(), l.end());
+    }
   }
 
   const int64_t partial_rows = head_partial * num_kv_heads;
@@ -498,9 +532,14 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   const int64_t head_members = int64_t(t_members.size());
   const int64_t grid = dtype == PA_F32 ? int64_t(total_q) * num_q_heads
                                        : int64_t(dispatch.size());
-  // layout: header, dispatch list, templates (shared, tile, row, group), member table
+  // layout: header, dispatch list, tail table and lists, counters,
+  // templates (shared, tile, row, group), member table
   const int64_t dispatch_off = pa::kHeaderWords;
-  const int64_t shared_off = dispatch_off + (dtype == PA_F32 ? 0 : grid);
+  int64_t n_tail = 0;
+  for (const auto& l : tail) n_tail += int64_t(l.size());
+  const int64_t tail_off = dispatch_off + (dtype == PA_F32 ? 0 : grid);
+  const int64_t ctr_off = tail_off + (n_tail ? 2 * pa::kXcdQueues + n_tail : 0);
+  const int64_t shared_off = ctr_off + (n_tail ? pa::kCounterBlockWords : 0);
   const int64_t tile_off = shared_off + int64_t(t_shared.size()) * pa::kSharedWords;
   const int64_t row_off = tile_off + int64_t(t_tiles.size()) * pa::kItemWords;
   const int64_t group_off = row_off + int64_t(sorted_rows.size()) * pa::kItemWords;
@@ -508,7 +547,7 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   const int64_t words = member_off + head_members;
   if (dtype == PA_BF16 &&
       (num_kv_heads >= (1 << (31 - pa::kDispatchHeadShift)) ||
-       t_shared.size() + t_tiles.size() + sorted_rows.size() > size_t(pa::kDispatchIndexMask)))
+       t_shared.size() + t_tiles.size() + sorted_rows.size() >= size_t(pa::kWildcard)))
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: launch too large");
   if (words >= (int64_t{1} << 31) || grid >= (int64_t{1} << 31) || partial_rows >= (int64_t{1} << 31))
     return pa::fail(PA_ERR_ARG, "pa_attn_plan: launch too large");
@@ -524,7 +563,9 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   info->grid = int32_t(grid);
   bool wide = false;
   for (const auto& it : t_rows) wide = wide || it[pa::I_NROWS] > 16;
-  info->variant = dtype == PA_F32 ? 0 : (pa::kVariantBf16 | (wide ? pa::kVariantWideRows : 0));
+  info->variant = dtype == PA_F32 ? 0
+                                  : (pa::kVariantBf16 | (wide ? pa::kVariantWideRows : 0) |
+                                     (n_tail ? pa::kVariantTail : 0));
   info->plan_words = words;
   info->workspace_bytes = partial_rows * int64_t(head_dim + 1) * int64_t(sizeof(float));
   info->n_seqs = n_seqs;
@@ -564,10 +605,25 @@ extern "C" int pa_attn_plan(int32_t kind, int32_t n_q, int32_t n_seqs, const int
   h[pa::H_N_TILE_TMPL] = int32_t(t_tiles.size());
   h[pa::H_N_ROW_TMPL] = int32_t(sorted_rows.size());
   h[pa::H_N_GROUP_TMPL] = int32_t(t_groups.size());
+  h[pa::H_TAIL_OFF] = int32_t(tail_off);
+  h[pa::H_N_TAIL] = int32_t(n_tail);
+  h[pa::H_N_WILD] = int32_t(n_tail);  // one wildcard per tail item
+  h[pa::H_CTR_OFF] = int32_t(ctr_off);
   if (dtype == PA_BF16) {
     int32_t* p = plan + dispatch_off;
     auto word = [](const Ref& r) { return (r.first << pa::kDispatchHeadShift) | r.second; };
     for (const auto& r : dispatch) *p++ = word(r);
+    if (n_tail) {
+      // tail table (list offsets, then lengths), the lists, zeroed counters
+      int32_t* tab = p;
+      p += 2 * pa::kXcdQueues;
+      for (int q = 0; q < pa::kXcdQueues; ++q) {
+        tab[q] = int32_t(p - plan);
+        tab[pa::kXcdQueues + q] = int32_t(tail[q].size());
+        for (const auto& r : tail[q]) *p++ = word(r);
+      }
+      std::fill(p, p + pa::kCounterBlockWords, 0);
+    }
     p = plan + shared_off;
     for (const auto& t : t_shared) {
       std::copy(t.begin(), t.end(), p);

@@ -45,10 +45,29 @@ enum : int32_t {
   H_N_TILE_TMPL,
   H_N_ROW_TMPL,
   H_N_GROUP_TMPL,
-  kHeaderWords = 24
+  H_TAIL_OFF,      // word offset of the tail table: kXcdQueues list offsets, then lengths
+                   // (each list in dispatch order)
+  H_N_TAIL,        // tile items in all tail lists
+  H_N_WILD,        // wildcard workgroups (dispatch words kWildcard), one per tail item
+  H_CTR_OFF,       // word offset of the counters (kCounterWords apart; zero in a fresh plan)
+  H_PAD28, H_PAD29, H_PAD30, H_PAD31,
+  kHeaderWords = 32
 };
 constexpr int32_t kDispatchHeadShift = 24;  // template index < 2^24 (all kinds), kv-head < 2^7
 constexpr int32_t kDispatchIndexMask = (1 << kDispatchHeadShift) - 1;
+// Dispatch word of a wildcard workgroup: it takes tile items one at a time
+// from the tail list of its own XCD queue (workgroup b runs on XCD
+// b % kXcdQueues), then from the other queues' lists in turn, each list
+// claimed through its own device-scope counter, until none is left: XCDs
+// that run ahead finish the work of the ones that fall behind, and an XCD
+// reads other kv-heads' keys only for the items it takes over at the end.
+// Counter q (claims of list q) is at word H_CTR_OFF + q * kCounterWords, the
+// count of finished wildcard workgroups after them; the last wildcard
+// workgroup resets them all to zero.
+constexpr int32_t kWildcard = kDispatchIndexMask;
+constexpr int32_t kXcdQueues = 8;
+constexpr int32_t kCounterWords = 32;  // one 128-byte line per counter
+constexpr int32_t kCounterBlockWords = (kXcdQueues + 1) * kCounterWords;
 
 // Work item (tile or row item; templates hold kvh = 0): rows [row0, row0 +
 // nrows) of sequence seq's packed (query, head-in-group) rows for kv-head
@@ -85,9 +104,11 @@ enum : int32_t {
 };
 
 // pa_plan_info.variant: 0 float32 kernel; bf16 plans 1, plus 2 when some
-// row item holds more than 16 rows (selects the wide row-item kernel).
+// row item holds more than 16 rows (selects the wide row-item kernel), plus 4
+// when the plan has tail lists (selects a kernel with wildcard workgroups).
 constexpr int32_t kVariantBf16 = 1;
 constexpr int32_t kVariantWideRows = 2;
+constexpr int32_t kVariantTail = 4;
 
 constexpr int32_t kTileRows = 128;    // rows per tile item (4 waves x 32)
 constexpr int32_t kRowItemRows = 32;  // rows per single-wave item (two 16-column MFMA tiles)

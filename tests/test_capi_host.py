@@ -4,6 +4,7 @@ block tables, slot mappings and prefix-hit counts as the oracle, bit for bit;
 error paths leave the pool unchanged.  Device entry points are only called
 with arguments that fail host validation (nothing is launched)."""
 import ctypes
+import itertools
 import os
 import re
 
@@ -200,12 +201,26 @@ H_N_SHARED, H_N_TILE, H_N_ROW, H_N_GROUPS, H_GRID = 2, 3, 4, 5, 6
 H_SHARED_OFF, H_TILE_OFF, H_ROW_OFF, H_GROUP_OFF, H_MEMBER_OFF, H_PARTIAL_ROWS = 12, 13, 14, 15, 16, 17
 H_DISPATCH_OFF, H_HEAD_PARTIAL, H_HKV = 18, 19, 8
 H_N_SHARED_TMPL, H_N_TILE_TMPL, H_N_ROW_TMPL, H_N_GROUP_TMPL = 20, 21, 22, 23
+H_TAIL_OFF, H_N_TAIL, H_N_WILD, H_CTR_OFF = 24, 25, 26, 27
+HEADER_WORDS = 32
+XCD_QUEUES, COUNTER_WORDS = 8, 32
 HEAD_SHIFT = 24           # dispatch word: (kv-head << 24) | template index
+WILDCARD = (1 << HEAD_SHIFT) - 1   # template index of a wildcard workgroup
 STREAM_FLAG = 1           # item flags word: no other item reads the item's keys
 WAVES = 4                 # wavefronts per workgroup: row items come WAVES to a workgroup
 TILE_ROWS = 32 * WAVES    # rows of a tile or shared item (32 per wavefront)
 ROW_ITEM_ROWS = 32        # rows of a row item (two 16-column MFMA tiles)
 VARIANT_WIDE_ROWS = 2     # plan info variant bit: some row item has more than 16 rows
+VARIANT_TAIL = 4          # plan info variant bit: the plan has tail lists (wildcard workgroups)
+
+
+def tail_lists(plan):
+    """The tail list of each XCD queue (dispatch words), from the tail table."""
+    h = plan[:HEADER_WORDS]
+    if not h[H_N_TAIL]:
+        return [[] for _ in range(XCD_QUEUES)]
+    tab = plan[h[H_TAIL_OFF]:h[H_TAIL_OFF] + 2 * XCD_QUEUES]
+    return [plan[tab[q]:tab[q] + tab[XCD_QUEUES + q]].tolist() for q in range(XCD_QUEUES)]
 
 
 def parse_plan(plan):
@@ -213,15 +228,25 @@ def parse_plan(plan):
     kv-head-0 templates: shared items as (member table, kvh, row0, nrows,
     kv0, kv1, rows per member, block sequence, partial offset), tile and row
     items and merge groups with their kv-head and partial rows stamped."""
-    h = plan[:24]
-    assert h[H_DISPATCH_OFF] == 24   # the dispatch list follows the header
+    h = plan[:HEADER_WORDS]
+    assert h[H_DISPATCH_OFF] == HEADER_WORDS   # the dispatch list follows the header
     hp = int(h[H_HEAD_PARTIAL])
     tmpl = lambda off, n: plan[off:off + 8 * n].reshape(-1, 8).tolist()
     ts, tt = tmpl(h[H_SHARED_OFF], h[H_N_SHARED_TMPL]), tmpl(h[H_TILE_OFF], h[H_N_TILE_TMPL])
     tr, tg = tmpl(h[H_ROW_OFF], h[H_N_ROW_TMPL]), tmpl(h[H_GROUP_OFF], h[H_N_GROUP_TMPL])
     disp = plan[h[H_DISPATCH_OFF]:h[H_DISPATCH_OFF] + h[H_GRID]].tolist()
     assert all(w >= 0 for w in disp)
-    split = [(w >> HEAD_SHIFT, w & ((1 << HEAD_SHIFT) - 1)) for w in disp]
+    # wildcard workgroups take the tail lists' tile items at run time: one
+    # wildcard per tail item, the table and lists right after the dispatch
+    # list, then the counters, zero
+    tail = sum(tail_lists(plan), [])
+    if h[H_N_TAIL]:
+        assert h[H_TAIL_OFF] == h[H_DISPATCH_OFF] + h[H_GRID]
+        assert h[H_CTR_OFF] == h[H_TAIL_OFF] + 2 * XCD_QUEUES + h[H_N_TAIL]
+        assert not plan[h[H_CTR_OFF]:h[H_CTR_OFF] + (XCD_QUEUES + 1) * COUNTER_WORDS].any()
+    assert disp.count(WILDCARD) == h[H_N_WILD] == len(tail) == h[H_N_TAIL]
+    split = [(w >> HEAD_SHIFT, w & ((1 << HEAD_SHIFT) - 1)) for w in disp if w != WILDCARD]
+    split += [(w >> HEAD_SHIFT, w & ((1 << HEAD_SHIFT) - 1)) for w in tail]
     # template indices run over the shared, tile and row templates in order
     n_st, n_tt = h[H_N_SHARED_TMPL], h[H_N_TILE_TMPL]
     s_split = [(g, i) for g, i in split if i < n_st]
@@ -264,6 +289,7 @@ def check_plan(plan, info, L, cu, G, hkv, D=128):
             writes[pr] = writes.get(pr, 0) + 1
     assert h[H_N_ROW] % WAVES == 0
     assert bool(info.variant & VARIANT_WIDE_ROWS) == any(t[3] > 16 for t in rows if t[0] >= 0)
+    assert bool(info.variant & VARIANT_TAIL) == (h[H_N_TAIL] > 0)
     assert all(0 < t[3] <= TILE_ROWS for t in tiles) and all(0 < t[3] <= TILE_ROWS for t in shared)
     assert all(t[3] <= ROW_ITEM_ROWS for t in rows if t[0] >= 0)
     # a row item's block ids are one 64-lane load: at most 64 blocks of 16 keys
@@ -372,9 +398,10 @@ def test_dispatch_keeps_kv_heads_on_their_xcds(name):
     g (mod Hkv) only, segment after segment of the dispatch list."""
     plan, info, md, cfg = _workload_plan(name, 0.25)
     hkv = cfg.num_kv_heads
-    disp = plan[24:24 + info.grid]
-    heads = disp >> HEAD_SHIFT
-    xcd = np.arange(info.grid) % 8
+    disp = plan[HEADER_WORDS:HEADER_WORDS + info.grid]
+    fixed = disp != WILDCARD   # wildcards take tail items on whichever XCD runs them
+    heads = disp[fixed] >> HEAD_SHIFT
+    xcd = np.arange(info.grid)[fixed] % 8
     assert np.array_equal(xcd % hkv, heads % 8 if hkv >= 8 else heads)
     check_plan(plan, info, md["seq_lens"], md["cu_seqlens_q"], cfg.group, hkv)
 
@@ -778,3 +805,48 @@ def test_noalloc_decode_rejects_before_launching():
     info.total_q = 2
     assert lib.pa_attn_decode_noalloc(*args) == B.PA_ERR_ARG
     assert b"plan was built for" in lib.pa_last_error()
+
+
+@pytest.mark.parametrize("name", ["prefill", "mixed", "decode", "verify"])
+def test_tail_lists_hold_last_full_tiles(name):
+    """Prefill and mixed: the last plain full tiles in dispatch order, about
+    5 % of the tile work, move to the tail list of their XCD queue
+    (workgroup b runs on XCD b % 8), still in dispatch order (a sequence's
+    tiles together), and their slots hold wildcards, as many per queue as its
+    list has items; decode and verify have no such tiles, so no tail."""
+    plan, info, md, cfg = _workload_plan(name, 0.25)
+    h = plan[:HEADER_WORDS]
+    disp = plan[HEADER_WORDS:HEADER_WORDS + info.grid]
+    lists = tail_lists(plan)
+    n_st = int(h[H_N_SHARED_TMPL])
+    tt = plan[h[H_TILE_OFF]:h[H_TILE_OFF] + 8 * h[H_N_TILE_TMPL]].reshape(-1, 8)
+    if name in ("decode", "verify"):
+        assert h[H_N_TAIL] == 0 and not (disp == WILDCARD).any()
+        return
+    assert h[H_N_TAIL] > 0
+    wild = disp == WILDCARD
+    total_tail = 0
+    for q, lst in enumerate(lists):
+        assert len(lst) == int(wild[q::XCD_QUEUES].sum())
+        if not lst:
+            continue
+        t = tt[(np.array(lst) & WILDCARD) - n_st]
+        assert (t[:, 3] > 96).all() and (t[:, 7] == 0).all()   # full tiles, not streamed
+        cost = t[:, 5].astype(np.int64) * t[:, 3]
+        seqs = [k for k, _ in itertools.groupby(t[:, 0].tolist())]
+        assert len(seqs) == len(set(seqs))                        # a sequence's tiles together
+        # a queue's items keep their kv-heads: the XCD's own heads
+        heads = np.array(lst) >> HEAD_SHIFT
+        fixed_heads = disp[q::XCD_QUEUES][~wild[q::XCD_QUEUES]] >> HEAD_SHIFT
+        assert set(heads.tolist()) <= set(fixed_heads.tolist())
+        total_tail += int(cost.sum())
+    is_full = np.array([w != WILDCARD and n_st <= (w & WILDCARD) < n_st + len(tt)
+                        and tt[(w & WILDCARD) - n_st][3] > 96 and tt[(w & WILDCARD) - n_st][7] == 0
+                        for w in disp])
+    fixed_cost = sum(int(tt[(w & WILDCARD) - n_st][5]) * int(tt[(w & WILDCARD) - n_st][3])
+                     for w in disp[is_full])
+    frac = total_tail / (total_tail + fixed_cost)
+    assert 0.05 <= frac < 0.06
+    # every wildcard sits after the last fixed full tile of the dispatch order
+    assert np.flatnonzero(wild).min() > np.flatnonzero(is_full).max()
+    check_plan(plan, info, md["seq_lens"], md["cu_seqlens_q"], cfg.group, cfg.num_kv_heads)
