@@ -144,7 +144,9 @@ def run_workload(name, W, K, C, cpu_budget, profile=False, settle_ms=0.0):
     wl = synth.workload(name, steps=W + K + C + 2)
     cfg = wl.cfg
     dev = DeviceReplay(wl).setup()
-    launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K + C)]
+    # one launch more than the steps: the host side of the step after the
+    # timed ones runs inside the timed region (see there)
+    launches = [wl.step(s) if wl.step else wl.launches[0] for s in range(W + K + C + 1)]
     # pack each step's token batches (input marshalling) before timing
     for ln in launches:
         marshal_launch(ln)
@@ -165,14 +167,22 @@ def run_workload(name, W, K, C, cpu_budget, profile=False, settle_ms=0.0):
     state = {"scrub": None}
     scrub_sink = []
 
-    def step(s, record=None):
+    def host(s, record=None):
+        # the host side of step s: pool operations, metadata and plan into
+        # its pinned staging buffer
+        share = record is not None and state["scrub"] is None
+        return dev.prepare_staged(launches[s], stagings[s % 2], q, k_new, v_new, out, lse,
+                                  guard=record[0] if share else None, upload=False)
+
+    def step(s, record=None, p=None):
         # A timed step's attention call carries its start and stop events on
         # its first and last kernel dispatches (no event packets between the
         # kernels); in a warm-cache step the start event also releases the
-        # staging buffer, so the step records no event of its own.
-        share = record is not None and state["scrub"] is None
-        p = dev.prepare_staged(launches[s], stagings[s % 2], q, k_new, v_new, out, lse,
-                               guard=record[0] if share else None)
+        # staging buffer, so the step records no event of its own.  p: its
+        # host side, when that already ran.
+        if p is None:
+            p = host(s, record)
+        dev.upload(p)
         if s == 0 and record is None:
             # KV memory of the live batch: blocks versus contiguous reservations
             # of the block-table capacity (outside the timed steps)
@@ -224,12 +234,26 @@ def run_workload(name, W, K, C, cpu_budget, profile=False, settle_ms=0.0):
             settle_s = time.perf_counter() - t_s
     for s in range(W):
         p = step(s)
+    # The host side of each step overlaps the device work of the step before
+    # (the pinned staging buffers alternate).  The barrier before the timed
+    # steps drains that pipeline, so the first timed step's host side runs
+    # before it, as it would have during the step before, and the host side
+    # of the step after the timed ones runs inside the timed region, as it
+    # would during the last one (its pool operations are rolled back after
+    # the region): the region holds exactly K steps of host work and K of
+    # device work, as a K-step stretch of the running pipeline does.
+    p = host(W, events[0]) if K else None
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
-        p = step(W + i, events[i])
+        p = step(W + i, events[i], p)
+        p_next = host(W + i + 1, events[i + 1] if i + 1 < K else None)
+        if i + 1 < K:
+            p = p_next
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    if K:
+        dev.finish(launches[W + K], batched=True)  # the prepared, never-run step
     gc.enable()
     gc.unfreeze()
     meta = {k: np.array(v, copy=True) for k, v in p.meta.items()}

@@ -221,7 +221,7 @@ class DeviceReplay:
             n_cached=dict(self.n_cached))
 
     def prepare_staged(self, launch, st: Staging, q, k_new, v_new, out, lse,
-                       guard=None) -> Prepared:
+                       guard=None, upload: bool = True) -> Prepared:
         """Like ``prepare`` but through a preallocated pinned/device staging
         pair: one library call applies the launch's pool operations and
         writes its metadata and plan into the pinned buffer, one
@@ -234,7 +234,11 @@ class DeviceReplay:
         caller passes ``guard`` (an event it wants on the stream anyway, such
         as the start of a timed attention call), that event, recorded by
         ``append`` after the KV append.  Each event record is a marker in the
-        stream that idles the device for a few microseconds."""
+        stream that idles the device for a few microseconds.
+
+        With upload=False only the host side runs (the pool operations,
+        metadata and plan into the pinned buffer); ``upload`` then puts the
+        upload on the stream, before the launch's kernels."""
         batched, inp = marshal_launch(launch)
         cfg = self.cfg
         n, T = inp.n, inp.total_q
@@ -245,18 +249,6 @@ class DeviceReplay:
                                         cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
                                         self.dcode, self.num_cus, self.cascade, info=st.info)
         self.n_cached = batched["pre"].admitted()
-        # one copy: everything up to the end of the plan
-        used = st.plan_off + int(info.plan_words)
-        if self.stage_kernel:
-            B.stage_upload(st.dev, st.host, 4 * used)
-        else:
-            st.dev[:used].copy_(st.host[:used], non_blocking=True)
-        if guard is None:
-            st.ready.record()
-            st.guard = st.ready
-        else:
-            st.guard = guard
-        st.used = True
         ws = None
         if info.workspace_bytes:
             if self._ws is None or self._ws.numel() < int(info.workspace_bytes):
@@ -264,11 +256,30 @@ class DeviceReplay:
                                        device=self.device)
             ws = self._ws
         bt, sl, cu, slots = st.device_views(n, T)
-        return Prepared(
+        p = Prepared(
             kind=kind, meta=st.buffers.meta(n, T), info=info,
             plan_host=st.buffers.plan[:int(info.plan_words)], block_table=bt, seq_lens=sl,
             cu=cu, slots=slots, plan=st.plan[1], q=q, k_new=k_new, v_new=v_new, ws=ws, out=out,
-            lse=lse, n_cached=self.n_cached, guard=guard)
+            lse=lse, n_cached=self.n_cached, guard=guard, staging=st)
+        if upload:
+            self.upload(p)
+        return p
+
+    def upload(self, p: Prepared):
+        """Put the upload of a staged launch's metadata and plan on the
+        stream (one copy, everything up to the end of the plan)."""
+        st = p.staging
+        used = st.plan_off + int(p.info.plan_words)
+        if self.stage_kernel:
+            B.stage_upload(st.dev, st.host, 4 * used)
+        else:
+            st.dev[:used].copy_(st.host[:used], non_blocking=True)
+        if p.guard is None:
+            st.ready.record()
+            st.guard = st.ready
+        else:
+            st.guard = p.guard
+        st.used = True
 
     def append(self, p: Prepared, stream=None, record_guard: bool = True):
         """KV append of the launch; records the caller's staging guard after
