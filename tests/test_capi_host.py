@@ -850,3 +850,14 @@ def test_tail_lists_hold_last_full_tiles(name):
     # every wildcard sits after the last fixed full tile of the dispatch order
     assert np.flatnonzero(wild).min() > np.flatnonzero(is_full).max()
     check_plan(plan, info, md["seq_lens"], md["cu_seqlens_q"], cfg.group, cfg.num_kv_heads)
+
+
+def test_set_launch_events_without_a_gpu():
+    """pa_set_launch_events only stores the two handles for the calling
+    thread's next attention call: it touches no device, accepts NULLs and
+    reports success."""
+    L = B.lib()
+    assert L.pa_set_launch_events(None, None) == B.PA_OK
+    assert L.pa_set_launch_events(ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000)) == B.PA_OK
+    # clear them again, so nothing on this thread carries stale handles
+    assert L.pa_set_launch_events(None, None) == B.PA_OK
