@@ -858,6 +858,8 @@ def test_set_launch_events_without_a_gpu():
     reports success."""
     L = B.lib()
     assert L.pa_set_launch_events(None, None) == B.PA_OK
-    assert L.pa_set_launch_events(ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000)) == B.PA_OK
-    # clear them again, so nothing on this thread carries stale handles
-    assert L.pa_set_launch_events(None, None) == B.PA_OK
+    try:
+        assert L.pa_set_launch_events(ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000)) == B.PA_OK
+    finally:
+        # clear them again, so no later call on this thread carries these handles
+        assert L.pa_set_launch_events(None, None) == B.PA_OK
