@@ -433,29 +433,32 @@ def test_edge_cases():
         close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"verify-G{G}-{max(lens)}")
 
 
-def test_tail_stealing_plan_reuse():
-    """A prefill launch whose plan has tail lists (wildcard workgroups taking
-    full tiles through counters in the plan) matches the oracle, and runs
-    twice more on the same device plan with the same output bit for bit: the
-    last wildcard workgroup leaves the counters zero, as uploaded."""
+@pytest.mark.parametrize("name", ["prefill", "mixed"])
+def test_tail_stealing_plan_reuse(name):
+    """A launch whose plan has tail lists (wildcard workgroups taking full
+    tiles through counters in the plan) matches the oracle, and runs eight
+    more times on the same device plan with the same output bit for bit
+    (which workgroup takes which tail item changes from run to run; each
+    item's result does not): the last wildcard workgroup leaves the
+    counters zero, as uploaded."""
     _gpu()
     from paper_2605_11232_amd.runtime import DeviceReplay
     from tests.parity import TOL, close
     from oracle.run import OracleReplay
-    wl = synth.workload("prefill", scale=0.125, steps=2)
+    wl = synth.workload(name, scale=0.125, steps=2)
     o = OracleReplay(wl).setup()
     dv = DeviceReplay(wl).setup()
-    launch = wl.step(0)
-    say("[tail] prefill@0.125 launch 0")
+    launch = wl.step(0) if wl.step else wl.launches[0]
+    say(f"[tail] {name}@0.125 launch 0")
     p = dv.run(launch)
     torch.cuda.synchronize()
     h = p.plan[:32].cpu().numpy()
     n_tail, n_wild, ctr_off = int(h[25]), int(h[26]), int(h[27])
     assert n_tail > 0 and n_wild == n_tail
     ro = o.launch(launch, rows=None)
-    close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], "tail-stealing prefill")
+    close(p.out.float().cpu().numpy(), ro["out"], *TOL["bf16"], f"tail-stealing {name}")
     first = p.out.clone()
-    for k in range(2):
+    for k in range(8):
         dv.attend(p)
         torch.cuda.synchronize()
         assert torch.equal(p.out, first), f"repeat {k}"
