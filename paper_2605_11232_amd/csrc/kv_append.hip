@@ -41,8 +41,10 @@ __global__ __launch_bounds__(256) void kv_append_kernel(const T* __restrict__ k_
     const int64_t src = ((int64_t)tok * hkv + h) * D + part * E;
     u32x4 kx = zero16(), vx = zero16();
     if (s >= 0) {
-      kx = ld16(k_new + src);
-      vx = ld16(v_new + src);
+      // the new tokens' rows are read once: non-temporal loads keep them out of
+      // the caches the attention call that follows re-reads
+      kx = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(k_new + src));
+      vx = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(v_new + src));
       const int blk = s / kBlock, off = s % kBlock;
       st16(kc + ((int64_t)blk * hkv + h) * kBlock * D + key_elem(off, part * E), kx);
     }
