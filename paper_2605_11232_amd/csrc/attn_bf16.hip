@@ -746,75 +746,75 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_e
   if constexpr (MIX & 1) {
     __shared__ TileSmem<D, kTileSub> sm;
     if constexpr ((MIX & 8) != 0) {
-    if (ti == kWildcard) {
-      // Take tail items (full tiles) from this XCD queue's list, then from
-      // the other queues' lists while any has items left.  Each list has its
-      // own counter in the plan (device-scope atomics, one cache line each);
-      // the last wildcard workgroup to finish resets them, so the plan serves
-      // the next call on the stream as uploaded.
-      __shared__ int claim_sh;
-      uint32_t* ctr = reinterpret_cast<uint32_t*>(const_cast<int32_t*>(plan)) + plan[H_CTR_OFF];
-      const int32_t* tab = plan + plan[H_TAIL_OFF];
-      const int32_t* tiles = plan + plan[H_TILE_OFF] - n_shared * kItemWords;
-      const int home = blockIdx.x % kXcdQueues;  // the XCD queue this workgroup runs in
-      // next item of list q, or past its end (every thread calls this)
-      auto claim = [&](int q) {
-        if (threadIdx.x == 0)
-          claim_sh = int(__hip_atomic_fetch_add(ctr + q * kCounterWords, 1u, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT));
-        __syncthreads();  // also: every wavefront is done with the previous item's LDS
-        const int c = __builtin_amdgcn_readfirstlane(claim_sh);
-        __syncthreads();  // claim_sh is written again next round
-        return c;
-      };
-      auto run = [&](int q, int c) {
-        const int tw = plan[tab[q] + c];
-        const int tg = tw >> kDispatchHeadShift;
-        tile_item<D, kTileSub, false, true>(tiles + (tw & kDispatchIndexMask) * kItemWords, tg,
-                                            tg * plan[H_HEAD_PARTIAL], a, sm);
-      };
-      for (;;) {
-        const int c = claim(home);
-        if (c >= tab[kXcdQueues + home]) break;
-        run(home, c);
-      }
-      // Other lists: one round trip reads their counters (lanes of the first
-      // wavefront, atomic reads at the same coherence point as the claims)
-      // and picks the first, in queue order after this one, with items left.
-      // Every claim advances a counter, so the loop ends; the bound is a
-      // second guarantee.
-      for (int round = 0; round <= plan[H_N_TAIL] + kXcdQueues; ++round) {
-        if (threadIdx.x < 64) {
-          const int l = threadIdx.x;
-          const int q = home + 1 + l < kXcdQueues ? home + 1 + l : home + 1 + l - kXcdQueues;
-          bool left = false;
-          if (l < kXcdQueues - 1)
-            left = int(__hip_atomic_fetch_add(ctr + q * kCounterWords, 0u, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT)) < tab[kXcdQueues + q];
-          const uint64_t m = __ballot(left);
-          if (l == 0) {
-            const int f = m ? __builtin_ctzll(m) : -1;
-            claim_sh = f < 0 ? -1 : (home + 1 + f) % kXcdQueues;
-          }
+      if (ti == kWildcard) {
+        // Take tail items (full tiles) from this XCD queue's list, then from
+        // the other queues' lists while any has items left.  Each list has its
+        // own counter in the plan (device-scope atomics, one cache line each);
+        // the last wildcard workgroup to finish resets them, so the plan serves
+        // the next call on the stream as uploaded.
+        __shared__ int claim_sh;
+        uint32_t* ctr = reinterpret_cast<uint32_t*>(const_cast<int32_t*>(plan)) + plan[H_CTR_OFF];
+        const int32_t* tab = plan + plan[H_TAIL_OFF];
+        const int32_t* tiles = plan + plan[H_TILE_OFF] - n_shared * kItemWords;
+        const int home = blockIdx.x % kXcdQueues;  // the XCD queue this workgroup runs in
+        // next item of list q, or past its end (every thread calls this)
+        auto claim = [&](int q) {
+          if (threadIdx.x == 0)
+            claim_sh = int(__hip_atomic_fetch_add(ctr + q * kCounterWords, 1u, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT));
+          __syncthreads();  // also: every wavefront is done with the previous item's LDS
+          const int c = __builtin_amdgcn_readfirstlane(claim_sh);
+          __syncthreads();  // claim_sh is written again next round
+          return c;
+        };
+        auto run = [&](int q, int c) {
+          const int tw = plan[tab[q] + c];
+          const int tg = tw >> kDispatchHeadShift;
+          tile_item<D, kTileSub, false, true>(tiles + (tw & kDispatchIndexMask) * kItemWords, tg,
+                                              tg * plan[H_HEAD_PARTIAL], a, sm);
+        };
+        for (;;) {
+          const int c = claim(home);
+          if (c >= tab[kXcdQueues + home]) break;
+          run(home, c);
         }
-        __syncthreads();
-        const int q = __builtin_amdgcn_readfirstlane(claim_sh);
-        __syncthreads();
-        if (q < 0) break;
-        const int c = claim(q);
-        if (c < tab[kXcdQueues + q]) run(q, c);
+        // Other lists: one round trip reads their counters (lanes of the first
+        // wavefront, atomic reads at the same coherence point as the claims)
+        // and picks the first, in queue order after this one, with items left.
+        // Every claim advances a counter, so the loop ends; the bound is a
+        // second guarantee.
+        for (int round = 0; round <= plan[H_N_TAIL] + kXcdQueues; ++round) {
+          if (threadIdx.x < 64) {
+            const int l = threadIdx.x;
+            const int q = home + 1 + l < kXcdQueues ? home + 1 + l : home + 1 + l - kXcdQueues;
+            bool left = false;
+            if (l < kXcdQueues - 1)
+              left = int(__hip_atomic_fetch_add(ctr + q * kCounterWords, 0u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT)) < tab[kXcdQueues + q];
+            const uint64_t m = __ballot(left);
+            if (l == 0) {
+              const int f = m ? __builtin_ctzll(m) : -1;
+              claim_sh = f < 0 ? -1 : (home + 1 + f) % kXcdQueues;
+            }
+          }
+          __syncthreads();
+          const int q = __builtin_amdgcn_readfirstlane(claim_sh);
+          __syncthreads();
+          if (q < 0) break;
+          const int c = claim(q);
+          if (c < tab[kXcdQueues + q]) run(q, c);
+        }
+        uint32_t* done = ctr + kXcdQueues * kCounterWords;
+        if (threadIdx.x == 0 &&
+            __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 ==
+                uint32_t(plan[H_N_WILD])) {
+          // every other wildcard workgroup has made its last claims
+          for (int q = 0; q <= kXcdQueues; ++q)
+            __hip_atomic_exchange(ctr + q * kCounterWords, 0u, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+        }
+        return;
       }
-      uint32_t* done = ctr + kXcdQueues * kCounterWords;
-      if (threadIdx.x == 0 &&
-          __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 ==
-              uint32_t(plan[H_N_WILD])) {
-        // every other wildcard workgroup has made its last claims
-        for (int q = 0; q <= kXcdQueues; ++q)
-          __hip_atomic_exchange(ctr + q * kCounterWords, 0u, __ATOMIC_RELAXED,
-                                __HIP_MEMORY_SCOPE_AGENT);
-      }
-      return;
-    }
     }
     if (ti < n_shared) {
       const int32_t* it = plan + plan[H_SHARED_OFF] + ti * kSharedWords;
