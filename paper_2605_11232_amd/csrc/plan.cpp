@@ -47,7 +47,7 @@
 namespace {
 
 constexpr int kXcds = 8;
-constexpr int64_t kRowWavesPerCu = 16;      // row-item split target
+constexpr int64_t kRowWavesPerCu = 10;      // row-item split target
 constexpr int64_t kPrivateTileKeys = 4160;  // most private keys a few-row tile item covers
 constexpr int64_t kMinRowKeys = 256;        // split target floor of row items
 constexpr int64_t kTailWorkPct = 10;        // row work given half-length items (per cent)

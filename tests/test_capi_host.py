@@ -439,7 +439,7 @@ def test_plan_finds_shared_prefix_of_workloads():
 def test_decode_tail_gets_half_length_items():
     """The sequences with the fewest private keys (about a tenth of the row
     work) are split with half the target length, so the shortest items run
-    last; the rest keep the full target (352 keys at full size)."""
+    last; the rest keep the full target (576 keys at full size)."""
     plan, info, md, cfg = _workload_plan("decode", 1.0)
     _, _, _, rows, _ = parse_plan(plan)
     items = [t for t in rows if t[0] >= 0 and t[1] == 0]
@@ -447,13 +447,13 @@ def test_decode_tail_gets_half_length_items():
     for t in items:
         per_seq.setdefault(t[0], []).append(t[5] - t[4])
     longest = max(max(v) for v in per_seq.values())
-    assert longest == 352
+    assert longest == 576
     private = {r: sum(v) for r, v in per_seq.items()}
-    halved = [r for r, v in per_seq.items() if max(v) <= 176 and private[r] > 352]
-    assert halved, "some multi-item sequence is split with the half target"
-    # halved sequences are among the shortest: none is longer than any
-    # sequence that kept the full target with more than one item
-    full = [r for r, v in per_seq.items() if max(v) > 176 and len(v) > 1]
+    halved = [r for r, v in per_seq.items() if max(v) <= 288 and len(v) > 1]
+    assert halved, "some sequence is split into several items with the half target"
+    # halved sequences are among the shortest: every sequence that kept
+    # full-target items is at least as long as every halved one
+    full = [r for r, v in per_seq.items() if max(v) > 288]
     assert max(private[r] for r in halved) <= min(private[r] for r in full)
     tail_work = sum(private[r] for r in halved)
     assert tail_work <= 0.1 * sum(private.values())
