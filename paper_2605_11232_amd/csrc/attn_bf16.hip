@@ -126,7 +126,7 @@ __device__ __forceinline__ float add_bf16x8(bf16x8 v, float acc) {
 }
 
 #ifndef PA_LDS_PREFETCH
-#define PA_LDS_PREFETCH 8
+#define PA_LDS_PREFETCH 3
 #endif
 // N MFMAs whose A operands are 16-byte LDS reads (addr(i) gives the address
 // of MFMA i), with PF reads in flight ahead of the MFMA that uses them: LDS
